@@ -1,0 +1,174 @@
+"""Pins of the oracle's central-difference estimator (Eq. 2, averaged over
+n_pert probes as in Section 2) and of its update (Eq. 7 / Algorithm 1)."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2505_17852_amd import workloads as wl
+
+TINY = dict(n_layers=1, vocab=8, embed=4, hidden=4, wdtype=0, probe=0)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_central_difference_exact_on_quadratic(oracle, kind):
+    """For L = 1/2 x^T A x + b^T x the even Taylor terms cancel, so
+    (L(x + eps z) - L(x - eps z)) / (2 eps) == (A x + b) . z up to rounding."""
+    rng = np.random.default_rng(3 + kind)
+    P = 64
+    M = rng.normal(size=(P, P))
+    A = M @ M.T / P
+    b = rng.normal(size=P)
+    x = rng.normal(size=P)
+    loss = lambda w: 0.5 * w @ A @ w + b @ w  # noqa: E731
+    N, eps, seed = 40, 1e-3, 77
+    lp, lm = oracle.cd_losses_generic(x, loss, kind, seed, eps, N)
+    g = A @ x + b
+    for i in range(N):
+        z = oracle.probe(kind, seed, i, 0, P).astype(np.float64)
+        d = (lp[i] - lm[i]) / (2 * eps)
+        scale = np.abs(g) @ np.abs(z) + abs(lp[i]) / eps
+        assert abs(d - g @ z) <= 1e-12 * scale
+    # the estimator of the oracle assembles exactly these directional terms
+    ghat = oracle.cd_gradient(P, kind, seed, eps, lp, lm)
+    zs = np.stack([oracle.probe(kind, seed, i, 0, P).astype(np.float64) for i in range(N)])
+    np.testing.assert_allclose(ghat, ((lp - lm) / (2 * eps)) @ zs / N, rtol=1e-12, atol=1e-14)
+
+
+def test_central_difference_bias_is_second_order(oracle):
+    """Cubic loss: the central difference errs by eps^2/6 D^3L[z,z,z] (Eq. 5),
+    a forward difference would err at first order (Eq. 3)."""
+    P = 16
+    rng = np.random.default_rng(11)
+    c3 = rng.normal(size=P)
+    x = rng.normal(size=P)
+    loss = lambda w: float(np.sum(c3 * w**3))  # noqa: E731
+    z = oracle.probe(0, 5, 0, 0, P).astype(np.float64)
+    exact = float(np.sum(3 * c3 * x**2 * z))
+    third = float(np.sum(6 * c3 * z**3))
+    for eps in (1e-1, 1e-2):
+        lp, lm = oracle.cd_losses_generic(x, loss, 0, 5, eps, 1)
+        err = (lp[0] - lm[0]) / (2 * eps) - exact
+        assert abs(err - eps**2 / 6 * third) < 1e-9 * max(1.0, abs(third))
+
+
+def test_z_to_minus_z_swaps_losses_bit_exactly(oracle):
+    for name in ("c1",):
+        cfg = wl.model_cfg(name)
+        th = oracle.init(cfg, 2001)
+        tokens, mask = wl.batch(name, B=2, C=6)
+        lp, lm = oracle.perturbed_losses(cfg, th, 3001, 1e-2, 3, tokens, mask, as_double=True)
+        np_, nm = oracle.perturbed_losses(cfg, th, 3001, 1e-2, 3, tokens, mask, negate=True)
+        assert np.array_equal(lp, nm) and np.array_equal(lm, np_)
+        assert not np.array_equal(lp, lm)
+
+
+def _bruteforce_grad(oracle, cfg, w, tokens, h=1e-5):
+    g = np.zeros_like(w)
+    for j in range(w.size):
+        e = np.zeros_like(w)
+        e[j] = h
+        g[j] = (oracle.lstm_loss(cfg, w + e, tokens) - oracle.lstm_loss(cfg, w - e, tokens)) / (2 * h)
+    return g
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_estimate_converges_to_bruteforce_gradient(oracle, kind):
+    """E|g_N - grad|^2 = (P-1)|grad|^2/N for Rademacher and (P+1)|grad|^2/N for
+    Gaussian probes (linearised; O(1/n_pert) variance of Section 2)."""
+    cfg = dict(TINY, probe=kind)
+    th = oracle.init(cfg, 17)
+    P = th.size
+    tokens = np.random.default_rng(2).integers(0, 8, size=(2, 5)).astype(np.int32)
+    w = th.astype(np.float64)
+    g = _bruteforce_grad(oracle, cfg, w, tokens)
+    eps = 1e-4
+    k = (P - 1) if kind == 0 else (P + 1)
+    ratios = []
+    for N in (128, 512, 2048):
+        vals = []
+        for rep in range(3):
+            seed = 900 + 10 * rep + N
+            lp, lm = oracle.perturbed_losses(cfg, th, seed, eps, N, tokens, as_double=True)
+            ghat = oracle.cd_gradient(P, kind, seed, eps, lp, lm)
+            vals.append(np.sum((ghat - g) ** 2) / np.sum(g**2))
+        r = float(np.mean(vals)) / (k / N)
+        ratios.append(r)
+        assert 0.6 < r < 1.5, (N, r)
+    # and the estimator is unbiased: regression of g_N on grad has slope ~ 1
+    lp, lm = oracle.perturbed_losses(cfg, th, 4242, eps, 4096, tokens, as_double=True)
+    ghat = oracle.cd_gradient(P, kind, 4242, eps, lp, lm)
+    slope = float(ghat @ g / (g @ g))
+    assert abs(slope - 1.0) < 5 * math.sqrt(k / 4096)
+
+
+def test_update_closed_forms(oracle):
+    cfg = dict(TINY)
+    th = oracle.init(cfg, 19)
+    P = th.size
+    # equal losses: theta bit-identical
+    t = th.copy()
+    assert oracle.update(cfg, t, 5, 1e-3, 1e-3, np.full(4, 2.5, np.float32), np.full(4, 2.5, np.float32)) == 0
+    assert np.array_equal(t, th)
+    # N = 1: theta_j - c z_j, one rounding
+    lp, lm = np.float32(3.25), np.float32(3.0)
+    c = oracle.update_coeff(0.01, 1, lp, lm, 1e-3)
+    assert c == np.float32((float(np.float32(0.01)) / 1) * ((float(lp) - float(lm)) / (2 * float(np.float32(1e-3)))))
+    t = th.copy()
+    assert oracle.update(cfg, t, 5, 1e-3, 0.01, np.array([lp]), np.array([lm])) == 0
+    z = oracle.probe(0, 5, 0, 0, P).astype(np.float64)
+    assert np.array_equal(t, (th.astype(np.float64) - float(c) * z).astype(np.float32))
+    # Eq. 7: with lr == eps the coefficient is (L+ - L-) / (2 n_pert)
+    for N in (1, 7, 64):
+        c = oracle.update_coeff(1e-3, N, np.float32(5.0), np.float32(4.5), 1e-3)
+        assert abs(c - 0.5 / (2 * N)) <= 2 * np.spacing(np.float32(0.5 / (2 * N)))
+
+
+def test_update_is_linear_in_loss_differences(oracle):
+    cfg = dict(TINY, probe=1)
+    th = oracle.init(cfg, 23)
+    lp = np.array([2.0, 2.5, 1.0], np.float32)
+    lm = np.array([1.5, 2.75, 1.25], np.float32)
+    d = {}
+    for s in (1.0, 2.0):
+        t = th.copy()
+        assert oracle.update(cfg, t, 8, 1e-3, 1e-4, lm + s * (lp - lm), lm) == 0
+        d[s] = th.astype(np.float64) - t.astype(np.float64)
+    np.testing.assert_allclose(d[2.0], 2 * d[1.0], rtol=0, atol=4 * np.spacing(np.float32(0.2)))
+
+
+def test_update_nonfinite_is_skipped(oracle):
+    cfg = dict(TINY)
+    th = oracle.init(cfg, 29)
+    t = th.copy()
+    st = oracle.update(cfg, t, 1, 1e-3, 1e-3, np.array([1.0, np.nan], np.float32), np.array([1.0, 1.0], np.float32))
+    assert st == -5 and np.array_equal(t, th)
+    st = oracle.update(cfg, t, 1, 1e-3, 1e-3, np.array([np.inf], np.float32), np.array([1.0], np.float32))
+    assert st == -5 and np.array_equal(t, th)
+
+
+@pytest.mark.parametrize("wdtype", [0, 1])
+def test_update_sampled_matches_full_update(oracle, wdtype):
+    for kind in (0, 1):
+        cfg = dict(TINY, wdtype=wdtype, probe=kind)
+        th = oracle.init(cfg, 31)
+        lp = np.array([3.0, 2.0, 2.5, 2.25], np.float32)
+        lm = np.array([2.0, 2.5, 2.5, 1.0], np.float32)
+        t = th.copy()
+        assert oracle.update(cfg, t, 12, 1e-2, 0.5, lp, lm, i0=3) == 0
+        idx = np.array([0, 5, 77, th.size - 1], np.uint64)
+        assert np.array_equal(oracle.update_sampled(cfg, th, 12, 1e-2, 0.5, lp, lm, idx, i0=3), t[idx.astype(np.int64)])
+
+
+def test_one_step_descends_on_tiny_lstm(oracle):
+    """theta' = theta - lr g_N lowers the loss for a small step (descent
+    direction of Eq. 7; Algorithm 1's ascent sign is read as a typo)."""
+    cfg = dict(TINY)
+    th = oracle.init(cfg, 37)
+    tokens = np.random.default_rng(4).integers(0, 8, size=(2, 5)).astype(np.int32)
+    L0 = oracle.lstm_loss(cfg, th.astype(np.float64), tokens)
+    lp, lm = oracle.perturbed_losses(cfg, th, 55, 1e-3, 2048, tokens)
+    t = th.copy()
+    assert oracle.update(cfg, t, 55, 1e-3, 0.2, lp, lm) == 0
+    L1 = oracle.lstm_loss(cfg, t.astype(np.float64), tokens)
+    assert L1 < L0

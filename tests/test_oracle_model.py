@@ -1,0 +1,160 @@
+"""Pins of the oracle's initialisation, parameter layout and LSTM forward +
+cross-entropy loss (Section 4.5: LSTM language models, next-token loss in
+nats), against closed forms and against torch.nn.LSTM / cross_entropy on the
+CPU in float64."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2505_17852_amd import workloads as wl
+
+TINY = dict(n_layers=2, vocab=11, embed=6, hidden=5, wdtype=0, probe=0)
+
+
+def test_param_count_matches_closed_form(oracle):
+    for name in wl.CONFIG_ORDER:
+        cfg = wl.model_cfg(name)
+        assert oracle.param_count(cfg) == wl.param_count(cfg)
+    # the sizes the workloads are quoted with
+    assert oracle.param_count(wl.model_cfg("c1")) == 49_664
+    assert oracle.param_count(wl.model_cfg("c4")) == 1_215_054_672
+    off = oracle.layout(TINY)
+    V, E, H = 11, 6, 5
+    assert off.tolist() == [0, V * E, V * E + 4 * H * E, V * E + 4 * H * E + 4 * H * H,
+                            V * E + 4 * H * E + 4 * H * H + 4 * H,
+                            V * E + 4 * H * E + 4 * H * H + 4 * H + 4 * H * H,
+                            V * E + 4 * H * E + 4 * H * H + 4 * H + 4 * H * H + 4 * H * H,
+                            V * E + 4 * H * E + 8 * H * H + 4 * H + 4 * H * H + 4 * H,
+                            V * E + 4 * H * E + 8 * H * H + 4 * H + 4 * H * H + 4 * H + V * H,
+                            wl.param_count(TINY)]
+
+
+@pytest.mark.parametrize("wdtype", [0, 1])
+def test_init_is_uniform_in_symmetric_interval(oracle, wdtype):
+    cfg = dict(n_layers=1, vocab=256, embed=32, hidden=64, wdtype=wdtype, probe=0)
+    th = oracle.init(cfg, 2001)
+    x = oracle.theta_as_f64(cfg, th)
+    a = 1.0 / math.sqrt(64)
+    assert np.all(np.abs(x) <= a)
+    n = x.size
+    assert abs(x.mean()) < 5 * a / math.sqrt(3 * n)
+    assert abs(x.var() - a * a / 3) < 5 * a * a * math.sqrt(4 / 45 / n)
+    if wdtype == 0:
+        assert len(np.unique(th)) > n // 4
+    th2 = oracle.init(cfg, 2002)
+    assert not np.array_equal(th, th2)
+    if wdtype == 1:
+        # bf16 storage is the round-to-nearest-even of the fp32 initial value
+        cfg32 = dict(cfg, wdtype=0)
+        f32 = oracle.init(cfg32, 2001)
+        ref = torch.from_numpy(f32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(th, ref)
+
+
+def _torch_model_loss(cfg, w, tokens, mask):
+    """Same model written with torch.nn modules (float64, CPU)."""
+    L, V, E, H = cfg["n_layers"], cfg["vocab"], cfg["embed"], cfg["hidden"]
+    off = [0]
+    p = V * E
+    emb = torch.tensor(w[0:V * E].reshape(V, E))
+    lstm = torch.nn.LSTM(E, H, num_layers=L, batch_first=True).double()
+    with torch.no_grad():
+        for l in range(L):
+            El = E if l == 0 else H
+            wih = w[p:p + 4 * H * El].reshape(4 * H, El); p += 4 * H * El
+            whh = w[p:p + 4 * H * H].reshape(4 * H, H); p += 4 * H * H
+            b = w[p:p + 4 * H]; p += 4 * H
+            getattr(lstm, f"weight_ih_l{l}").copy_(torch.tensor(wih))
+            getattr(lstm, f"weight_hh_l{l}").copy_(torch.tensor(whh))
+            getattr(lstm, f"bias_ih_l{l}").copy_(torch.tensor(b))
+            getattr(lstm, f"bias_hh_l{l}").zero_()
+        wout = torch.tensor(w[p:p + V * H].reshape(V, H)); p += V * H
+        bout = torch.tensor(w[p:p + V]); p += V
+        assert p == w.size
+        x = emb[torch.tensor(tokens[:, :-1], dtype=torch.long)]
+        hs, _ = lstm(x)
+        logits = hs @ wout.T + bout
+        tgt = torch.tensor(tokens[:, 1:], dtype=torch.long)
+        ce = torch.nn.functional.cross_entropy(logits.reshape(-1, V), tgt.reshape(-1), reduction="none")
+        ce = ce.reshape(tokens.shape[0], -1).numpy()
+    m = np.ones_like(ce) if mask is None else mask.astype(np.float64)
+    return float((ce * m).sum() / m.sum()), ce * m
+
+
+@pytest.mark.parametrize("masked", [False, True])
+def test_lstm_loss_matches_torch_modules(oracle, masked):
+    rng = np.random.default_rng(5)
+    P = wl.param_count(TINY)
+    w = rng.normal(0, 0.7, size=P)
+    tokens = rng.integers(0, 11, size=(3, 8)).astype(np.int32)
+    mask = (rng.random((3, 7)) < 0.6).astype(np.uint8) if masked else None
+    L, tl = oracle.lstm_loss(TINY, w, tokens, mask, token_losses=True)
+    Lt, tlt = _torch_model_loss(TINY, w, tokens, mask)
+    assert abs(L - Lt) < 1e-12 * max(1.0, abs(Lt))
+    np.testing.assert_allclose(tl, tlt, rtol=1e-12, atol=1e-12)
+
+
+def test_lstm_loss_zero_weights_is_log_vocab(oracle):
+    for V in (256, 50000):
+        cfg = dict(n_layers=2, vocab=V, embed=4, hidden=4, wdtype=0, probe=0)
+        w = np.zeros(wl.param_count(cfg))
+        tokens = np.random.default_rng(0).integers(0, V, size=(2, 5)).astype(np.int32)
+        assert abs(oracle.lstm_loss(cfg, w, tokens) - math.log(V)) < 1e-12
+
+
+def test_lstm_bias_only_closed_form(oracle):
+    """With every matrix zero, the cell follows c_t = s(b_f) c_{t-1} + s(b_i) tanh(b_g)
+    and h_t = s(b_o) tanh(c_t) irrespective of the input; the head sees only
+    h of the top layer through b_out (W_out == 0), so the loss is the CE of b_out."""
+    cfg = dict(n_layers=1, vocab=7, embed=3, hidden=2, wdtype=0, probe=0)
+    off = oracle.layout(cfg)
+    w = np.zeros(wl.param_count(cfg))
+    H = 2
+    bias = np.array([0.3, -0.2, 1.1, -0.7, 0.5, 2.0, -0.4, 0.9])  # i(2) f(2) g(2) o(2)
+    w[off[3]:off[3] + 4 * H] = bias
+    bout = np.linspace(-1, 1, 7)
+    w[off[5]:off[5] + 7] = bout
+    tokens = np.array([[1, 2, 3, 4, 5]], np.int32)
+    L, tl = oracle.lstm_loss(cfg, w, tokens, token_losses=True)
+    lse = math.log(np.exp(bout).sum())
+    np.testing.assert_allclose(tl[0], [lse - bout[t] for t in tokens[0, 1:]], rtol=1e-13)
+    # now make the head read h: W_out row v = v * [1, -1]; closed-form h recurrence
+    wout = np.stack([np.arange(7) * 1.0, -np.arange(7) * 1.0], axis=1)
+    w[off[4]:off[4] + 14] = wout.reshape(-1)
+    sig = lambda x: 1 / (1 + math.exp(-x))  # noqa: E731
+    c = np.zeros(2)
+    ref = []
+    for t in range(4):
+        c = np.array([sig(bias[2 + u]) * c[u] + sig(bias[u]) * math.tanh(bias[4 + u]) for u in range(2)])
+        h = np.array([sig(bias[6 + u]) * math.tanh(c[u]) for u in range(2)])
+        y = wout @ h + bout
+        ref.append(math.log(np.exp(y).sum()) - y[tokens[0, t + 1]])
+    L, tl = oracle.lstm_loss(cfg, w, tokens, token_losses=True)
+    np.testing.assert_allclose(tl[0], ref, rtol=1e-13)
+    assert abs(L - np.mean(ref)) < 1e-13
+
+
+def test_masked_mean_and_empty_mask(oracle):
+    rng = np.random.default_rng(1)
+    w = rng.normal(0, 0.5, size=wl.param_count(TINY))
+    tokens = rng.integers(0, 11, size=(2, 6)).astype(np.int32)
+    _, tl = oracle.lstm_loss(TINY, w, tokens, token_losses=True)
+    mask = np.zeros((2, 5), np.uint8)
+    mask[0, 1] = mask[1, 4] = 1
+    assert abs(oracle.lstm_loss(TINY, w, tokens, mask) - (tl[0, 1] + tl[1, 4]) / 2) < 1e-14
+    assert oracle.lstm_loss(TINY, w, tokens, np.zeros((2, 5), np.uint8)) == 0.0
+
+
+def test_materialise_is_theta_plus_signed_eps_probe(oracle):
+    for wdtype, kind in [(0, 0), (1, 0), (0, 1), (1, 1)]:
+        cfg = dict(TINY, wdtype=wdtype, probe=kind)
+        th = oracle.init(cfg, 7)
+        P = th.size
+        z = oracle.probe(kind, 42, 9, 0, P).astype(np.float64)
+        w = oracle.materialise(cfg, th, 42, 9, 1e-3)
+        base = oracle.theta_as_f64(cfg, th)
+        np.testing.assert_array_equal(w, base + 1e-3 * z)
+        wn = oracle.materialise(cfg, th, 42, 9, 1e-3, negate=True)
+        np.testing.assert_array_equal(wn, base - 1e-3 * z)
