@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Throughput of one CD-RGE training step on one MI355X.
+
+A step is the whole hot path: the 2N perturbed forward passes of the
+stacked-LSTM language model over one batch (zo_perturbed_losses) and the
+parameter update (zo_update), with inputs already resident in device memory.
+Prints one JSON line: perturbed-forward tokens per second (2N*B*C / step
+time), the roofline position of the dominant kernel (the fused gate kernel,
+timed live with HIP events over the timed region) and the CPU oracle timed on
+a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "perturbed-forward tokens/sec per CD-RGE step (2N·B·C/s); % MFMA peak"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
+DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 3), "c4": (1, 3), "c5": (1, 5)}
+DESCRIPTION = {
+    "c1": "1-layer LSTM V=256 E=32 H=64 fp32; B=4 C=32 uniform tokens; N=8 Rademacher",
+    "c2": "2-layer LSTM V=256 E=128 H=256 fp32; B=64 C=256 REVERSE transduction (loss on "
+          "reversed half); N=32 Rademacher, eps=lr=1e-3",
+    "c3": "3-layer LSTM V=50000 E=H=1024 bf16; B=256 C=1024 Zipf(1.1); N=64 Gaussian",
+    "c4": "6-layer LSTM V=50000 E=H=4096 bf16 (~1.2B params); B=256 C=1024 Zipf(1.1); "
+          "N=16 Rademacher",
+    "c5": "2-layer LSTM V=256 E=32 H=512 fp32; fixed batch B=32 C=128 uniform; N=1024 Gaussian",
+}
+
+
+def gate_flops(cfg, N, B):
+    """Algorithmic flops of all gate products of one timestep (every layer):
+    2 * (2N B rows) * 4H * (E_l + H) per layer."""
+    L, E, H = cfg["n_layers"], cfg["embed"], cfg["hidden"]
+    rows = 2 * N * B
+    return sum(2 * rows * 4 * H * ((E if l == 0 else H) + H) for l in range(L))
+
+
+def cpu_baseline(name, budget_s=20.0):
+    """The oracle on the host cores, on a bounded sample of the workload:
+    the full batch with the first N' probes (N' doubling until the budget is
+    used), losses and update. Rate = 2 N' B C / time."""
+    import numpy as np  # noqa: F401
+    from oracle import oracle as ref
+    from paper_2505_17852_amd import workloads as wl
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tokens, mask = wl.batch(name)
+    B, C = tokens.shape[0], tokens.shape[1] - 1
+    if w["embed"] >= 1024:  # billion-parameter shapes: a few sequences, short context
+        B, C = 2, 8
+        tokens = tokens[:B, :C + 1].copy()
+    theta = ref.init(cfg, sd["init"])
+    n, spent, rate, sample = 1, 0.0, None, None
+    while True:
+        th = theta.copy()
+        t0 = time.perf_counter()
+        lp, lm = ref.perturbed_losses(cfg, th, sd["step"], w["eps"], n, tokens, mask)
+        ref.update(cfg, th, sd["step"], w["eps"], w["lr"], lp, lm)
+        dt = time.perf_counter() - t0
+        spent += dt
+        rate = 2 * n * B * C / dt
+        sample = f"{name} with the first {n} of {w['N']} probes, B={B} C={C} (losses + update)"
+        if spent + 2.2 * dt > budget_s or n >= w["N"]:
+            break
+        n *= 2
+    return {"value": rate, "unit": "tokens/s", "cores": ref.threads(), "kind": "oracle",
+            "sample": sample}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="c2", choices=sorted(DESCRIPTION))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs one GPU's share of the step; --gpus {args.gpus} is not supported "
+              "(perturbations would be sharded across GPUs with one all-gather of the 2N "
+              "losses per step; that path is not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2505_17852_amd import workloads as wl
+    from paper_2505_17852_amd import zo
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    zo.lib()  # fails loudly if the HIP library is not built
+    name = args.workload
+    W_def, K_def = DEFAULTS[name]
+    W = W_def if args.warmup is None else args.warmup
+    K = K_def if args.steps is None else args.steps
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    N, eps, lr = w["N"], w["eps"], w["lr"]
+    tokens, mask = wl.batch(name)
+    B, C = tokens.shape[0], tokens.shape[1] - 1
+    dev = torch.device("cuda:0")
+    theta = zo.new_theta(cfg, dev)
+    zo.init(cfg, theta, sd["init"])
+    td = torch.from_numpy(tokens).to(dev)
+    md = None if mask is None else torch.from_numpy(mask).to(dev)
+    assert int(td.min()) >= 0 and int(td.max()) < cfg["vocab"]
+    ws = zo.new_workspace(cfg, N, B, C, dev)
+    Lp = torch.empty(N, dtype=torch.float32, device=dev)
+    Lm = torch.empty(N, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(k):
+        zo.perturbed_losses(cfg, theta, sd["step"] + k, eps, N, td, md, Lplus=Lp, Lminus=Lm,
+                            workspace=ws, stream=stream, check_tokens=False)
+        zo.update(cfg, theta, sd["step"] + k, eps, lr, Lp, Lm, stream=stream)
+
+    for k in range(W):
+        step(k)
+    torch.cuda.synchronize()
+    zo.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(W, W + K):
+        step(k)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = zo.profile_read()
+    zo.profile_enable(False)
+    losses_ok = bool(torch.isfinite(Lp).all() and torch.isfinite(Lm).all())
+
+    ms_per_step = dt / K * 1e3
+    tokens_per_step = 2 * N * B * C
+    value = tokens_per_step / (dt / K)
+    dtype = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"
+    peak = PEAK_TFLOPS[dtype]
+    gate_ms, gate_n = prof["gate"]
+    fl_step = gate_flops(cfg, N, B) * C  # algorithmic gate flops per step
+    fl_launch = fl_step / (cfg["n_layers"] * C)
+    achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
+    fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
+    kernels = {k: {"ms_per_step": v[0] / K, "launches_per_step": v[1] / K} for k, v in prof.items()}
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{name}: {DESCRIPTION[name]}", "N": N, "B": B, "C": C,
+                   "params": zo.param_count(cfg), "eps": eps, "lr": lr},
+        "roofline": {"bound": "mfma", "kernel": "gate (fused LSTM layer step)",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": None if achieved is None else achieved / peak, "traffic": None,
+                     "flops_per_launch": fl_launch},
+        "step_mfma_frac_algorithmic": fwd_flops / (dt / K) / 1e12 / peak,
+        "kernels": kernels,
+        "losses_finite": losses_ok,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(name)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

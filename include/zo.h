@@ -1,0 +1,166 @@
+/*
+ * zo.h - C ABI of the MI355X (gfx950) library for one Central-Difference
+ * Random-vector Gradient Estimation (CD-RGE) training step of a stacked-LSTM
+ * language model (Chaubard & Kochenderfer, "Scaling Recurrent Neural Networks
+ * to a Billion Parameters with Zero-Order Optimization").
+ *
+ * One step, as stated in the paper (Section 2, Eq. 2 and Eq. 7; Section 3,
+ * Algorithm 1 and Algorithm 2):
+ *   for every probe i: L+_i = L(theta + eps z_i, x),  L-_i = L(theta - eps z_i, x)
+ *   theta <- theta - lr * (1/N) * sum_i (L+_i - L-_i) / (2 eps) * z_i
+ * With lr == eps this is Eq. 7 (the paper ties the step size to eps).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Device pointers. Every buffer argument (theta, tokens, mask, losses,
+ * workspace, out) is a device pointer on the current HIP device, allocated
+ * and owned by the caller. The library never allocates, frees or retains
+ * caller memory, and keeps no state between calls.
+ *
+ * Streams. `stream` is a hipStream_t (NULL = the default stream). Every call
+ * only enqueues work on that stream and returns; outputs are valid once the
+ * stream has been synchronised. Calls on distinct streams with distinct
+ * workspaces may run concurrently.
+ *
+ * Errors. Calls return a zo_status. Arguments are validated on the host
+ * before anything is enqueued; on an error nothing is enqueued and no caller
+ * buffer is touched. zo_last_error() returns a thread-local description of
+ * the last failure. No C++ exception crosses this interface.
+ *
+ * Parameter vector theta (flat, row major, one contiguous array of P
+ * elements, fp32 or bf16 according to zo_config.wdtype). The paper keeps the
+ * model as one flat vector and perturbs every element of it (Algorithm 1
+ * input theta in R^d; Algorithm 2 loops over all of theta):
+ *   EMB[V][E]
+ *   for l = 0..L-1: W_ih[4H][E_l], W_hh[4H][H], b[4H]   (E_0 = E, E_l = H)
+ *                   gate row blocks in the order i, f, g, o
+ *   W_out[V][H], b_out[V]
+ *
+ * Probes. z_i[j] is regenerated from (seed, i, j) by Philox4x32-10 (Salmon
+ * et al., SC'11) with key (seed low word, seed high word) and counter
+ * (block low, block high, i, tag):
+ *   Rademacher (tag 0): block j>>7, word (j>>5)&3, bit j&31; bit 1 -> +1,
+ *                       bit 0 -> -1 (Section 2; Algorithm 2's Bernoulli sign);
+ *   normal     (tag 1): block j>>2; words (0,1) give elements 4b, 4b+1 and
+ *                       words (2,3) give 4b+2, 4b+3 by Box-Muller with fixed
+ *                       fp32 operation sequences for ln, sqrt and sin/cos of
+ *                       2 pi k / 2^24 (Section 2 evaluates N(0,1) probes).
+ * Perturbed weights theta +- eps z_i are never materialised.
+ */
+#ifndef ZO_H
+#define ZO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ZO_OK = 0,
+    ZO_EINVAL = -1,     /* a null pointer, a non-positive size, eps <= 0, a non-finite lr ... */
+    ZO_ESHAPE = -2,     /* a model shape the kernels do not support (see zo_config) */
+    ZO_EDEVICE = -3,    /* a HIP runtime error, or no gfx950 device */
+    ZO_ENOMEM = -4,     /* the workspace is smaller than zo_workspace_bytes() */
+    ZO_ENONFINITE = -5  /* reserved: a non-finite loss (zo_update reports it through skipped_out) */
+} zo_status;
+
+enum { ZO_WFP32 = 0, ZO_WBF16 = 1 };
+enum { ZO_RADEMACHER = 0, ZO_GAUSSIAN = 1 };
+
+/* Model shape. All fields > 0; embed and hidden must be multiples of 32
+ * (ZO_ESHAPE otherwise); n_layers <= 64. wdtype: ZO_WFP32 or ZO_WBF16
+ * (storage type of theta; bf16 runs the matrix products in bf16 with fp32
+ * accumulation and fp32 cell state). probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
+typedef struct {
+    int32_t n_layers;
+    int32_t vocab;
+    int32_t embed;
+    int32_t hidden;
+    int32_t wdtype;
+    int32_t probe;
+} zo_config;
+
+/* Number of elements P of theta for this shape (layout above); 0 if the
+ * configuration is invalid. Host only. */
+size_t zo_param_count(const zo_config* cfg);
+
+/* Bytes of device workspace zo_perturbed_losses needs for N probes and a
+ * batch of B sequences of C positions; 0 if the arguments are invalid.
+ * Host only. */
+size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
+
+/* Initialisation: every parameter ~ U(-1/sqrt(H), 1/sqrt(H)), drawn from
+ * Philox tag 2, block j>>2, word j&3 (m = word>>8, value (2m+1-2^24) 2^-24
+ * times fp32(1/sqrt(H)); bf16 storage rounds that fp32 value to nearest
+ * even). theta: device, P elements of the storage type. Setup, not part of
+ * the step. */
+int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
+
+/* The 2N perturbed forward passes of one step (Algorithm 1, the loop over
+ * the worker's probes; Eq. 2's two loss queries per probe).
+ *   theta    device, P elements (read only)
+ *   seed     Philox key of this step's probes; probe n uses index i0 + n
+ *   eps      perturbation size, > 0 and finite
+ *   N        number of probes (>= 1); 2N forward passes
+ *   i0       global index of the first probe (a slice [i0, i0+N) of a larger
+ *            set gives bit-identical losses to the same probes in the full set)
+ *   tokens   device int32 [B][C+1], ids in [0, V): position t reads token
+ *            tokens[b][t] and is scored on the next token tokens[b][t+1]
+ *            (teacher forcing). Ids outside [0, V) are not checked on the
+ *            device: the caller guarantees the range.
+ *   mask     device uint8 [B][C] or NULL (all positions scored)
+ *   Lplus, Lminus  device fp32 [N]: the masked mean over (b, t) of the
+ *            next-token cross-entropy in nats at theta + eps z and at
+ *            theta - eps z (0 when the mask selects nothing)
+ *   workspace, ws_bytes  device scratch of at least zo_workspace_bytes()
+ * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_ENOMEM or ZO_EDEVICE. */
+int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
+                        int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
+                        int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
+                        size_t ws_bytes, void* stream);
+
+/* The update of Eq. 7 in its general form (Algorithm 1's closing loop):
+ *   c_n = fp32( (lr / N) * (L+_n - L-_n) / (2 eps) )  (computed in double)
+ *   theta_j <- theta_j - sum_{n=0}^{N-1} c_n z_{i0+n}[j]  (fp32, ascending n;
+ *   bf16 storage rounds the fp32 result to nearest even)
+ * theta is read and written once, in place. Lplus and Lminus are device fp32
+ * [N]. If any of them is not finite the update is skipped on the device,
+ * theta is left bit-unchanged and, when skipped_out (device int32, may be
+ * NULL) is given, *skipped_out is set to 1 (0 otherwise).
+ * Returns ZO_OK, ZO_EINVAL or ZO_EDEVICE. */
+int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+              uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
+              void* stream);
+
+/* Writes z_i[j0 .. j0+n) of the probe kind `probe` (ZO_RADEMACHER or
+ * ZO_GAUSSIAN) to out (device fp32 [n], n <= 2^30). For checking the regenerated probe
+ * stream; not part of the step. */
+int zo_debug_probe(int32_t probe, uint64_t seed, uint32_t i, uint64_t j0, uint64_t n, float* out,
+                   void* stream);
+
+/* Applies the Box-Muller transform of the normal probes to n_pairs given
+ * word pairs: words (device uint32 [2 n_pairs]) -> out (device fp32
+ * [2 n_pairs]), pair p giving out[2p] = r cos and out[2p+1] = r sin. For
+ * checking the fixed fp32 ln / sqrt / sin / cos sequences over their whole
+ * input range (n_pairs <= 2^30); not part of the step. */
+int zo_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out, void* stream);
+
+/* Kernel timing (instrumentation, off by default). zo_profile_enable(1)
+ * starts recording a HIP event pair around every launch of the timed kernel
+ * classes, on the stream of the launch, and discards earlier records;
+ * zo_profile_enable(0) stops recording. zo_profile_read() waits for the
+ * recorded events and returns, for one class, the summed kernel time in
+ * milliseconds and the number of launches since the last enable. */
+enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4 };
+int zo_profile_enable(int32_t on);
+int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches);
+
+/* Thread-local text of the last error (empty string if none). */
+const char* zo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ZO_H */

@@ -53,6 +53,7 @@ def _declare(L):
     u8p = C.POINTER(C.c_uint8)
     u64p = C.POINTER(C.c_uint64)
     cfgp = C.POINTER(RefConfig)
+    L.zo_ref_threads.restype = C.c_int
     L.zo_ref_philox4x32_10.argtypes = [u32p, u32p, u32p]
     L.zo_ref_log_f32.argtypes = [C.c_float]
     L.zo_ref_log_f32.restype = C.c_float
@@ -101,6 +102,10 @@ def theta_dtype(cfg):
 
 
 # ---------------------------------------------------------------------------
+def threads() -> int:
+    return int(lib().zo_ref_threads())
+
+
 def philox(ctr, key) -> np.ndarray:
     c = np.asarray(ctr, dtype=np.uint32)
     k = np.asarray(key, dtype=np.uint32)

@@ -33,6 +33,9 @@
 #include <stdlib.h>
 #include <string.h>
 
+/* Threads the OpenMP loops of this library use (for reporting timings). */
+int zo_ref_threads(void) { return omp_get_max_threads(); }
+
 /* ======================================================================= */
 /* Philox4x32-10 (Salmon et al., SC'11): 10 rounds of the 4x32 S-box with   */
 /* multipliers 0xD2511F53 and 0xCD9E8D57 and Weyl key increments            */

@@ -54,6 +54,8 @@ enum {
 /* Philox tags (fourth counter word). */
 enum { ZO_REF_TAG_RADEMACHER = 0, ZO_REF_TAG_GAUSSIAN = 1, ZO_REF_TAG_INIT = 2 };
 
+int zo_ref_threads(void);
+
 /* ---- random stream ---------------------------------------------------- */
 void zo_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 float zo_ref_log_f32(float u);

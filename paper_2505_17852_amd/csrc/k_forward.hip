@@ -1,0 +1,641 @@
+// The 2N perturbed forward passes of one CD-RGE step (Algorithm 1's probe
+// loop; Eq. 2's two loss queries per probe), batched over all passes.
+//
+// Every pass (probe n, sign s) runs the same LSTM on the same B sequences
+// with weights theta + s eps z_n. A matrix product of a timestep is computed
+// for all 2N*B rows at once as
+//     a[r] = sum_k A[r][k] W[c][k]  +  sum_k (s_r A[r][k]) (eps z_n[c][k])
+// i.e. the shared weights times the state plus the probe times the signed
+// state, accumulated in one MFMA accumulator. z_n is regenerated tile by
+// tile in LDS from (seed, n, parameter offset); theta + s eps z_n is never
+// formed in memory.
+//
+// Per timestep: embed (perturbed embedding rows) -> one gate kernel per
+// layer (both input products, bias, gate nonlinearities and the cell update
+// fused). Every kTimeChunk timesteps: one output-head kernel over the
+// chunk's top-layer states (vocabulary-tiled, online logsumexp partials),
+// then a combine kernel that adds each position's cross-entropy to its row.
+// At the end a reduction turns row sums into the 2N losses.
+#include <hip/hip_runtime.h>
+
+#include "zo_kernels.hpp"
+#include "zo_profile.hpp"
+#include "zo_rng.hpp"
+
+namespace zo {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 64;    // rows per workgroup tile
+constexpr int BNC = 128;  // columns per workgroup tile
+constexpr int BK = 32;    // K per LDS tile
+constexpr int LDK = BK + 4;
+
+static_assert(BM % kRowGranule == 0 || kRowGranule % BM == 0, "row tiles must stay inside a pass pair");
+static_assert(2 * kRowGranule % BM == 0, "a probe's rows must be a whole number of row tiles");
+static_assert(BNC == kVocabTile, "head vocabulary tile");
+
+struct RowMap {
+  int Bp;
+  int64_t pair_rows;
+};
+
+// ---------------------------------------------------------------------------
+// Bias probes: zb[l][n][c] = eps z_{i0+n}[bias_l + c], zbo[n][v] = eps z[b_out + v]
+// (the biases' perturbation is the same for every timestep).
+struct BiasOffsets {
+  uint64_t layer[kMaxLayers];
+};
+
+__global__ __launch_bounds__(256) void prep_bias_kernel(int kind, Key key, uint32_t i0, float eps,
+                                                        int N, int L, int H4, int V,
+                                                        BiasOffsets bias_off, uint64_t bout_off,
+                                                        float* zb, float* zbo) {
+  const int64_t per_layer = (int64_t)N * H4;
+  const int64_t total = per_layer * L + (int64_t)N * V;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    if (t < per_layer * L) {
+      const int l = (int)(t / per_layer);
+      const int64_t rem = t - l * per_layer;
+      const int n = (int)(rem / H4);
+      const int c = (int)(rem - (int64_t)n * H4);
+      zb[t] = fmul(eps, probe_value(kind, key, i0 + n, bias_off.layer[l] + c));
+    } else {
+      const int64_t rem = t - per_layer * L;
+      const int n = (int)(rem / V);
+      const int v = (int)(rem - (int64_t)n * V);
+      zbo[rem] = fmul(eps, probe_value(kind, key, i0 + n, bout_off + v));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// x0[r][e] = EMB[tok][e] + s eps z_n[emb + tok E + e] for the input token of
+// row r at time t; zeros for padding rows. One thread per 4 elements.
+template <int kind>
+__global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint64_t emb_off, int E,
+                                                        const int32_t* tokens, int C, int t, int B,
+                                                        RowMap rm, int64_t M, Key key, uint32_t i0,
+                                                        float eps, float* x0) {
+  const int E4 = E >> 2;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= M * E4) return;
+  const int64_t r = idx / E4;
+  const int e = (int)(idx - r * E4) * 4;
+  const int pair = (int)(r / rm.pair_rows);
+  const int loc = (int)(r - pair * rm.pair_rows);
+  const int sidx = loc >= rm.Bp;
+  const int b = loc - sidx * rm.Bp;
+  f4 out = {0.f, 0.f, 0.f, 0.f};
+  if (b < B) {
+    const int tok = tokens[(int64_t)b * (C + 1) + t];
+    const uint64_t j = emb_off + (uint64_t)tok * E + e;
+    const f4 w = *(const f4*)(theta + j);
+    float z[4];
+    if constexpr (kind == ZO_RADEMACHER) {
+      const uint32_t word = rademacher_word(key, i0 + pair, j >> 5) >> (uint32_t)(j & 31u);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) z[q] = ((word >> q) & 1u) ? 1.0f : -1.0f;
+    } else {
+      gauss_block(key, i0 + pair, j >> 2, z);
+    }
+    const float se = sidx ? -eps : eps;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[q] = w[q] + fmul(se, z[q]);
+  }
+  *(f4*)(x0 + r * E + e) = out;
+}
+
+// ---------------------------------------------------------------------------
+// fp32 MFMA main loop shared by the gate and head kernels.
+//
+// Workgroup tile: BM=64 rows x BNC=128 columns, 4 waves in 2 (rows) x 2
+// (columns); each wave owns 2 row tiles x 4 column tiles of 16x16 and runs
+// v_mfma_f32_16x16x4_f32. Within a K tile of 32, lane group g (lane/16) feeds
+// k = 8g + s at MFMA step s, so each lane reads 8 consecutive k with two
+// 128-bit LDS loads (the order in which k is summed is free).
+//
+// LDS: A tile [64][36], W tile [128][36], eps z tile [128][36] (fp32).
+struct Seg {
+  const float* A;  // row r of this tile at A + r * lda
+  int64_t lda;
+  const float* W;  // weight row n at W + n * ldw
+  int64_t ldw;
+  uint64_t zoff;   // offset of W inside theta (probe coordinates)
+  int K;
+};
+
+struct Smem {
+  float a[BM * LDK];
+  float w[BNC * LDK];
+  float z[BNC * LDK];
+};
+
+// colmap(rho, &n) -> true if LDS column rho maps to a real weight row n.
+template <int kind, typename ColMap>
+__device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg& sg, ColMap colmap,
+                                             const int (&wrow)[4], int arow0,
+                                             const uint32_t (&sgn)[2], Key key, uint32_t probe,
+                                             float eps, Smem& sm) {
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int g4 = lane >> 4;
+  const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
+  // this thread's Z-generation row
+  const int zr = t >> 1, zhalf = t & 1;
+  int zn;
+  const bool zok = colmap(zr, zn);
+  Words zcache{{0u, 0u, 0u, 0u}};
+  for (int k0 = 0; k0 < sg.K; k0 += BK) {
+    __syncthreads();
+    // A tile: 64 x 32 floats, 2 float4 per thread
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = t + 256 * q;
+      const int row = idx >> 3, c4 = idx & 7;
+      const f4 v = *(const f4*)(sg.A + (int64_t)row * sg.lda + k0 + 4 * c4);
+      *(f4*)(&sm.a[row * LDK + 4 * c4]) = v;
+    }
+    // W tile: 128 x 32 floats, 4 float4 per thread
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = t + 256 * q;
+      const int rho = idx >> 3, c4 = idx & 7;
+      int n;
+      f4 v = {0.f, 0.f, 0.f, 0.f};
+      if (colmap(rho, n)) v = *(const f4*)(sg.W + (int64_t)n * sg.ldw + k0 + 4 * c4);
+      *(f4*)(&sm.w[rho * LDK + 4 * c4]) = v;
+    }
+    // eps z tile: thread (zr, zhalf) writes 16 values of row zr
+    {
+      float zv[16];
+      const uint64_t jrow = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0;
+      if constexpr (kind == ZO_RADEMACHER) {
+        uint32_t word;
+        if (aligned) {
+          if ((k0 & 127) == 0) zcache = stream_block(key, jrow >> 7, probe, kTagRademacher);
+          const int s = (k0 >> 5) & 3;
+          word = s == 0 ? zcache.w[0] : s == 1 ? zcache.w[1] : s == 2 ? zcache.w[2] : zcache.w[3];
+        } else {
+          word = rademacher_word(key, probe, jrow >> 5);
+        }
+        word >>= 16 * zhalf;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
+      } else {
+        const uint64_t j0 = jrow + 16 * zhalf;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          float z4[4];
+          gauss_block(key, probe, (j0 >> 2) + b, z4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) zv[4 * b + e] = fmul(eps, z4[e]);
+        }
+      }
+      if (!zok) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zv[e] = 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f4 v = {zv[4 * q], zv[4 * q + 1], zv[4 * q + 2], zv[4 * q + 3]};
+        *(f4*)(&sm.z[zr * LDK + 16 * zhalf + 4 * q]) = v;
+      }
+    }
+    __syncthreads();
+    // fragments
+    f4 a[2][2], w[4][2], z[4][2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const float* p = &sm.a[(arow0 + 16 * mt + (lane & 15)) * LDK + 8 * g4];
+      a[mt][0] = *(const f4*)p;
+      a[mt][1] = *(const f4*)(p + 4);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float* pw = &sm.w[wrow[q] * LDK + 8 * g4];
+      const float* pz = &sm.z[wrow[q] * LDK + 8 * g4];
+      w[q][0] = *(const f4*)pw;
+      w[q][1] = *(const f4*)(pw + 4);
+      z[q][0] = *(const f4*)pz;
+      z[q][1] = *(const f4*)(pz + 4);
+    }
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const float av = a[mt][s >> 2][s & 3];
+        const float sav = __uint_as_float(__float_as_uint(av) ^ sgn[mt]);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, w[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
+          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(sav, z[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
+__device__ __forceinline__ float tanhf_(float x) { return 1.0f - 2.0f / (__expf(2.0f * x) + 1.0f); }
+
+// ---------------------------------------------------------------------------
+// One LSTM layer at one timestep for all rows:
+//   a = W_ih x + W_hh h + b  (+ s eps (Z_ih x + Z_hh h + z_b))
+//   i, f, o = sigmoid, g = tanh; c <- f c + i g; h <- o tanh(c)
+// Workgroup: 64 rows x 32 hidden units (4 gates x 32 = 128 columns); LDS
+// column rho = gate * 32 + unit.
+struct GateArgs {
+  const float* x;      // [M][El]
+  const float* hprev;  // [M][H]
+  float* hout;         // [M][H]
+  float* cst;          // [M][H]
+  const float* theta;
+  uint64_t off_ih, off_hh, off_b;
+  int El, H;
+  const float* zb;     // [N][4H] eps z of this layer's bias
+  Key key;
+  uint32_t i0;
+  float eps;
+  RowMap rm;
+};
+
+template <int kind>
+__global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
+  __shared__ Smem sm;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int u0 = blockIdx.x * 32;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const int pair = (int)(m0 / g.rm.pair_rows);
+  const int H = g.H;
+  auto colmap = [&](int rho, int& n) {
+    n = (rho >> 5) * H + u0 + (rho & 31);
+    return true;
+  };
+  int wrow[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) wrow[q] = q * 32 + 16 * wn + (lane & 15);
+  uint32_t sgn[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int64_t r = m0 + 32 * wm + 16 * mt + (lane & 15);
+    sgn[mt] = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp ? 0x80000000u : 0u;
+  }
+  f4 acc[2][4];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
+
+  const uint32_t probe = g.i0 + (uint32_t)pair;
+  Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
+  mainloop_f32<kind>(acc, s0, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
+  Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
+  mainloop_f32<kind>(acc, s1, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
+
+  // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
+  const int u = u0 + 16 * wn + (lane & 15);
+  const float* bias = g.theta + g.off_b;
+  const float* zb = g.zb + (int64_t)pair * 4 * H;
+  float bp[4], bm[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float bb = bias[q * H + u], zz = zb[q * H + u];
+    bp[q] = bb + zz;
+    bm[q] = bb - zz;
+  }
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t r = m0 + 32 * wm + 16 * mt + 4 * (lane >> 4) + v;
+      const bool neg = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
+      const float ai = acc[mt][0][v] + (neg ? bm[0] : bp[0]);
+      const float af = acc[mt][1][v] + (neg ? bm[1] : bp[1]);
+      const float ag = acc[mt][2][v] + (neg ? bm[2] : bp[2]);
+      const float ao = acc[mt][3][v] + (neg ? bm[3] : bp[3]);
+      const float ig = sigmoidf_(ai), fg = sigmoidf_(af), gg = tanhf_(ag), og = sigmoidf_(ao);
+      const int64_t o = r * H + u;
+      const float c = fg * g.cst[o] + ig * gg;
+      g.cst[o] = c;
+      g.hout[o] = og * tanhf_(c);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Output head over a chunk of timesteps: rows rr = tt*M + r of the chunk's
+// top-layer states. Logits y = W_out h + b_out (+ s eps (Z_out h + z_bout))
+// for a 128-wide vocabulary tile; the tile's running max and sum of
+// exp(y - max) per row go to pmax/psum, and the logit of the target token is
+// written by the tile that holds it.
+struct HeadArgs {
+  const float* h;  // [Tc*M][H]
+  const float* theta;
+  uint64_t off_w, off_b;
+  int H, V;
+  const float* zbo;  // [N][V]
+  Key key;
+  uint32_t i0;
+  float eps;
+  RowMap rm;
+  int64_t M;
+  int64_t rows;  // Tc * M
+  const int32_t* tokens;
+  int C, t0, B;
+  float* pmax;  // [nvt][rows]
+  float* psum;
+  float* ptgt;  // [rows]
+};
+
+template <int kind>
+__global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
+  __shared__ Smem sm;
+  __shared__ float red_m[2][BM], red_s[2][BM];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int vt = blockIdx.x;
+  const int v0 = vt * BNC;
+  const int64_t rr0 = (int64_t)blockIdx.y * BM;
+  const int tt = (int)(rr0 / g.M);
+  const int64_t r0 = rr0 - (int64_t)tt * g.M;
+  const int pair = (int)(r0 / g.rm.pair_rows);
+  const int V = g.V;
+  auto colmap = [&](int rho, int& n) {
+    n = v0 + rho;
+    const bool ok = n < V;
+    if (!ok) n = 0;
+    return ok;
+  };
+  int wrow[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) wrow[q] = 64 * wn + 16 * q + (lane & 15);
+  uint32_t sgn[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+    const int64_t r = r0 + 32 * wm + 16 * mt + (lane & 15);
+    sgn[mt] = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp ? 0x80000000u : 0u;
+  }
+  f4 acc[2][4];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
+  const uint32_t probe = g.i0 + (uint32_t)pair;
+  Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
+  mainloop_f32<kind>(acc, s0, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
+
+  const float* bout = g.theta + g.off_b;
+  const float* zbo = g.zbo + (int64_t)pair * V;
+  float bp[4], bmn[4];
+  bool cok[4];
+  int col[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    col[q] = v0 + 64 * wn + 16 * q + (lane & 15);
+    cok[q] = col[q] < V;
+    const float bb = cok[q] ? bout[col[q]] : 0.f, zz = cok[q] ? zbo[col[q]] : 0.f;
+    bp[q] = bb + zz;
+    bmn[q] = bb - zz;
+  }
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int lrow = 32 * wm + 16 * mt + 4 * (lane >> 4) + v;
+      const int64_t r = r0 + lrow;
+      const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
+      const bool neg = loc >= g.rm.Bp;
+      const int b = neg ? loc - g.rm.Bp : loc;
+      float y[4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        y[q] = cok[q] ? acc[mt][q][v] + (neg ? bmn[q] : bp[q]) : -INFINITY;
+        mx = fmaxf(mx, y[q]);
+      }
+      if (b < g.B) {
+        const int tgt = g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (col[q] == tgt) g.ptgt[rr0 + lrow] = y[q];
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+      float se = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) se += cok[q] ? __expf(y[q] - mx) : 0.f;
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
+      if ((lane & 15) == 0) {
+        red_m[wn][lrow] = mx;
+        red_s[wn][lrow] = se;
+      }
+    }
+  }
+  __syncthreads();
+  if (t < BM) {
+    const float m_a = red_m[0][t], m_b = red_m[1][t];
+    const float mx = fmaxf(m_a, m_b);
+    const float sa = m_a == -INFINITY ? 0.f : red_s[0][t] * __expf(m_a - mx);
+    const float sb = m_b == -INFINITY ? 0.f : red_s[1][t] * __expf(m_b - mx);
+    g.pmax[(int64_t)vt * g.rows + rr0 + t] = mx;
+    g.psum[(int64_t)vt * g.rows + rr0 + t] = sa + sb;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Adds the cross-entropy of every scored position of the chunk to its row:
+// logsumexp over the vocabulary tiles' partials minus the target logit.
+__global__ __launch_bounds__(256) void combine_kernel(const float* pmax, const float* psum,
+                                                      const float* ptgt, int nvt, int64_t rows,
+                                                      int64_t M, int Tc, int t0, int C, int B,
+                                                      RowMap rm, const uint8_t* mask,
+                                                      double* row_loss) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= M) return;
+  const int64_t loc = r % rm.pair_rows;
+  const int b = (int)(loc >= rm.Bp ? loc - rm.Bp : loc);
+  if (b >= B) return;
+  double acc = row_loss[r];
+  for (int tt = 0; tt < Tc; ++tt) {
+    if (mask && !mask[(int64_t)b * C + t0 + tt]) continue;
+    const int64_t rr = (int64_t)tt * M + r;
+    float mx = -INFINITY;
+    for (int v = 0; v < nvt; ++v) mx = fmaxf(mx, pmax[(int64_t)v * rows + rr]);
+    float s = 0.f;
+    for (int v = 0; v < nvt; ++v) {
+      const float m = pmax[(int64_t)v * rows + rr];
+      if (m != -INFINITY) s += psum[(int64_t)v * rows + rr] * expf(m - mx);
+    }
+    acc += (double)(mx + logf(s) - ptgt[rr]);
+  }
+  row_loss[r] = acc;
+}
+
+// L+-_n = (sum over the pass's sequences of their row sums) / (scored positions).
+__global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int N, int B, int C,
+                                                     RowMap rm, const uint8_t* mask, float* Lp,
+                                                     float* Lm) {
+  __shared__ double part[256];
+  double cnt = 0.0;
+  if (mask) {
+    for (int64_t k = threadIdx.x; k < (int64_t)B * C; k += blockDim.x) cnt += mask[k] ? 1.0 : 0.0;
+  } else if (threadIdx.x == 0) {
+    cnt = (double)B * (double)C;
+  }
+  part[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
+    __syncthreads();
+  }
+  const double total = part[0];
+  for (int p = threadIdx.x; p < 2 * N; p += blockDim.x) {
+    double s = 0.0;
+    const double* rl = row_loss + (int64_t)p * rm.Bp;
+    for (int b = 0; b < B; ++b) s += rl[b];
+    const float L = total > 0.0 ? (float)(s / total) : 0.0f;
+    if (p & 1) Lm[p >> 1] = L;
+    else Lp[p >> 1] = L;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
+  const zo_config& c = a.cfg;
+  const int L = c.n_layers, H = c.hidden, E = c.embed, V = c.vocab;
+  const Rows& R = a.rows;
+  const WsPlan& W = a.ws;
+  const int64_t M = R.M;
+  const Key key = make_key(a.seed);
+  const RowMap rm{R.Bp, R.pair_rows};
+  const float* theta = (const float*)a.theta;
+  char* ws = a.work;
+  float* x0 = (float*)(ws + W.x0);
+  float* hbuf = (float*)(ws + W.hbuf);
+  float* hist = (float*)(ws + W.hist);
+  float* cbuf = (float*)(ws + W.cbuf);
+  float* zb = (float*)(ws + W.zb);
+  float* zbo = (float*)(ws + W.zbo);
+  float* pmax = (float*)(ws + W.pmax);
+  float* psum = (float*)(ws + W.psum);
+  float* ptgt = (float*)(ws + W.ptgt);
+  double* row_loss = (double*)(ws + W.row_loss);
+  hipError_t e;
+#define ZO_TRY(x)                       \
+  do {                                  \
+    if ((e = (x)) != hipSuccess) return e; \
+  } while (0)
+
+  // zero initial states (every pass starts from h = c = 0) and the row sums
+  if (L > 1) ZO_TRY(hipMemsetAsync(hbuf, 0, (size_t)(L - 1) * 2 * M * H * 4, st));
+  ZO_TRY(hipMemsetAsync(hist, 0, (size_t)W.T * M * H * 4, st));
+  ZO_TRY(hipMemsetAsync(cbuf, 0, (size_t)L * M * H * 4, st));
+  ZO_TRY(hipMemsetAsync(row_loss, 0, (size_t)M * 8, st));
+
+  // bias probes
+  {
+    BiasOffsets boff{};
+    for (int l = 0; l < L; ++l) boff.layer[l] = a.lay.bias[l];
+    const int64_t total = (int64_t)R.N * 4 * H * L + (int64_t)R.N * V;
+    int64_t grid = (total + 255) / 256;
+    if (grid > 65536) grid = 65536;
+    prep_bias_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>(c.probe, key, a.i0, a.eps, R.N, L,
+                                                                4 * H, V, boff, a.lay.b_out, zb, zbo);
+    ZO_TRY(hipGetLastError());
+  }
+
+  const int T = W.T;
+  for (int t = 0; t < a.C; ++t) {
+    {
+      const int64_t n = M * (E / 4);
+      const unsigned grid = (unsigned)((n + 255) / 256);
+      ProfScope ps(kKEmbed, st);
+      if (c.probe == ZO_RADEMACHER)
+        embed_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(theta, a.lay.emb, E, a.tokens, a.C, t,
+                                                              R.B, rm, M, key, a.i0, a.eps, x0);
+      else
+        embed_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(theta, a.lay.emb, E, a.tokens, a.C, t,
+                                                            R.B, rm, M, key, a.i0, a.eps, x0);
+      ZO_TRY(hipGetLastError());
+    }
+    const float* xin = x0;
+    for (int l = 0; l < L; ++l) {
+      GateArgs g;
+      g.x = xin;
+      if (l < L - 1) {
+        float* base = hbuf + (size_t)l * 2 * M * H;
+        g.hprev = base + (size_t)((t + 1) & 1) * M * H;
+        g.hout = base + (size_t)(t & 1) * M * H;
+      } else {
+        g.hprev = hist + (size_t)((t + T - 1) % T) * M * H;
+        g.hout = hist + (size_t)(t % T) * M * H;
+      }
+      g.cst = cbuf + (size_t)l * M * H;
+      g.theta = theta;
+      g.off_ih = a.lay.w_ih[l];
+      g.off_hh = a.lay.w_hh[l];
+      g.off_b = a.lay.bias[l];
+      g.El = l == 0 ? E : H;
+      g.H = H;
+      g.zb = zb + (size_t)l * R.N * 4 * H;
+      g.key = key;
+      g.i0 = a.i0;
+      g.eps = a.eps;
+      g.rm = rm;
+      const dim3 grid((unsigned)(H / 32), (unsigned)(M / BM));
+      ProfScope ps(kKGate, st);
+      if (c.probe == ZO_RADEMACHER) gate_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(g);
+      else gate_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(g);
+      ZO_TRY(hipGetLastError());
+      xin = g.hout;
+    }
+    if (t % T == T - 1 || t == a.C - 1) {
+      const int t0 = t - t % T;
+      const int Tc = t - t0 + 1;
+      HeadArgs h;
+      h.h = hist;
+      h.theta = theta;
+      h.off_w = a.lay.w_out;
+      h.off_b = a.lay.b_out;
+      h.H = H;
+      h.V = V;
+      h.zbo = zbo;
+      h.key = key;
+      h.i0 = a.i0;
+      h.eps = a.eps;
+      h.rm = rm;
+      h.M = M;
+      h.rows = (int64_t)Tc * M;
+      h.tokens = a.tokens;
+      h.C = a.C;
+      h.t0 = t0;
+      h.B = R.B;
+      h.pmax = pmax;
+      h.psum = psum;
+      h.ptgt = ptgt;
+      const dim3 grid((unsigned)W.nvt, (unsigned)(h.rows / BM));
+      {
+        ProfScope ps(kKHead, st);
+        if (c.probe == ZO_RADEMACHER) head_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(h);
+        else head_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(h);
+      }
+      ZO_TRY(hipGetLastError());
+      ProfScope ps(kKCombine, st);
+      combine_kernel<<<dim3((unsigned)((M + 255) / 256)), 256, 0, st>>>(
+          pmax, psum, ptgt, W.nvt, h.rows, M, Tc, t0, a.C, R.B, rm, a.mask, row_loss);
+      ZO_TRY(hipGetLastError());
+    }
+  }
+  reduce_kernel<<<1, 256, 0, st>>>(row_loss, R.N, R.B, a.C, rm, a.mask, a.Lplus, a.Lminus);
+  ZO_TRY(hipGetLastError());
+#undef ZO_TRY
+  return hipSuccess;
+}
+
+}  // namespace zo

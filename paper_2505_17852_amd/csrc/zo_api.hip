@@ -1,0 +1,149 @@
+// C ABI entry points: argument validation on the host, then kernel launches
+// on the caller's stream. Nothing here allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/zo.h"
+#include "zo_common.hpp"
+#include "zo_kernels.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return ZO_OK;
+}
+
+int device_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(ZO_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Shape rules of the kernels: every matrix dimension that a K tile or a
+// column tile walks is a multiple of 32 (so that a 32-element probe word
+// never straddles two weight rows).
+int check_config(const zo_config* c) {
+  if (!zo::config_valid(c)) return fail(ZO_EINVAL, "invalid zo_config");
+  if (c->embed % 32 || c->hidden % 32)
+    return fail(ZO_ESHAPE, "embed (%d) and hidden (%d) must be multiples of 32", c->embed,
+                c->hidden);
+  return ZO_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+size_t zo_param_count(const zo_config* cfg) {
+  if (!zo::config_valid(cfg)) return 0;
+  return (size_t)zo::make_layout(*cfg).total;
+}
+
+size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
+  if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1) return 0;
+  const zo::Rows r = zo::make_rows(N, B);
+  return zo::plan_workspace(*cfg, r, C).total;
+}
+
+int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (!theta) return fail(ZO_EINVAL, "theta is NULL");
+  const uint64_t P = zo::make_layout(*cfg).total;
+  const float scale = (float)(1.0 / std::sqrt((double)cfg->hidden));
+  return device_status(zo::launch_init(cfg->wdtype, theta, P, seed, scale, (hipStream_t)stream),
+                       "zo_init");
+}
+
+int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
+                        int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
+                        int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
+                        size_t ws_bytes, void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (cfg->wdtype != ZO_WFP32)
+    return fail(ZO_ESHAPE, "bf16 weights are not supported by this build of the forward");
+  if (!theta || !tokens || !Lplus || !Lminus || !workspace)
+    return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (!aligned16(theta) || !aligned16(workspace))
+    return fail(ZO_EINVAL, "theta and workspace must be 16-byte aligned");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
+  if (N < 1 || B < 1 || C < 1) return fail(ZO_EINVAL, "N, B and C must be >= 1");
+  if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
+    return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
+  const zo::Rows rows = zo::make_rows(N, B);
+  if (rows.M > (int64_t)1 << 30) return fail(ZO_ESHAPE, "2N*B rows too large");
+  const zo::WsPlan plan = zo::plan_workspace(*cfg, rows, C);
+  if (ws_bytes < plan.total)
+    return fail(ZO_ENOMEM, "workspace of %zu bytes < %zu required", ws_bytes, plan.total);
+  zo::ForwardArgs a;
+  a.cfg = *cfg;
+  a.lay = zo::make_layout(*cfg);
+  a.rows = rows;
+  a.ws = plan;
+  a.theta = theta;
+  a.seed = seed;
+  a.eps = eps;
+  a.i0 = i0;
+  a.tokens = tokens;
+  a.mask = mask;
+  a.C = C;
+  a.Lplus = Lplus;
+  a.Lminus = Lminus;
+  a.work = (char*)workspace;
+  return device_status(zo::launch_forward(a, (hipStream_t)stream), "zo_perturbed_losses");
+}
+
+int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+              uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
+              void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (!theta || !Lplus || !Lminus) return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
+  if (!std::isfinite(lr)) return fail(ZO_EINVAL, "lr must be finite");
+  if (N < 1) return fail(ZO_EINVAL, "N must be >= 1");
+  if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
+    return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
+  const uint64_t P = zo::make_layout(*cfg).total;
+  return device_status(zo::launch_update(cfg->wdtype, cfg->probe, theta, P, seed, eps, lr, N, i0,
+                                         Lplus, Lminus, skipped_out, (hipStream_t)stream),
+                       "zo_update");
+}
+
+int zo_debug_probe(int32_t probe, uint64_t seed, uint32_t i, uint64_t j0, uint64_t n, float* out,
+                   void* stream) {
+  if (probe != ZO_RADEMACHER && probe != ZO_GAUSSIAN) return fail(ZO_EINVAL, "unknown probe kind");
+  if (!out && n) return fail(ZO_EINVAL, "out is NULL");
+  if (n > ((uint64_t)1 << 30)) return fail(ZO_EINVAL, "n must be <= 2^30");
+  return device_status(zo::launch_debug_probe(probe, seed, i, j0, n, out, (hipStream_t)stream),
+                       "zo_debug_probe");
+}
+
+int zo_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out, void* stream) {
+  if ((!words || !out) && n_pairs) return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (n_pairs > ((uint64_t)1 << 30)) return fail(ZO_EINVAL, "n_pairs must be <= 2^30");
+  return device_status(zo::launch_debug_gauss_pairs(words, n_pairs, out, (hipStream_t)stream),
+                       "zo_debug_gauss_pairs");
+}
+
+const char* zo_last_error(void) { return g_err; }
+
+}  // extern "C"

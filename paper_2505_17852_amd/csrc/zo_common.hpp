@@ -1,0 +1,131 @@
+// Shapes, parameter layout, pass/row numbering and workspace plan of the
+// CD-RGE step, shared by the host launchers and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/zo.h"
+
+namespace zo {
+
+constexpr int kMaxLayers = 64;
+
+// Flat parameter layout (the model as one vector, every element perturbed):
+// EMB[V][E]; per layer W_ih[4H][E_l], W_hh[4H][H], b[4H]; W_out[V][H]; b_out[V].
+struct Layout {
+  uint64_t emb;
+  uint64_t w_ih[kMaxLayers];
+  uint64_t w_hh[kMaxLayers];
+  uint64_t bias[kMaxLayers];
+  uint64_t w_out;
+  uint64_t b_out;
+  uint64_t total;
+};
+
+inline bool config_valid(const zo_config* c) {
+  return c && c->n_layers >= 1 && c->n_layers <= kMaxLayers && c->vocab >= 1 && c->embed >= 1 &&
+         c->hidden >= 1 && (c->wdtype == ZO_WFP32 || c->wdtype == ZO_WBF16) &&
+         (c->probe == ZO_RADEMACHER || c->probe == ZO_GAUSSIAN);
+}
+
+inline Layout make_layout(const zo_config& c) {
+  Layout L{};
+  const uint64_t V = (uint64_t)c.vocab, E = (uint64_t)c.embed, H = (uint64_t)c.hidden;
+  uint64_t p = 0;
+  L.emb = p;
+  p += V * E;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const uint64_t El = l == 0 ? E : H;
+    L.w_ih[l] = p;
+    p += 4 * H * El;
+    L.w_hh[l] = p;
+    p += 4 * H * H;
+    L.bias[l] = p;
+    p += 4 * H;
+  }
+  L.w_out = p;
+  p += V * H;
+  L.b_out = p;
+  p += V;
+  L.total = p;
+  return L;
+}
+
+// Rows of the batched forward. The 2N passes (probe n, sign s) each run the
+// B sequences; every matrix product of a timestep covers all of them at once.
+// Row r = (2 n + sidx) * Bp + b with sidx 0 for +eps and 1 for -eps; B is
+// padded to Bp (a multiple of kRowGranule) so that every row tile of a
+// kernel lies inside one probe's rows. Padded rows (b >= B) carry zeros in,
+// are computed like the others and never scored.
+constexpr int kRowGranule = 32;
+
+struct Rows {
+  int32_t B, Bp, N;
+  int64_t pair_rows;  // 2 Bp
+  int64_t M;          // N * 2 Bp
+};
+
+inline Rows make_rows(int32_t N, int32_t B) {
+  Rows r;
+  r.B = B;
+  r.N = N;
+  r.Bp = (B + kRowGranule - 1) / kRowGranule * kRowGranule;
+  r.pair_rows = 2 * (int64_t)r.Bp;
+  r.M = (int64_t)N * r.pair_rows;
+  return r;
+}
+
+// Time steps whose top-layer states are kept for one batched output-head pass.
+constexpr int kTimeChunk = 16;
+
+// Output-head vocabulary tile (columns per workgroup).
+constexpr int kVocabTile = 128;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workspace plan (byte offsets from the workspace base, 256-aligned).
+struct WsPlan {
+  size_t x0;         // f32 [M][E]         perturbed embeddings of one timestep
+  size_t hbuf;       // f32 [L-1][2][M][H] double-buffered states of the lower layers
+  size_t hist;       // f32 [T][M][H]      top-layer states of the current time chunk
+  size_t cbuf;       // f32 [L][M][H]      cell states
+  size_t zb;         // f32 [L][N][4H]     eps * z of the gate biases, per probe
+  size_t zbo;        // f32 [N][V]         eps * z of the head bias, per probe
+  size_t pmax;       // f32 [nvt][T*M]     per vocabulary tile: running max
+  size_t psum;       // f32 [nvt][T*M]     per vocabulary tile: sum of exp(y - max)
+  size_t ptgt;       // f32 [T*M]          target logit
+  size_t row_loss;   // f64 [M]            masked loss sum of each row
+  size_t total;
+  int nvt;           // vocabulary tiles
+  int T;             // time chunk
+};
+
+inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
+  WsPlan w{};
+  const size_t M = (size_t)r.M, E = (size_t)c.embed, H = (size_t)c.hidden, V = (size_t)c.vocab;
+  const size_t L = (size_t)c.n_layers;
+  const size_t el = c.wdtype == ZO_WBF16 ? 2 : 4;  // activation operand element size
+  w.T = C < kTimeChunk ? C : kTimeChunk;
+  w.nvt = (int)((V + kVocabTile - 1) / kVocabTile);
+  size_t p = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = p;
+    p = align_up(p + bytes, 256);
+    return o;
+  };
+  w.x0 = take(M * E * el);
+  w.hbuf = take((L - 1) * 2 * M * H * el);
+  w.hist = take((size_t)w.T * M * H * el);
+  w.cbuf = take(L * M * H * 4);
+  w.zb = take(L * (size_t)r.N * 4 * H * 4);
+  w.zbo = take((size_t)r.N * V * 4);
+  w.pmax = take((size_t)w.nvt * w.T * M * 4);
+  w.psum = take((size_t)w.nvt * w.T * M * 4);
+  w.ptgt = take((size_t)w.T * M * 4);
+  w.row_loss = take(M * 8);
+  w.total = p;
+  return w;
+}
+
+}  // namespace zo

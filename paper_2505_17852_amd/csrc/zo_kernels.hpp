@@ -1,0 +1,41 @@
+// Launchers of the HIP kernels (host side). Every launcher only enqueues on
+// `stream`; argument checking happens in the C ABI layer before these run.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "zo_common.hpp"
+
+namespace zo {
+
+// k_rng.hip
+hipError_t launch_debug_probe(int kind, uint64_t seed, uint32_t i, uint64_t j0, uint64_t n,
+                              float* out, hipStream_t s);
+hipError_t launch_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out,
+                                    hipStream_t s);
+hipError_t launch_init(int wdtype, void* theta, uint64_t P, uint64_t seed, float scale,
+                       hipStream_t s);
+hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t seed, float eps,
+                         float lr, int32_t N, uint32_t i0, const float* Lp, const float* Lm,
+                         int32_t* skipped, hipStream_t s);
+
+// k_forward.hip: one call of the perturbed forward passes.
+struct ForwardArgs {
+  zo_config cfg;
+  Layout lay;
+  Rows rows;
+  WsPlan ws;
+  const void* theta;
+  uint64_t seed;
+  float eps;
+  uint32_t i0;
+  const int32_t* tokens;
+  const uint8_t* mask;
+  int32_t C;
+  float* Lplus;
+  float* Lminus;
+  char* work;
+};
+hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
+
+}  // namespace zo

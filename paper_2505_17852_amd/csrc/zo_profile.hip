@@ -1,0 +1,71 @@
+// Event-based kernel timing behind zo_profile_enable / zo_profile_read.
+#include "zo_profile.hpp"
+
+#include <mutex>
+#include <vector>
+
+#include "../../include/zo.h"
+
+namespace zo {
+
+std::atomic<int> g_profile_on{0};
+
+namespace {
+struct Slot {
+  hipEvent_t a, b;
+  int cls;
+};
+std::mutex g_mu;
+std::vector<Slot> g_slots;  // event pairs, reused across enable/read cycles
+size_t g_used = 0;
+}  // namespace
+
+int prof_begin(KernelClass k, hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (g_used == g_slots.size()) {
+    Slot sl{};
+    if (hipEventCreate(&sl.a) != hipSuccess || hipEventCreate(&sl.b) != hipSuccess) return -1;
+    g_slots.push_back(sl);
+  }
+  Slot& sl = g_slots[g_used];
+  sl.cls = (int)k;
+  if (hipEventRecord(sl.a, s) != hipSuccess) return -1;
+  return (int)g_used++;
+}
+
+void prof_end(int slot, hipStream_t s) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  (void)hipEventRecord(g_slots[(size_t)slot].b, s);
+}
+
+}  // namespace zo
+
+extern "C" {
+
+int zo_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(zo::g_mu);
+  zo::g_used = 0;
+  zo::g_profile_on.store(on ? 1 : 0);
+  return ZO_OK;
+}
+
+int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches) {
+  if (!total_ms || !launches || kernel_class < 0 || kernel_class >= zo::kKClasses) return ZO_EINVAL;
+  std::lock_guard<std::mutex> lk(zo::g_mu);
+  double ms = 0.0;
+  int64_t n = 0;
+  for (size_t i = 0; i < zo::g_used; ++i) {
+    const auto& sl = zo::g_slots[i];
+    if (sl.cls != kernel_class) continue;
+    if (hipEventSynchronize(sl.b) != hipSuccess) return ZO_EDEVICE;
+    float e = 0.f;
+    if (hipEventElapsedTime(&e, sl.a, sl.b) != hipSuccess) return ZO_EDEVICE;
+    ms += e;
+    ++n;
+  }
+  *total_ms = ms;
+  *launches = n;
+  return ZO_OK;
+}
+
+}  // extern "C"

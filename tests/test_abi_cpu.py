@@ -1,0 +1,100 @@
+"""Host-side checks of the C ABI library (no GPU needed): it loads, exports
+every entry point that include/zo.h declares, its host-only functions agree
+with the oracle's layout, and argument errors are reported before anything
+touches a device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2505_17852_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zo.h")
+
+
+@pytest.fixture(scope="module")
+def zo():
+    from paper_2505_17852_amd import zo as z
+    if not os.path.exists(z.LIB_PATH):
+        from paper_2505_17852_amd import build
+        build.build()
+    z.lib()
+    return z
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(zo_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_step(zo):
+    names = declared_symbols()
+    for n in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_param_count",
+              "zo_workspace_bytes", "zo_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(zo):
+    L = zo.lib()
+    for n in declared_symbols():
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("name", wl.CONFIG_ORDER)
+def test_param_count_matches_oracle_layout(zo, oracle, name):
+    cfg = wl.model_cfg(name)
+    assert zo.param_count(cfg) == oracle.param_count(cfg) == wl.param_count(cfg)
+
+
+def test_param_count_survey_values(zo):
+    # closed-form counts of the five workloads
+    expect = {"c1": 49_664, "c2": 1_018_112, "c3": 127_628_112, "c4": 1_215_054_672,
+              "c5": 3_354_880}
+    for name, p in expect.items():
+        assert zo.param_count(wl.model_cfg(name)) == p
+
+
+def test_workspace_bytes(zo):
+    cfg = wl.model_cfg("c2")
+    n = zo.workspace_bytes(cfg, 32, 64, 256)
+    assert n > 0
+    assert zo.workspace_bytes(cfg, 64, 64, 256) > n
+    assert zo.workspace_bytes(cfg, 0, 64, 256) == 0
+    bad = dict(cfg, n_layers=0)
+    assert zo.workspace_bytes(bad, 4, 4, 4) == 0
+
+
+def _call_losses(zo, cfg, eps=1e-3, N=2, B=2, Cn=4, ptrs=True):
+    c = zo._cfg(cfg)
+    fake = C.c_void_p(0x10000) if ptrs else None
+    return zo.lib().zo_perturbed_losses(C.byref(c), fake, 1, eps, N, 0, fake, None, B, Cn,
+                                        fake, fake, fake, 1 << 40, None)
+
+
+def test_argument_errors_before_any_device_work(zo):
+    cfg = wl.model_cfg("c1")
+    assert _call_losses(zo, dict(cfg, n_layers=0)) == zo.ZO_EINVAL
+    assert _call_losses(zo, dict(cfg, probe=7)) == zo.ZO_EINVAL
+    assert _call_losses(zo, dict(cfg, hidden=48)) == zo.ZO_ESHAPE
+    assert _call_losses(zo, dict(cfg, embed=20)) == zo.ZO_ESHAPE
+    assert _call_losses(zo, cfg, eps=0.0) == zo.ZO_EINVAL
+    assert _call_losses(zo, cfg, eps=float("nan")) == zo.ZO_EINVAL
+    assert _call_losses(zo, cfg, N=0) == zo.ZO_EINVAL
+    assert _call_losses(zo, cfg, B=0) == zo.ZO_EINVAL
+    assert _call_losses(zo, cfg, ptrs=False) == zo.ZO_EINVAL
+    assert "NULL" in zo.lib().zo_last_error().decode()
+    c = zo._cfg(cfg)
+    fake = C.c_void_p(0x10000)
+    ws_small = zo.lib().zo_perturbed_losses(C.byref(c), fake, 1, 1e-3, 2, 0, fake, None, 2, 4,
+                                            fake, fake, fake, 16, None)
+    assert ws_small == zo.ZO_ENOMEM
+    L = zo.lib()
+    assert L.zo_update(C.byref(c), fake, 1, 1e-3, float("inf"), 2, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_update(C.byref(c), fake, 1, -1.0, 1e-3, 2, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_update(C.byref(c), fake, 1, 1e-3, 1e-3, 0, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    # probe indices must stay within 32 bits
+    assert L.zo_update(C.byref(c), fake, 1, 1e-3, 1e-3, 4, 0xFFFFFFFE, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_debug_probe(5, 1, 0, 0, 4, fake, None) == zo.ZO_EINVAL

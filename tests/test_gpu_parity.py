@@ -1,0 +1,244 @@
+"""GPU path vs the CPU oracle, on the same seeded inputs, through the C ABI.
+
+Bars: probe values and initial weights bit-exact; per-pass losses within
+1e-5 relative (fp32 path); updated fp32 theta within 1e-5 relative with an
+absolute floor of 1e-5 times the mean |theta|.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from paper_2505_17852_amd import workloads as wl  # noqa: E402
+
+LOSS_RTOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def zo():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_17852_amd import zo as z
+    z.lib()
+    return z
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def dev_tokens(tokens, mask):
+    t = torch.from_numpy(np.ascontiguousarray(tokens)).cuda()
+    m = None if mask is None else torch.from_numpy(np.ascontiguousarray(mask)).cuda()
+    return t, m
+
+
+def theta_close(got, ref, cfg):
+    if cfg["wdtype"] == wl.BF16:
+        g = (got.astype(np.uint32) << 16).view(np.float32)
+        r = (ref.astype(np.uint32) << 16).view(np.float32)
+        ulp = np.abs(r) * 2.0 ** -7 + 1e-30
+        return np.all(np.abs(g - r) <= ulp)
+    tol = 1e-5 * np.abs(ref) + 1e-5 * np.abs(ref).mean()
+    return np.all(np.abs(got.astype(np.float64) - ref) <= tol)
+
+
+# ---------------------------------------------------------------------------
+# probe stream
+
+@pytest.mark.parametrize("kind", [wl.RADEMACHER, wl.GAUSSIAN])
+@pytest.mark.parametrize("seed,i,j0,n", [(1, 0, 0, 5000), (0xDEADBEEF12345678, 7, 1 << 33, 3001),
+                                         (3003, 1023, 123457, 777)])
+def test_probe_bit_exact(zo, oracle, kind, seed, i, j0, n):
+    say(f"probe kind={kind} seed={seed} i={i} j0={j0} n={n}")
+    got = zo.debug_probe(kind, seed, i, j0, n).cpu().numpy()
+    ref = oracle.probe(kind, seed, i, j0, n)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_gaussian_transform_exhaustive(zo, oracle):
+    """Every one of the 2^24 radius inputs and 2^24 angle inputs (the low 8
+    bits of each word are ignored by the transform; fill them at random)."""
+    say("box-muller over all 2^24 inputs")
+    rng = np.random.default_rng(7)
+    k = np.arange(1 << 24, dtype=np.uint32)
+    words = np.empty(2 << 24, np.uint32)
+    words[0::2] = (k << 8) | rng.integers(0, 256, k.size, dtype=np.uint32)
+    words[1::2] = (k[::-1] << 8) | rng.integers(0, 256, k.size, dtype=np.uint32)
+    got = zo.debug_gauss_pairs(torch.from_numpy(words.view(np.int32)).cuda()).cpu().numpy()
+    ref = oracle.gauss_pairs(words)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# initialisation
+
+@pytest.mark.parametrize("cfg", [wl.model_cfg("c1"), wl.model_cfg("c2"),
+                                 dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wl.BF16, probe=0)])
+def test_init_bit_exact(zo, oracle, cfg):
+    say(f"init {cfg}")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 2001)
+    got = theta.view(torch.int16 if cfg["wdtype"] == wl.BF16 else torch.int32).cpu().numpy()
+    ref = oracle.init(cfg, 2001)
+    assert np.array_equal(got.view(ref.dtype), ref)
+
+
+# ---------------------------------------------------------------------------
+# update
+
+UPDATE_CASES = [
+    ("c1-rad", dict(wl.model_cfg("c1")), 8, 1e-2, 1e-3),
+    ("ragged-rad-bf16", dict(n_layers=1, vocab=77, embed=32, hidden=32, wdtype=wl.BF16, probe=0), 37, 1e-3, 1e-3),
+    ("gauss-fp32", dict(n_layers=1, vocab=50, embed=32, hidden=64, wdtype=wl.FP32, probe=1), 19, 1e-2, 1e-2),
+    ("gauss-bf16", dict(n_layers=2, vocab=50, embed=32, hidden=32, wdtype=wl.BF16, probe=1), 300, 1e-3, 1e-3),
+]
+
+
+@pytest.mark.parametrize("name,cfg,N,eps,lr", UPDATE_CASES, ids=[c[0] for c in UPDATE_CASES])
+def test_update_parity(zo, oracle, name, cfg, N, eps, lr):
+    say(f"update {name} P={zo.param_count(cfg)} N={N}")
+    rng = np.random.default_rng(11)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 5)
+    ref = oracle.init(cfg, 5)
+    Lp = (5.0 + rng.standard_normal(N) * 0.01).astype(np.float32)
+    Lm = (5.0 + rng.standard_normal(N) * 0.01).astype(np.float32)
+    zo.update(cfg, theta, 99, eps, lr, torch.from_numpy(Lp).cuda(), torch.from_numpy(Lm).cuda(), i0=3)
+    got = theta.view(torch.int16 if cfg["wdtype"] == wl.BF16 else torch.int32).cpu().numpy().view(ref.dtype)
+    assert oracle.update(cfg, ref, 99, eps, lr, Lp, Lm, i0=3) == 0
+    assert theta_close(got, ref, cfg)
+
+
+def test_update_equal_losses_leave_theta_unchanged(zo):
+    cfg = wl.model_cfg("c1")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 5)
+    before = theta.clone()
+    L = torch.full((8,), 3.25, device="cuda")
+    zo.update(cfg, theta, 1, 1e-2, 1e-3, L, L.clone())
+    assert torch.equal(theta.view(torch.int32), before.view(torch.int32))
+
+
+def test_update_nonfinite_skips(zo):
+    cfg = wl.model_cfg("c1")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 5)
+    before = theta.clone()
+    Lp = torch.full((8,), 3.0, device="cuda")
+    Lm = Lp.clone()
+    Lm[5] = float("nan")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    zo.update(cfg, theta, 1, 1e-2, 1e-3, Lp, Lm, skipped=flag)
+    assert flag.item() == 1
+    assert torch.equal(theta.view(torch.int32), before.view(torch.int32))
+    Lm[5] = 3.5
+    zo.update(cfg, theta, 1, 1e-2, 1e-3, Lp, Lm, skipped=flag)
+    assert flag.item() == 0
+    assert not torch.equal(theta.view(torch.int32), before.view(torch.int32))
+
+
+# ---------------------------------------------------------------------------
+# perturbed losses
+
+LOSS_CASES = [
+    # name, model cfg, N, B, C, eps, masked
+    ("c1", wl.model_cfg("c1"), 8, 4, 32, 1e-2, False),
+    # several tiles and ragged tails: 3 unit tiles (H=96, unaligned K), vocab 300 (2 full
+    # vocabulary tiles + 44), B=5 (padded rows), C=20 (a full and a partial time chunk)
+    ("ragged-rad", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=0, probe=0), 3, 5, 20, 1e-2, True),
+    ("ragged-gauss", dict(n_layers=2, vocab=300, embed=32, hidden=128, wdtype=0, probe=1), 2, 3, 18, 1e-2, True),
+    ("deep3-gauss", dict(n_layers=3, vocab=130, embed=128, hidden=64, wdtype=0, probe=1), 2, 2, 9, 1e-3, False),
+    ("c2-widths", wl.model_cfg("c2"), 2, 3, 12, 1e-3, True),
+    ("c5-widths", wl.model_cfg("c5"), 2, 2, 10, 1e-2, False),
+]
+
+
+def _tokens_for(name, cfg, B, C, masked, seed=4242):
+    rng = np.random.default_rng(seed)
+    if name.startswith("c2"):
+        return wl.reverse_task(rng, B, C, cfg["vocab"])
+    tok = wl.uniform_tokens(rng, B, C, cfg["vocab"])
+    mask = (rng.random((B, C)) < 0.6).astype(np.uint8) if masked else None
+    return tok, mask
+
+
+@pytest.mark.parametrize("name,cfg,N,B,C,eps,masked", LOSS_CASES, ids=[c[0] for c in LOSS_CASES])
+def test_losses_match_oracle(zo, oracle, name, cfg, N, B, C, eps, masked):
+    say(f"losses {name} cfg={cfg} N={N} B={B} C={C}")
+    tok, mask = _tokens_for(name, cfg, B, C, masked)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 77)
+    ref_theta = oracle.init(cfg, 77)
+    td, md = dev_tokens(tok, mask)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 12345, eps, N, td, md, i0=4)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    rp, rm = oracle.perturbed_losses(cfg, ref_theta, 12345, eps, N, tok, mask, i0=4, as_double=True)
+    say("gpu", gp, gm, "oracle", rp, rm)
+    assert np.all(np.abs(gp - rp) <= LOSS_RTOL * np.abs(rp))
+    assert np.all(np.abs(gm - rm) <= LOSS_RTOL * np.abs(rm))
+
+
+def test_losses_slice_and_determinism(zo):
+    """Probe slices [i0, i0+n) reproduce the full set's losses bit for bit,
+    and two runs are bit-identical."""
+    cfg = dict(n_layers=2, vocab=200, embed=64, hidden=64, wdtype=0, probe=0)
+    B, C = 6, 17
+    tok, _ = _tokens_for("x", cfg, B, C, False)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 3)
+    td, _ = dev_tokens(tok, None)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 9, 1e-2, 7, td)
+    Lp2, Lm2 = zo.perturbed_losses(cfg, theta, 9, 1e-2, 7, td)
+    assert torch.equal(Lp, Lp2) and torch.equal(Lm, Lm2)
+    sp, sm = zo.perturbed_losses(cfg, theta, 9, 1e-2, 3, td, i0=2)
+    assert torch.equal(sp, Lp[2:5]) and torch.equal(sm, Lm[2:5])
+
+
+def test_empty_mask_gives_zero_loss(zo):
+    cfg = wl.model_cfg("c1")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 3)
+    tok, _ = _tokens_for("x", cfg, 2, 5, False)
+    td, _ = dev_tokens(tok, None)
+    m = torch.zeros((2, 5), dtype=torch.uint8, device="cuda")
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 1, 1e-2, 2, td, m)
+    assert torch.all(Lp == 0) and torch.all(Lm == 0)
+
+
+def test_zero_weights_give_ln_v(zo):
+    """theta = 0 and eps tiny: every logit is O(eps), so L is ln V to O(eps)."""
+    cfg = dict(n_layers=2, vocab=256, embed=32, hidden=64, wdtype=0, probe=0)
+    theta = torch.zeros(zo.param_count(cfg), dtype=torch.float32, device="cuda")
+    tok, _ = _tokens_for("x", cfg, 3, 6, False)
+    td, _ = dev_tokens(tok, None)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 1, 1e-6, 2, td)
+    assert torch.allclose(Lp.double(), torch.full_like(Lp.double(), np.log(256)), rtol=1e-5)
+    assert torch.allclose(Lm.double(), torch.full_like(Lm.double(), np.log(256)), rtol=1e-5)
+
+
+# ---------------------------------------------------------------------------
+# a full step at a workload's real size, in the launch configuration the
+# benchmark times, checked on the first probe's two passes
+
+def test_c2_full_size_first_probe(zo, oracle):
+    name = "c2"
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tok, mask = wl.batch(name)
+    say(f"full-size {name}: N={w['N']} B={w['B']} C={w['C']}")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    td, md = dev_tokens(tok, mask)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, sd["step"], w["eps"], w["N"], td, md)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    ref_theta = oracle.init(cfg, sd["init"])
+    rp, rm = oracle.perturbed_losses(cfg, ref_theta, sd["step"], w["eps"], 1, tok, mask, i0=0,
+                                     as_double=True)
+    say("gpu", gp[0], gm[0], "oracle", rp[0], rm[0])
+    assert abs(gp[0] - rp[0]) <= LOSS_RTOL * abs(rp[0])
+    assert abs(gm[0] - rm[0]) <= LOSS_RTOL * abs(rm[0])
+    assert np.all(np.isfinite(gp)) and np.all(np.isfinite(gm))
