@@ -10,8 +10,10 @@
 //
 // The fp32 operation sequences below (ln, sin/cos of a 24-bit angle, the
 // Box-Muller pair and the initial-weight scaling) are a fixed contract: every
-// operation is an explicitly rounded single fp32 operation (no contraction),
-// so that every implementation of the contract yields the same bits.
+// operation is a single correctly rounded fp32 operation, so that every
+// implementation of the contract yields the same bits. HIP compiles with
+// floating-point contraction on by default; the helpers fmul/fadd/fdiv turn
+// it off (a multiply followed by an add must not become one fma).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -71,8 +73,23 @@ __device__ __forceinline__ uint32_t rademacher_word(Key key, uint32_t i, uint64_
 
 // ---- fixed fp32 sequences ------------------------------------------------
 
-__device__ __forceinline__ float fmul(float a, float b) { return __fmul_rn(a, b); }
-__device__ __forceinline__ float fadd(float a, float b) { return __fadd_rn(a, b); }
+// Single rounded operations. The contraction pragma sits inside each helper
+// (an fma can only form when both the multiply and the add allow it), and
+// sqrt / division use the compiler's correctly rounded expansions
+// (__fsqrt_rn would map to the 1-ulp hardware square root).
+__device__ __forceinline__ float fmul(float a, float b) {
+#pragma clang fp contract(off)
+  return a * b;
+}
+__device__ __forceinline__ float fadd(float a, float b) {
+#pragma clang fp contract(off)
+  return a + b;
+}
+__device__ __forceinline__ float fdiv(float a, float b) {
+#pragma clang fp contract(off)
+  return a / b;
+}
+__device__ __forceinline__ float fsqrt(float a) { return __builtin_sqrtf(a); }
 
 // Natural log of a normal float u in (0, 1]. Write u = 2^e m with m folded
 // into (sqrt(1/2), sqrt(2)]; then ln m = 2 atanh(s) with s = (m-1)/(m+1),
@@ -87,7 +104,7 @@ __device__ __forceinline__ float ln_u(float u) {
     m = fmul(m, 0.5f);
     e += 1;
   }
-  const float s = __fdiv_rn(fadd(m, -1.0f), fadd(m, 1.0f));
+  const float s = fdiv(fadd(m, -1.0f), fadd(m, 1.0f));
   const float s2 = fmul(s, s);
   float p = (float)(2.0 / 9.0);
   p = fadd(fmul(p, s2), (float)(2.0 / 7.0));
@@ -139,7 +156,7 @@ __device__ __forceinline__ void sincos_turn24(uint32_t k24, float& s_out, float&
 // angle x1>>8 of 2^24; returns (r cos, r sin) with r = sqrt(-2 ln u1).
 __device__ __forceinline__ void gauss_pair(uint32_t x0, uint32_t x1, float& z0, float& z1) {
   const float u1 = fmul((float)((x0 >> 8) + 1u), __uint_as_float(0x33800000u));  // 2^-24
-  const float r = __fsqrt_rn(fmul(-2.0f, ln_u(u1)));
+  const float r = fsqrt(fmul(-2.0f, ln_u(u1)));
   float s, c;
   sincos_turn24(x1 >> 8, s, c);
   z0 = fmul(r, c);

@@ -35,6 +35,15 @@ def dev_tokens(tokens, mask):
     return t, m
 
 
+def assert_bits_equal(got, ref, what):
+    g, r = got.view(np.uint32), ref.view(np.uint32)
+    bad = np.nonzero(g != r)[0]
+    if bad.size:
+        k = bad[:8]
+        raise AssertionError(f"{what}: {bad.size} of {g.size} differ; first at {k.tolist()}: "
+                             f"gpu {got[k].tolist()} oracle {ref[k].tolist()}")
+
+
 def theta_close(got, ref, cfg):
     if cfg["wdtype"] == wl.BF16:
         g = (got.astype(np.uint32) << 16).view(np.float32)
@@ -55,7 +64,7 @@ def test_probe_bit_exact(zo, oracle, kind, seed, i, j0, n):
     say(f"probe kind={kind} seed={seed} i={i} j0={j0} n={n}")
     got = zo.debug_probe(kind, seed, i, j0, n).cpu().numpy()
     ref = oracle.probe(kind, seed, i, j0, n)
-    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    assert_bits_equal(got, ref, "probe")
 
 
 def test_gaussian_transform_exhaustive(zo, oracle):
@@ -69,7 +78,7 @@ def test_gaussian_transform_exhaustive(zo, oracle):
     words[1::2] = (k[::-1] << 8) | rng.integers(0, 256, k.size, dtype=np.uint32)
     got = zo.debug_gauss_pairs(torch.from_numpy(words.view(np.int32)).cuda()).cpu().numpy()
     ref = oracle.gauss_pairs(words)
-    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    assert_bits_equal(got, ref, "box-muller")
 
 
 # ---------------------------------------------------------------------------
