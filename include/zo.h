@@ -115,7 +115,11 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
  *            next-token cross-entropy in nats at theta + eps z and at
  *            theta - eps z (0 when the mask selects nothing)
  *   workspace, ws_bytes  device scratch of at least zo_workspace_bytes()
- * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_ENOMEM or ZO_EDEVICE. */
+ * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_ENOMEM or ZO_EDEVICE.
+ * fp32 weights: each matrix product uses the perturbed weight tile
+ * w +- eps z formed in LDS (one fp32 rounding); with the environment variable
+ * ZO_FP32_SPLIT=1 it instead accumulates W.x and (+-x).(eps z) as two MFMA
+ * streams (same result to rounding, twice the matrix work; for measurement). */
 int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
                         int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
                         int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,

@@ -117,7 +117,17 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
 // k = 8g + s at MFMA step s, so each lane reads 8 consecutive k with two
 // 128-bit LDS loads (the order in which k is summed is free).
 //
-// LDS: A tile [64][36], W tile [128][36], eps z tile [128][36] (fp32).
+// Every 32-row wave tile lies inside one sign half of one probe's rows, so a
+// wave needs a single weight operand: W + eps z (rows of the + pass) or
+// W - eps z (rows of the - pass). The loader threads form both tiles in LDS
+// from the weight tile and the regenerated probe tile (one fp32 rounding of
+// w +- eps z), and each wave runs one MFMA stream over its own tile. The
+// split variant (kSplit) keeps W and eps z apart and runs two MFMA streams,
+// W.h and (s h).(eps z), into one accumulator (twice the MFMA work).
+//
+// Software pipeline: the next K tile's global loads and probe generation are
+// issued before the current tile's MFMAs, so their latency overlaps the
+// matrix work; LDS holds one tile (A [64][36], two weight tiles [128][36]).
 struct Seg {
   const float* A;  // row r of this tile at A + r * lda
   int64_t lda;
@@ -129,109 +139,131 @@ struct Seg {
 
 struct Smem {
   float a[BM * LDK];
-  float w[BNC * LDK];
-  float z[BNC * LDK];
+  float p[BNC * LDK];  // W + eps z (split: W)
+  float m[BNC * LDK];  // W - eps z (split: eps z)
 };
 
 // colmap(rho, &n) -> true if LDS column rho maps to a real weight row n.
-template <int kind, typename ColMap>
-__device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg& sg, ColMap colmap,
-                                             const int (&wrow)[4], int arow0,
-                                             const uint32_t (&sgn)[2], Key key, uint32_t probe,
-                                             float eps, Smem& sm) {
+template <int kind, bool kSplit, typename ColMap>
+__device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, const Seg s1,
+                                             int nseg, ColMap colmap, const int (&wrow)[4], int arow0,
+                                             bool wave_neg, Key key, uint32_t probe, float eps,
+                                             Smem& sm) {
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int g4 = lane >> 4;
-  const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
-  // this thread's Z-generation row
-  const int zr = t >> 1, zhalf = t & 1;
-  int zn;
-  const bool zok = colmap(zr, zn);
+  // loader roles: A rows (t + 256 q) >> 3, float4 column t & 7; weight row
+  // rho = t >> 1, 16 consecutive k starting at 16 * (t & 1)
+  const int rho = t >> 1, half = t & 1;
+  int wn;
+  const bool wok = colmap(rho, wn);
+  const int ntiles = s0.K / BK + (nseg > 1 ? s1.K / BK : 0);
+
+  f4 ra[2], rw[4];
+  float zv[16];
   Words zcache{{0u, 0u, 0u, 0u}};
-  for (int k0 = 0; k0 < sg.K; k0 += BK) {
-    __syncthreads();
-    // A tile: 64 x 32 floats, 2 float4 per thread
+  int seg = 0, k0 = 0;  // position of the tile being fetched
+
+  auto fetch = [&]() {
+    const Seg sg = seg == 0 ? s0 : s1;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int idx = t + 256 * q;
-      const int row = idx >> 3, c4 = idx & 7;
-      const f4 v = *(const f4*)(sg.A + (int64_t)row * sg.lda + k0 + 4 * c4);
-      *(f4*)(&sm.a[row * LDK + 4 * c4]) = v;
+      ra[q] = *(const f4*)(sg.A + (int64_t)(idx >> 3) * sg.lda + k0 + 4 * (idx & 7));
     }
-    // W tile: 128 x 32 floats, 4 float4 per thread
+    const float* wp = sg.W + (int64_t)wn * sg.ldw + k0 + 16 * half;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) rw[q] = wok ? *(const f4*)(wp + 4 * q) : f4{0.f, 0.f, 0.f, 0.f};
+    const uint64_t jrow = sg.zoff + (uint64_t)wn * (uint64_t)sg.ldw + (uint64_t)k0;
+    if constexpr (kind == ZO_RADEMACHER) {
+      uint32_t word;
+      const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
+      if (aligned) {
+        if ((k0 & 127) == 0) zcache = stream_block(key, jrow >> 7, probe, kTagRademacher);
+        const int q = (k0 >> 5) & 3;
+        word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
+      } else {
+        word = rademacher_word(key, probe, jrow >> 5);
+      }
+      word >>= 16 * half;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
+    } else {
+      const uint64_t j0 = jrow + 16 * half;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        float z4[4];
+        gauss_block(key, probe, (j0 >> 2) + b, z4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) zv[4 * b + e] = fmul(eps, z4[e]);
+      }
+    }
+    k0 += BK;
+    if (k0 == sg.K) {
+      k0 = 0;
+      ++seg;
+    }
+  };
+
+  fetch();
+  for (int it = 0; it < ntiles; ++it) {
+    __syncthreads();  // the previous tile's fragments have been read
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = t + 256 * q;
+      *(f4*)(&sm.a[(idx >> 3) * LDK + 4 * (idx & 7)]) = ra[q];
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = t + 256 * q;
-      const int rho = idx >> 3, c4 = idx & 7;
-      int n;
-      f4 v = {0.f, 0.f, 0.f, 0.f};
-      if (colmap(rho, n)) v = *(const f4*)(sg.W + (int64_t)n * sg.ldw + k0 + 4 * c4);
-      *(f4*)(&sm.w[rho * LDK + 4 * c4]) = v;
-    }
-    // eps z tile: thread (zr, zhalf) writes 16 values of row zr
-    {
-      float zv[16];
-      const uint64_t jrow = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0;
-      if constexpr (kind == ZO_RADEMACHER) {
-        uint32_t word;
-        if (aligned) {
-          if ((k0 & 127) == 0) zcache = stream_block(key, jrow >> 7, probe, kTagRademacher);
-          const int s = (k0 >> 5) & 3;
-          word = s == 0 ? zcache.w[0] : s == 1 ? zcache.w[1] : s == 2 ? zcache.w[2] : zcache.w[3];
+      f4 vp, vm;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float w = rw[q][e], z = zv[4 * q + e];
+        if constexpr (kSplit) {
+          vp[e] = w;
+          vm[e] = z;
         } else {
-          word = rademacher_word(key, probe, jrow >> 5);
-        }
-        word >>= 16 * zhalf;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
-      } else {
-        const uint64_t j0 = jrow + 16 * zhalf;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          float z4[4];
-          gauss_block(key, probe, (j0 >> 2) + b, z4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) zv[4 * b + e] = fmul(eps, z4[e]);
+          vp[e] = fadd(w, z);
+          vm[e] = fadd(w, -z);
         }
       }
-      if (!zok) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) zv[e] = 0.f;
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f4 v = {zv[4 * q], zv[4 * q + 1], zv[4 * q + 2], zv[4 * q + 3]};
-        *(f4*)(&sm.z[zr * LDK + 16 * zhalf + 4 * q]) = v;
-      }
+      *(f4*)(&sm.p[rho * LDK + 16 * half + 4 * q]) = vp;
+      *(f4*)(&sm.m[rho * LDK + 16 * half + 4 * q]) = vm;
     }
     __syncthreads();
-    // fragments
-    f4 a[2][2], w[4][2], z[4][2];
+    if (it + 1 < ntiles) fetch();  // next tile's loads and probe overlap this tile's MFMAs
+
+    f4 a[2][2], b[4][2], z[4][2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      const float* p = &sm.a[(arow0 + 16 * mt + (lane & 15)) * LDK + 8 * g4];
-      a[mt][0] = *(const f4*)p;
-      a[mt][1] = *(const f4*)(p + 4);
+      const float* pa = &sm.a[(arow0 + 16 * mt + (lane & 15)) * LDK + 8 * g4];
+      a[mt][0] = *(const f4*)pa;
+      a[mt][1] = *(const f4*)(pa + 4);
     }
+    const float* bsrc = (!kSplit && wave_neg) ? sm.m : sm.p;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float* pw = &sm.w[wrow[q] * LDK + 8 * g4];
-      const float* pz = &sm.z[wrow[q] * LDK + 8 * g4];
-      w[q][0] = *(const f4*)pw;
-      w[q][1] = *(const f4*)(pw + 4);
-      z[q][0] = *(const f4*)pz;
-      z[q][1] = *(const f4*)(pz + 4);
+      const float* pb = &bsrc[wrow[q] * LDK + 8 * g4];
+      b[q][0] = *(const f4*)pb;
+      b[q][1] = *(const f4*)(pb + 4);
+      if constexpr (kSplit) {
+        const float* pz = &sm.m[wrow[q] * LDK + 8 * g4];
+        z[q][0] = *(const f4*)pz;
+        z[q][1] = *(const f4*)(pz + 4);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const float av = a[mt][s >> 2][s & 3];
-        const float sav = __uint_as_float(__float_as_uint(av) ^ sgn[mt]);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, w[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
-          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(sav, z[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
+          acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
+          if constexpr (kSplit) {
+            const float sav = wave_neg ? -av : av;
+            acc[mt][q] = __builtin_amdgcn_mfma_f32_16x16x4f32(sav, z[q][s >> 2][s & 3], acc[mt][q], 0, 0, 0);
+          }
         }
       }
     }
@@ -262,7 +294,7 @@ struct GateArgs {
   RowMap rm;
 };
 
-template <int kind>
+template <int kind, bool kSplit>
 __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
   __shared__ Smem sm;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -278,12 +310,7 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
   int wrow[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) wrow[q] = q * 32 + 16 * wn + (lane & 15);
-  uint32_t sgn[2];
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-    const int64_t r = m0 + 32 * wm + 16 * mt + (lane & 15);
-    sgn[mt] = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp ? 0x80000000u : 0u;
-  }
+  const bool wave_neg = (m0 + 32 * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
   f4 acc[2][4];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
@@ -291,10 +318,9 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
     for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t probe = g.i0 + (uint32_t)pair;
-  Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
-  mainloop_f32<kind>(acc, s0, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
-  Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
-  mainloop_f32<kind>(acc, s1, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
+  const Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
+  const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
+  mainloop_f32<kind, kSplit>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
 
   // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
   const int u = u0 + 16 * wn + (lane & 15);
@@ -351,7 +377,7 @@ struct HeadArgs {
   float* ptgt;  // [rows]
 };
 
-template <int kind>
+template <int kind, bool kSplit>
 __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
   __shared__ Smem sm;
   __shared__ float red_m[2][BM], red_s[2][BM];
@@ -373,20 +399,15 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
   int wrow[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) wrow[q] = 64 * wn + 16 * q + (lane & 15);
-  uint32_t sgn[2];
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-    const int64_t r = r0 + 32 * wm + 16 * mt + (lane & 15);
-    sgn[mt] = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp ? 0x80000000u : 0u;
-  }
+  const bool wave_neg = (r0 + 32 * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
   f4 acc[2][4];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
   const uint32_t probe = g.i0 + (uint32_t)pair;
-  Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
-  mainloop_f32<kind>(acc, s0, colmap, wrow, 32 * wm, sgn, g.key, probe, g.eps, sm);
+  const Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
+  mainloop_f32<kind, kSplit>(acc, s0, s0, 1, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
 
   const float* bout = g.theta + g.off_b;
   const float* zbo = g.zbo + (int64_t)pair * V;
@@ -550,6 +571,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     ZO_TRY(hipGetLastError());
   }
 
+  const bool split = a.fp32_split;
   const int T = W.T;
   for (int t = 0; t < a.C; ++t) {
     {
@@ -590,8 +612,13 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
       g.rm = rm;
       const dim3 grid((unsigned)(H / 32), (unsigned)(M / BM));
       ProfScope ps(kKGate, st);
-      if (c.probe == ZO_RADEMACHER) gate_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(g);
-      else gate_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(g);
+      if (c.probe == ZO_RADEMACHER) {
+        if (split) gate_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(g);
+        else gate_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(g);
+      } else {
+        if (split) gate_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(g);
+        else gate_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(g);
+      }
       ZO_TRY(hipGetLastError());
       xin = g.hout;
     }
@@ -622,8 +649,13 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
       const dim3 grid((unsigned)W.nvt, (unsigned)(h.rows / BM));
       {
         ProfScope ps(kKHead, st);
-        if (c.probe == ZO_RADEMACHER) head_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(h);
-        else head_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(h);
+        if (c.probe == ZO_RADEMACHER) {
+          if (split) head_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(h);
+          else head_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(h);
+        } else {
+          if (split) head_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(h);
+          else head_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(h);
+        }
       }
       ZO_TRY(hipGetLastError());
       ProfScope ps(kKCombine, st);

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 
 #include "../../include/zo.h"
@@ -108,6 +109,8 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   a.Lplus = Lplus;
   a.Lminus = Lminus;
   a.work = (char*)workspace;
+  const char* split = std::getenv("ZO_FP32_SPLIT");
+  a.fp32_split = split && split[0] == '1';
   return device_status(zo::launch_forward(a, (hipStream_t)stream), "zo_perturbed_losses");
 }
 

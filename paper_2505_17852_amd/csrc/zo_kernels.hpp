@@ -35,6 +35,7 @@ struct ForwardArgs {
   float* Lplus;
   float* Lminus;
   char* work;
+  bool fp32_split;  // fp32 path: separate W.h and probe MFMA streams (measurement variant)
 };
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
 
