@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libzo.so")
 OBJ = os.path.join(HERE, "_build")
-SOURCES = ["zo_api.hip", "zo_profile.hip", "k_rng.hip", "k_forward.hip"]
+SOURCES = ["zo_api.hip", "zo_profile.hip", "k_rng.hip", "k_forward.hip", "k_forward_bf16.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -32,14 +32,9 @@ constexpr int BNC = 128;  // columns per workgroup tile
 constexpr int BK = 32;    // K per LDS tile
 constexpr int LDK = BK + 4;
 
-static_assert(BM % kRowGranule == 0 || kRowGranule % BM == 0, "row tiles must stay inside a pass pair");
-static_assert(2 * kRowGranule % BM == 0, "a probe's rows must be a whole number of row tiles");
+static_assert(2 * kRowGranuleF32 % BM == 0, "a probe's rows must be a whole number of row tiles");
+static_assert(kRowGranuleF32 % 32 == 0, "a 32-row wave tile must lie inside one sign");
 static_assert(BNC == kVocabTile, "head vocabulary tile");
-
-struct RowMap {
-  int Bp;
-  int64_t pair_rows;
-};
 
 // ---------------------------------------------------------------------------
 // Bias probes: zb[l][n][c] = eps z_{i0+n}[bias_l + c], zbo[n][v] = eps z[b_out + v]
@@ -527,19 +522,116 @@ __global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int
 
 }  // namespace
 
+namespace {
+
+hipError_t launch_embed_f32(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
+  const Rows& R = a.rows;
+  const int E = a.cfg.embed;
+  const RowMap rm{R.Bp, R.pair_rows};
+  const int64_t n = R.M * (E / 4);
+  const unsigned grid = (unsigned)((n + 255) / 256);
+  const Key key = make_key(a.seed);
+  ProfScope ps(kKEmbed, st);
+  if (a.cfg.probe == ZO_RADEMACHER)
+    embed_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
+                                                          a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
+                                                          a.eps, (float*)x0);
+  else
+    embed_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
+                                                        a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
+                                                        a.eps, (float*)x0);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_f32(const ForwardArgs& a, int l, const void* x, const void* hprev, void* hout,
+                           float* cst, const float* zb, hipStream_t st) {
+  const Rows& R = a.rows;
+  GateArgs g;
+  g.x = (const float*)x;
+  g.hprev = (const float*)hprev;
+  g.hout = (float*)hout;
+  g.cst = cst;
+  g.theta = (const float*)a.theta;
+  g.off_ih = a.lay.w_ih[l];
+  g.off_hh = a.lay.w_hh[l];
+  g.off_b = a.lay.bias[l];
+  g.El = l == 0 ? a.cfg.embed : a.cfg.hidden;
+  g.H = a.cfg.hidden;
+  g.zb = zb;
+  g.key = make_key(a.seed);
+  g.i0 = a.i0;
+  g.eps = a.eps;
+  g.rm = RowMap{R.Bp, R.pair_rows};
+  const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / BM));
+  const bool split = a.fp32_split;
+  ProfScope ps(kKGate, st);
+  if (a.cfg.probe == ZO_RADEMACHER) {
+    if (split) gate_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(g);
+    else gate_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(g);
+  } else {
+    if (split) gate_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(g);
+    else gate_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(g);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_head_f32(const ForwardArgs& a, const void* hist, int t0, int Tc, const float* zbo,
+                           float* pmax, float* psum, float* ptgt, hipStream_t st) {
+  const Rows& R = a.rows;
+  HeadArgs h;
+  h.h = (const float*)hist;
+  h.theta = (const float*)a.theta;
+  h.off_w = a.lay.w_out;
+  h.off_b = a.lay.b_out;
+  h.H = a.cfg.hidden;
+  h.V = a.cfg.vocab;
+  h.zbo = zbo;
+  h.key = make_key(a.seed);
+  h.i0 = a.i0;
+  h.eps = a.eps;
+  h.rm = RowMap{R.Bp, R.pair_rows};
+  h.M = R.M;
+  h.rows = (int64_t)Tc * R.M;
+  h.tokens = a.tokens;
+  h.C = a.C;
+  h.t0 = t0;
+  h.B = R.B;
+  h.pmax = pmax;
+  h.psum = psum;
+  h.ptgt = ptgt;
+  const dim3 grid((unsigned)a.ws.nvt, (unsigned)(h.rows / BM));
+  const bool split = a.fp32_split;
+  ProfScope ps(kKHead, st);
+  if (a.cfg.probe == ZO_RADEMACHER) {
+    if (split) head_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(h);
+    else head_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(h);
+  } else {
+    if (split) head_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(h);
+    else head_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(h);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// The step driver: per timestep the perturbed embedding and one gate launch
+// per layer; per time chunk one head launch and one combine; then the
+// per-pass reduction. The fp32 and bf16 paths differ only in their embed,
+// gate and head kernels.
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   const zo_config& c = a.cfg;
-  const int L = c.n_layers, H = c.hidden, E = c.embed, V = c.vocab;
+  const bool bf16 = c.wdtype == ZO_WBF16;
+  const int L = c.n_layers, H = c.hidden, V = c.vocab;
   const Rows& R = a.rows;
   const WsPlan& W = a.ws;
   const int64_t M = R.M;
-  const Key key = make_key(a.seed);
+  const size_t el = bf16 ? 2 : 4;  // activation element size
+  const size_t state = (size_t)M * H * el;
   const RowMap rm{R.Bp, R.pair_rows};
-  const float* theta = (const float*)a.theta;
   char* ws = a.work;
-  float* x0 = (float*)(ws + W.x0);
-  float* hbuf = (float*)(ws + W.hbuf);
-  float* hist = (float*)(ws + W.hist);
+  char* x0 = ws + W.x0;
+  char* hbuf = ws + W.hbuf;
+  char* hist = ws + W.hist;
   float* cbuf = (float*)(ws + W.cbuf);
   float* zb = (float*)(ws + W.zb);
   float* zbo = (float*)(ws + W.zbo);
@@ -547,15 +639,18 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   float* psum = (float*)(ws + W.psum);
   float* ptgt = (float*)(ws + W.ptgt);
   double* row_loss = (double*)(ws + W.row_loss);
+  auto embed = bf16 ? launch_embed_bf16 : launch_embed_f32;
+  auto gate = bf16 ? launch_gate_bf16 : launch_gate_f32;
+  auto head = bf16 ? launch_head_bf16 : launch_head_f32;
   hipError_t e;
-#define ZO_TRY(x)                       \
-  do {                                  \
+#define ZO_TRY(x)                          \
+  do {                                     \
     if ((e = (x)) != hipSuccess) return e; \
   } while (0)
 
   // zero initial states (every pass starts from h = c = 0) and the row sums
-  if (L > 1) ZO_TRY(hipMemsetAsync(hbuf, 0, (size_t)(L - 1) * 2 * M * H * 4, st));
-  ZO_TRY(hipMemsetAsync(hist, 0, (size_t)W.T * M * H * 4, st));
+  if (L > 1) ZO_TRY(hipMemsetAsync(hbuf, 0, (size_t)(L - 1) * 2 * state, st));
+  ZO_TRY(hipMemsetAsync(hist, 0, (size_t)W.T * state, st));
   ZO_TRY(hipMemsetAsync(cbuf, 0, (size_t)L * M * H * 4, st));
   ZO_TRY(hipMemsetAsync(row_loss, 0, (size_t)M * 8, st));
 
@@ -566,101 +661,37 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     const int64_t total = (int64_t)R.N * 4 * H * L + (int64_t)R.N * V;
     int64_t grid = (total + 255) / 256;
     if (grid > 65536) grid = 65536;
-    prep_bias_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>(c.probe, key, a.i0, a.eps, R.N, L,
-                                                                4 * H, V, boff, a.lay.b_out, zb, zbo);
+    prep_bias_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>(c.probe, make_key(a.seed), a.i0,
+                                                                a.eps, R.N, L, 4 * H, V, boff,
+                                                                a.lay.b_out, zb, zbo);
     ZO_TRY(hipGetLastError());
   }
 
-  const bool split = a.fp32_split;
   const int T = W.T;
   for (int t = 0; t < a.C; ++t) {
-    {
-      const int64_t n = M * (E / 4);
-      const unsigned grid = (unsigned)((n + 255) / 256);
-      ProfScope ps(kKEmbed, st);
-      if (c.probe == ZO_RADEMACHER)
-        embed_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>(theta, a.lay.emb, E, a.tokens, a.C, t,
-                                                              R.B, rm, M, key, a.i0, a.eps, x0);
-      else
-        embed_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>(theta, a.lay.emb, E, a.tokens, a.C, t,
-                                                            R.B, rm, M, key, a.i0, a.eps, x0);
-      ZO_TRY(hipGetLastError());
-    }
-    const float* xin = x0;
+    ZO_TRY(embed(a, t, x0, st));
+    const char* xin = x0;
     for (int l = 0; l < L; ++l) {
-      GateArgs g;
-      g.x = xin;
+      char* hprev;
+      char* hout;
       if (l < L - 1) {
-        float* base = hbuf + (size_t)l * 2 * M * H;
-        g.hprev = base + (size_t)((t + 1) & 1) * M * H;
-        g.hout = base + (size_t)(t & 1) * M * H;
+        char* base = hbuf + (size_t)l * 2 * state;
+        hprev = base + (size_t)((t + 1) & 1) * state;
+        hout = base + (size_t)(t & 1) * state;
       } else {
-        g.hprev = hist + (size_t)((t + T - 1) % T) * M * H;
-        g.hout = hist + (size_t)(t % T) * M * H;
+        hprev = hist + (size_t)((t + T - 1) % T) * state;
+        hout = hist + (size_t)(t % T) * state;
       }
-      g.cst = cbuf + (size_t)l * M * H;
-      g.theta = theta;
-      g.off_ih = a.lay.w_ih[l];
-      g.off_hh = a.lay.w_hh[l];
-      g.off_b = a.lay.bias[l];
-      g.El = l == 0 ? E : H;
-      g.H = H;
-      g.zb = zb + (size_t)l * R.N * 4 * H;
-      g.key = key;
-      g.i0 = a.i0;
-      g.eps = a.eps;
-      g.rm = rm;
-      const dim3 grid((unsigned)(H / 32), (unsigned)(M / BM));
-      ProfScope ps(kKGate, st);
-      if (c.probe == ZO_RADEMACHER) {
-        if (split) gate_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(g);
-        else gate_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(g);
-      } else {
-        if (split) gate_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(g);
-        else gate_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(g);
-      }
-      ZO_TRY(hipGetLastError());
-      xin = g.hout;
+      ZO_TRY(gate(a, l, xin, hprev, hout, cbuf + (size_t)l * M * H, zb + (size_t)l * R.N * 4 * H, st));
+      xin = hout;
     }
     if (t % T == T - 1 || t == a.C - 1) {
       const int t0 = t - t % T;
       const int Tc = t - t0 + 1;
-      HeadArgs h;
-      h.h = hist;
-      h.theta = theta;
-      h.off_w = a.lay.w_out;
-      h.off_b = a.lay.b_out;
-      h.H = H;
-      h.V = V;
-      h.zbo = zbo;
-      h.key = key;
-      h.i0 = a.i0;
-      h.eps = a.eps;
-      h.rm = rm;
-      h.M = M;
-      h.rows = (int64_t)Tc * M;
-      h.tokens = a.tokens;
-      h.C = a.C;
-      h.t0 = t0;
-      h.B = R.B;
-      h.pmax = pmax;
-      h.psum = psum;
-      h.ptgt = ptgt;
-      const dim3 grid((unsigned)W.nvt, (unsigned)(h.rows / BM));
-      {
-        ProfScope ps(kKHead, st);
-        if (c.probe == ZO_RADEMACHER) {
-          if (split) head_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(h);
-          else head_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(h);
-        } else {
-          if (split) head_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(h);
-          else head_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(h);
-        }
-      }
-      ZO_TRY(hipGetLastError());
+      ZO_TRY(head(a, hist, t0, Tc, zbo, pmax, psum, ptgt, st));
       ProfScope ps(kKCombine, st);
       combine_kernel<<<dim3((unsigned)((M + 255) / 256)), 256, 0, st>>>(
-          pmax, psum, ptgt, W.nvt, h.rows, M, Tc, t0, a.C, R.B, rm, a.mask, row_loss);
+          pmax, psum, ptgt, W.nvt, (int64_t)Tc * M, M, Tc, t0, a.C, R.B, rm, a.mask, row_loss);
       ZO_TRY(hipGetLastError());
     }
   }

@@ -43,6 +43,9 @@ int check_config(const zo_config* c) {
   if (c->embed % 32 || c->hidden % 32)
     return fail(ZO_ESHAPE, "embed (%d) and hidden (%d) must be multiples of 32", c->embed,
                 c->hidden);
+  if (c->wdtype == ZO_WBF16 && (c->embed % 64 || c->hidden % 64))
+    return fail(ZO_ESHAPE, "bf16 weights: embed (%d) and hidden (%d) must be multiples of 64",
+                c->embed, c->hidden);
   return ZO_OK;
 }
 
@@ -59,7 +62,7 @@ size_t zo_param_count(const zo_config* cfg) {
 
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
   if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1) return 0;
-  const zo::Rows r = zo::make_rows(N, B);
+  const zo::Rows r = zo::make_rows(N, B, zo::row_granule(*cfg));
   return zo::plan_workspace(*cfg, r, C).total;
 }
 
@@ -79,8 +82,6 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
                         size_t ws_bytes, void* stream) {
   int st = check_config(cfg);
   if (st) return st;
-  if (cfg->wdtype != ZO_WFP32)
-    return fail(ZO_ESHAPE, "bf16 weights are not supported by this build of the forward");
   if (!theta || !tokens || !Lplus || !Lminus || !workspace)
     return fail(ZO_EINVAL, "a required pointer is NULL");
   if (!aligned16(theta) || !aligned16(workspace))
@@ -89,7 +90,7 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   if (N < 1 || B < 1 || C < 1) return fail(ZO_EINVAL, "N, B and C must be >= 1");
   if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
     return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
-  const zo::Rows rows = zo::make_rows(N, B);
+  const zo::Rows rows = zo::make_rows(N, B, zo::row_granule(*cfg));
   if (rows.M > (int64_t)1 << 30) return fail(ZO_ESHAPE, "2N*B rows too large");
   const zo::WsPlan plan = zo::plan_workspace(*cfg, rows, C);
   if (ws_bytes < plan.total)

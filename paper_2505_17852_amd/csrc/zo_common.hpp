@@ -55,10 +55,16 @@ inline Layout make_layout(const zo_config& c) {
 // Rows of the batched forward. The 2N passes (probe n, sign s) each run the
 // B sequences; every matrix product of a timestep covers all of them at once.
 // Row r = (2 n + sidx) * Bp + b with sidx 0 for +eps and 1 for -eps; B is
-// padded to Bp (a multiple of kRowGranule) so that every row tile of a
-// kernel lies inside one probe's rows. Padded rows (b >= B) carry zeros in,
-// are computed like the others and never scored.
-constexpr int kRowGranule = 32;
+// padded to Bp (a multiple of the path's row granule) so that every row tile
+// of a kernel lies inside one probe's rows (and, for the fp32 path, every
+// 32-row wave tile inside one sign). Padded rows (b >= B) carry zeros in, are
+// computed like the others and never scored.
+constexpr int kRowGranuleF32 = 32;   // fp32 path: 64-row tiles, 32-row wave tiles
+constexpr int kRowGranuleBF16 = 128; // bf16 path: 256-row tiles
+
+inline int row_granule(const zo_config& c) {
+  return c.wdtype == ZO_WBF16 ? kRowGranuleBF16 : kRowGranuleF32;
+}
 
 struct Rows {
   int32_t B, Bp, N;
@@ -66,11 +72,16 @@ struct Rows {
   int64_t M;          // N * 2 Bp
 };
 
-inline Rows make_rows(int32_t N, int32_t B) {
+struct RowMap {
+  int Bp;
+  int64_t pair_rows;
+};
+
+inline Rows make_rows(int32_t N, int32_t B, int granule) {
   Rows r;
   r.B = B;
   r.N = N;
-  r.Bp = (B + kRowGranule - 1) / kRowGranule * kRowGranule;
+  r.Bp = (B + granule - 1) / granule * granule;
   r.pair_rows = 2 * (int64_t)r.Bp;
   r.M = (int64_t)N * r.pair_rows;
   return r;

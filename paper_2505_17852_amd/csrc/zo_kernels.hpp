@@ -39,4 +39,11 @@ struct ForwardArgs {
 };
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
 
+// k_forward_bf16.hip: the bf16 path's per-timestep kernels.
+hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t st);
+hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const void* hprev, void* hout,
+                            float* cst, const float* zb, hipStream_t st);
+hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int Tc, const float* zbo,
+                            float* pmax, float* psum, float* ptgt, hipStream_t st);
+
 }  // namespace zo

@@ -1,0 +1,131 @@
+"""bf16 path (bf16 weights and matrix operands, fp32 accumulation and cell
+state) vs the fp64 CPU oracle, through the C ABI.
+
+Bar: per-pass losses within 2e-2 relative. The oracle perturbs and runs in
+fp64; the GPU keeps the probe term of every product at fp32 precision but
+rounds the states h and the perturbed embeddings to bf16 between steps.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from paper_2505_17852_amd import workloads as wl  # noqa: E402
+
+LOSS_RTOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module")
+def zo():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_17852_amd import zo as z
+    z.lib()
+    return z
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def run_pair(zo, oracle, cfg, N, tok, mask, eps, i0=0, seed=555, init_seed=91, ref_tok=None,
+             ref_mask=None, ref_i0=None, ref_N=None):
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, init_seed)
+    td = torch.from_numpy(np.ascontiguousarray(tok)).cuda()
+    md = None if mask is None else torch.from_numpy(np.ascontiguousarray(mask)).cuda()
+    Lp, Lm = zo.perturbed_losses(cfg, theta, seed, eps, N, td, md, i0=i0)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    del theta
+    ref_theta = oracle.init(cfg, init_seed)
+    rt = tok if ref_tok is None else ref_tok
+    rmk = mask if ref_tok is None else ref_mask
+    rN = N if ref_N is None else ref_N
+    ri0 = i0 if ref_i0 is None else ref_i0
+    rp, rm = oracle.perturbed_losses(cfg, ref_theta, seed, eps, rN, rt, rmk, i0=ri0, as_double=True)
+    return gp, gm, rp, rm
+
+
+def check(gp, gm, rp, rm, tol=LOSS_RTOL_BF16):
+    ep = np.abs(gp - rp) / np.abs(rp)
+    em = np.abs(gm - rm) / np.abs(rm)
+    say(f"gpu L+ {gp} L- {gm}\noracle L+ {rp} L- {rm}\nmax rel err {max(ep.max(), em.max()):.3e}")
+    assert ep.max() <= tol and em.max() <= tol
+
+
+CASES = [
+    # several unit tiles (H=128), a ragged vocabulary (300 = 2 tiles + 44), B=5
+    # (padded to 128 rows per sign), C=20 (a full and a partial time chunk)
+    ("rad-ragged", dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=1, probe=0), 2, 5, 20, 1e-2, True),
+    ("gauss", dict(n_layers=2, vocab=200, embed=128, hidden=64, wdtype=1, probe=1), 2, 3, 9, 1e-2, True),
+    ("deep3-rad", dict(n_layers=3, vocab=130, embed=64, hidden=192, wdtype=1, probe=0), 3, 2, 7, 1e-3, False),
+]
+
+
+@pytest.mark.parametrize("name,cfg,N,B,C,eps,masked", CASES, ids=[c[0] for c in CASES])
+def test_bf16_losses_match_oracle(zo, oracle, name, cfg, N, B, C, eps, masked):
+    say(f"bf16 losses {name} cfg={cfg} N={N} B={B} C={C}")
+    rng = np.random.default_rng(17)
+    tok = wl.uniform_tokens(rng, B, C, cfg["vocab"])
+    mask = (rng.random((B, C)) < 0.7).astype(np.uint8) if masked else None
+    check(*run_pair(zo, oracle, cfg, N, tok, mask, eps, i0=2))
+
+
+@pytest.mark.parametrize("name", ["c3", "c4"])
+def test_bf16_real_widths_short(zo, oracle, name):
+    """The real layer widths and vocabulary (1024 / 4096 hidden, 50,000 ids)
+    on a short batch: B=2, C=3, one probe."""
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    tok, _ = wl.batch(name, B=2, C=3)
+    say(f"{name} widths: B=2 C=3 N=1")
+    check(*run_pair(zo, oracle, cfg, 1, tok, None, w["eps"], i0=5))
+
+
+def test_bf16_slice_and_determinism(zo):
+    cfg = dict(n_layers=2, vocab=256, embed=64, hidden=64, wdtype=1, probe=0)
+    rng = np.random.default_rng(3)
+    tok = wl.uniform_tokens(rng, 4, 11, 256)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 8)
+    td = torch.from_numpy(tok).cuda()
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 4, 1e-3, 5, td)
+    Lp2, Lm2 = zo.perturbed_losses(cfg, theta, 4, 1e-3, 5, td)
+    assert torch.equal(Lp, Lp2) and torch.equal(Lm, Lm2)
+    sp, sm = zo.perturbed_losses(cfg, theta, 4, 1e-3, 2, td, i0=3)
+    assert torch.equal(sp, Lp[3:5]) and torch.equal(sm, Lm[3:5])
+
+
+def test_c4_full_size_sampled(zo, oracle):
+    """c4 at its full launch configuration (N=16, B=256, C=1024) with a mask
+    that scores only the first positions of two sequences; causality makes
+    those losses computable by the oracle on the 2-sequence, 3-position
+    prefix. Probes 0 and 15 (first and last row block) are checked."""
+    name = "c4"
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tok, _ = wl.batch(name)
+    B, C = tok.shape[0], tok.shape[1] - 1
+    mask = np.zeros((B, C), np.uint8)
+    mask[0, :3] = 1
+    mask[1, :2] = 1
+    say(f"c4 full size N={w['N']} B={B} C={C}, sampled positions")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    td = torch.from_numpy(tok).cuda()
+    md = torch.from_numpy(mask).cuda()
+    Lp, Lm = zo.perturbed_losses(cfg, theta, sd["step"], w["eps"], w["N"], td, md)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    del theta
+    torch.cuda.empty_cache()
+    assert np.all(np.isfinite(gp)) and np.all(np.isfinite(gm))
+    ref_theta = oracle.init(cfg, sd["init"])
+    ref_tok = np.ascontiguousarray(tok[:2, :4])
+    ref_mask = np.ascontiguousarray(mask[:2, :3])
+    for i in (0, w["N"] - 1):
+        rp, rm = oracle.perturbed_losses(cfg, ref_theta, sd["step"], w["eps"], 1, ref_tok, ref_mask,
+                                         i0=i, as_double=True)
+        check(gp[i:i + 1], gm[i:i + 1], rp, rm)
