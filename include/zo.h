@@ -69,8 +69,9 @@ typedef enum {
 enum { ZO_WFP32 = 0, ZO_WBF16 = 1 };
 enum { ZO_RADEMACHER = 0, ZO_GAUSSIAN = 1 };
 
-/* Model shape. All fields > 0; embed and hidden must be multiples of 32, and
- * of 64 for bf16 weights (ZO_ESHAPE otherwise); n_layers <= 64. wdtype: ZO_WFP32 or ZO_WBF16
+/* Model shape. All fields > 0; embed and hidden must be multiples of 32
+ * (ZO_ESHAPE otherwise), and for zo_perturbed_losses with bf16 weights
+ * multiples of 64; n_layers <= 64. wdtype: ZO_WFP32 or ZO_WBF16
  * (storage type of theta; bf16 runs the matrix products in bf16 with fp32
  * accumulation and fp32 cell state). probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
 typedef struct {

@@ -464,31 +464,47 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Adds the cross-entropy of every scored position of the chunk to its row:
-// logsumexp over the vocabulary tiles' partials minus the target logit.
+// Cross-entropy of every position of the chunk: logsumexp over the
+// vocabulary tiles' (max, sum of exp) partials, merged online in tile order,
+// minus the target logit. One thread per (timestep, row); the loss replaces
+// the target logit in ptgt (0 for unscored positions and padding rows).
 __global__ __launch_bounds__(256) void combine_kernel(const float* pmax, const float* psum,
-                                                      const float* ptgt, int nvt, int64_t rows,
-                                                      int64_t M, int Tc, int t0, int C, int B,
-                                                      RowMap rm, const uint8_t* mask,
-                                                      double* row_loss) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= M) return;
+                                                      float* ptgt, int nvt, int64_t rows,
+                                                      int64_t M, int t0, int C, int B, RowMap rm,
+                                                      const uint8_t* mask) {
+  const int64_t rr = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (rr >= rows) return;
+  const int tt = (int)(rr / M);
+  const int64_t r = rr - (int64_t)tt * M;
   const int64_t loc = r % rm.pair_rows;
   const int b = (int)(loc >= rm.Bp ? loc - rm.Bp : loc);
-  if (b >= B) return;
-  double acc = row_loss[r];
-  for (int tt = 0; tt < Tc; ++tt) {
-    if (mask && !mask[(int64_t)b * C + t0 + tt]) continue;
-    const int64_t rr = (int64_t)tt * M + r;
-    float mx = -INFINITY;
-    for (int v = 0; v < nvt; ++v) mx = fmaxf(mx, pmax[(int64_t)v * rows + rr]);
-    float s = 0.f;
-    for (int v = 0; v < nvt; ++v) {
-      const float m = pmax[(int64_t)v * rows + rr];
-      if (m != -INFINITY) s += psum[(int64_t)v * rows + rr] * expf(m - mx);
-    }
-    acc += (double)(mx + logf(s) - ptgt[rr]);
+  if (b >= B || (mask && !mask[(int64_t)b * C + t0 + tt])) {
+    ptgt[rr] = 0.f;
+    return;
   }
+  float mx = -INFINITY, s = 0.f;
+  for (int v = 0; v < nvt; ++v) {
+    const float m = pmax[(int64_t)v * rows + rr];
+    const float e = psum[(int64_t)v * rows + rr];
+    if (m == -INFINITY) continue;
+    if (m > mx) {
+      s = s * expf(mx - m) + e;
+      mx = m;
+    } else {
+      s += e * expf(m - mx);
+    }
+  }
+  ptgt[rr] = mx + logf(s) - ptgt[rr];
+}
+
+// Adds the chunk's per-position losses to each row's running sum, in time
+// order (a fixed summation order: the result does not depend on scheduling).
+__global__ __launch_bounds__(256) void accumulate_kernel(const float* ell, int64_t M, int Tc,
+                                                         double* row_loss) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= M) return;
+  double acc = row_loss[r];
+  for (int tt = 0; tt < Tc; ++tt) acc += (double)ell[(int64_t)tt * M + r];
   row_loss[r] = acc;
 }
 
@@ -690,8 +706,11 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
       const int Tc = t - t0 + 1;
       ZO_TRY(head(a, hist, t0, Tc, zbo, pmax, psum, ptgt, st));
       ProfScope ps(kKCombine, st);
-      combine_kernel<<<dim3((unsigned)((M + 255) / 256)), 256, 0, st>>>(
-          pmax, psum, ptgt, W.nvt, (int64_t)Tc * M, M, Tc, t0, a.C, R.B, rm, a.mask, row_loss);
+      const int64_t rows = (int64_t)Tc * M;
+      combine_kernel<<<dim3((unsigned)((rows + 255) / 256)), 256, 0, st>>>(
+          pmax, psum, ptgt, W.nvt, rows, M, t0, a.C, R.B, rm, a.mask);
+      ZO_TRY(hipGetLastError());
+      accumulate_kernel<<<dim3((unsigned)((M + 255) / 256)), 256, 0, st>>>(ptgt, M, Tc, row_loss);
       ZO_TRY(hipGetLastError());
     }
   }

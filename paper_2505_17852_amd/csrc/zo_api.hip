@@ -43,9 +43,6 @@ int check_config(const zo_config* c) {
   if (c->embed % 32 || c->hidden % 32)
     return fail(ZO_ESHAPE, "embed (%d) and hidden (%d) must be multiples of 32", c->embed,
                 c->hidden);
-  if (c->wdtype == ZO_WBF16 && (c->embed % 64 || c->hidden % 64))
-    return fail(ZO_ESHAPE, "bf16 weights: embed (%d) and hidden (%d) must be multiples of 64",
-                c->embed, c->hidden);
   return ZO_OK;
 }
 
@@ -82,6 +79,10 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
                         size_t ws_bytes, void* stream) {
   int st = check_config(cfg);
   if (st) return st;
+  // the bf16 forward walks K in tiles of 64
+  if (cfg->wdtype == ZO_WBF16 && (cfg->embed % 64 || cfg->hidden % 64))
+    return fail(ZO_ESHAPE, "bf16 weights: embed (%d) and hidden (%d) must be multiples of 64",
+                cfg->embed, cfg->hidden);
   if (!theta || !tokens || !Lplus || !Lminus || !workspace)
     return fail(ZO_EINVAL, "a required pointer is NULL");
   if (!aligned16(theta) || !aligned16(workspace))

@@ -80,6 +80,7 @@ def test_argument_errors_before_any_device_work(zo):
     assert _call_losses(zo, dict(cfg, probe=7)) == zo.ZO_EINVAL
     assert _call_losses(zo, dict(cfg, hidden=48)) == zo.ZO_ESHAPE
     assert _call_losses(zo, dict(cfg, embed=20)) == zo.ZO_ESHAPE
+    assert _call_losses(zo, dict(cfg, wdtype=1, hidden=96)) == zo.ZO_ESHAPE  # bf16: K tiles of 64
     assert _call_losses(zo, cfg, eps=0.0) == zo.ZO_EINVAL
     assert _call_losses(zo, cfg, eps=float("nan")) == zo.ZO_EINVAL
     assert _call_losses(zo, cfg, N=0) == zo.ZO_EINVAL
