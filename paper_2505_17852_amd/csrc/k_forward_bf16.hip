@@ -198,6 +198,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
     }
   };
 
+  // Fragments of one 16-k step: activations (2 row tiles), weights and probe
+  // values (2 column tiles). The next step's LDS reads and sign expansion are
+  // issued between the current step's MFMAs (software pipelining within the
+  // K tile), so the matrix pipe is fed while the VALU and LDS work proceeds.
+  struct Frag {
+    bf8 a[2], w[2], z[2];
+  };
   auto compute = [&](int b) {
     const uint16_t* pa = sa(b) + (64 * wm + lr) * LDB + 8 * lg;
     const uint16_t* pw = sw(b) + (64 * wn + lr) * LDB + 8 * lg;
@@ -213,30 +220,45 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
         bits[nt][1] = v.y << pre;
       }
     }
+    auto load = [&](int s, Frag& f) {
 #pragma unroll
-    for (int s = 0; s < TK / 16; ++s) {
-      bf8 a[2], w[2], z[2];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * LDB + 16 * s));
+      for (int mt = 0; mt < 2; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * LDB + 16 * s));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * LDB + 16 * s));
+        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * LDB + 16 * s));
         if constexpr (kind == ZO_RADEMACHER) {
           const uint32_t x = bits[nt][s >> 1];
           u4 v;
 #pragma unroll
           for (int d = 0; d < 4; ++d) v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) | 0x3F803F80u;
-          z[nt] = as_bf8(v);
+          f.z[nt] = as_bf8(v);
         } else {
-          z[nt] = as_bf8(*(const u4*)(sz(b) + (64 * wn + 32 * nt + lr) * LDB + 16 * s + 8 * lg));
+          f.z[nt] = as_bf8(*(const u4*)(sz(b) + (64 * wn + 32 * nt + lr) * LDB + 16 * s + 8 * lg));
         }
       }
+    };
+    Frag f[2];
+    load(0, f[0]);
+#pragma unroll
+    for (int s = 0; s < TK / 16; ++s) {
+      const Frag& c = f[s & 1];
+      if (s + 1 < TK / 16) load(s + 1, f[(s + 1) & 1]);
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
-          accW[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], w[nt], accW[mt][nt], 0, 0, 0);
-          accZ[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], z[nt], accZ[mt][nt], 0, 0, 0);
+          accW[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], accW[mt][nt], 0, 0, 0);
+          accZ[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], accZ[mt][nt], 0, 0, 0);
+        }
+      }
+      if (s + 1 < TK / 16) {
+        // per step: the next step's LDS reads first, then each MFMA followed by
+        // a few VALU instructions of the next step's sign expansion
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
         }
       }
     }
