@@ -44,6 +44,34 @@ def gate_flops(cfg, N, B):
     return sum(2 * rows * 4 * H * ((E if l == 0 else H) + H) for l in range(L))
 
 
+def kernel_source_hash(dtype):
+    """Hash of the gate kernel's sources, to match the committed counter runs."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2505_17852_amd", "csrc")
+    files = ["k_forward_bf16.hip" if dtype == "bf16" else "k_forward.hip", "zo_rng.hpp", "zo_common.hpp"]
+    m = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(src, f), "rb") as fh:
+            m.update(fh.read())
+    return m.hexdigest()[:16]
+
+
+def measured_traffic(name, dtype):
+    """HBM bytes (read + write) per gate launch from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs, if they were taken on the current kernel
+    sources; None otherwise."""
+    path = os.path.join(ROOT, "profiles", "gate_traffic_c4_c2.md")
+    if not os.path.exists(path):
+        return None
+    want = kernel_source_hash(dtype)
+    with open(path) as fh:
+        for line in fh:
+            parts = line.split()
+            if len(parts) == 5 and parts[0] == "traffic" and parts[1] == name and parts[2] == want:
+                return float(parts[3]) + float(parts[4])
+    return None
+
+
 def cpu_baseline(name, budget_s=20.0):
     """The oracle on the host cores, on a bounded sample of the workload:
     the full batch with the first N' probes (N' doubling until the budget is
@@ -174,7 +202,8 @@ def main():
                    "params": zo.param_count(cfg), "eps": eps, "lr": lr},
         "roofline": {"bound": "mfma", "kernel": "gate (fused LSTM layer step)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": None if achieved is None else achieved / peak, "traffic": None,
+                     "frac": None if achieved is None else achieved / peak,
+                     "traffic": measured_traffic(name, dtype),
                      "flops_per_launch": fl_launch,
                      # the bf16 kernels run the weight and probe products as two MFMA
                      # streams: executed matrix work is twice the algorithmic work

@@ -251,3 +251,30 @@ def test_c2_full_size_first_probe(zo, oracle):
     assert abs(gp[0] - rp[0]) <= LOSS_RTOL * abs(rp[0])
     assert abs(gm[0] - rm[0]) <= LOSS_RTOL * abs(rm[0])
     assert np.all(np.isfinite(gp)) and np.all(np.isfinite(gm))
+
+
+# ---------------------------------------------------------------------------
+# the estimator's signal: L+ - L- per probe (what the update consumes)
+
+@pytest.mark.parametrize("name,B,C", [("c1", 4, 32), ("c5", 4, 16), ("c2", 4, 140)])
+def test_delta_loss_matches_oracle(zo, oracle, name, B, C):
+    """L+_n - L-_n agrees with the oracle's to within the fp32 spacing of the
+    losses themselves (8 ulp of L) plus 1e-4 relative: the forward loses no
+    resolution beyond the fp32 rounding of its outputs."""
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tok, mask = wl.batch(name, B=B, C=C)
+    N = 8
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    td, md = dev_tokens(tok, mask)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, sd["step"], w["eps"], N, td, md)
+    gp, gm = Lp.cpu().numpy().astype(np.float64), Lm.cpu().numpy().astype(np.float64)
+    rp, rm = oracle.perturbed_losses(cfg, oracle.init(cfg, sd["init"]), sd["step"], w["eps"], N,
+                                     tok, mask, as_double=True)
+    dg, dr = gp - gm, rp - rm
+    say(f"{name}: dL gpu {dg} oracle {dr}")
+    assert np.all(np.abs(dr) > 0)
+    tol = 8 * 2.0 ** -24 * np.abs(rp) + 1e-4 * np.abs(dr)
+    assert np.all(np.abs(dg - dr) <= tol)
