@@ -10,15 +10,17 @@
 //     a    = accW + s eps accZ   (fp32, in the epilogue)
 // so the probe term is formed at fp32 precision relative to itself.
 //
-// Tiles: a workgroup of 8 waves computes 256 rows x 128 columns with K tiles
-// of 64; wave (wm, wn) owns rows 64 wm .. +63 and columns 64 wn .. +63 as
-// 2 x 2 tiles of v_mfma_f32_32x32x16_bf16 per stream (128 accumulator
-// registers), so two waves fit on each SIMD and one wave's LDS reads, probe
-// expansion and address work run under the other's matrix instructions.
+// Tiles: a workgroup of 8 waves computes TM = 256 rows x 128 columns with K
+// tiles of 64; wave (wm, wn) owns rows 64 wm .. +63 and columns 64 wn .. +63
+// as 2 x 2 tiles of v_mfma_f32_32x32x16_bf16 per stream (128 accumulator
+// registers, under 256 VGPRs), so two waves share each SIMD and one wave's
+// LDS reads, probe expansion and address work run under the other's matrix
+// instructions. (Measured alternative: 128-row workgroups, two per CU, are
+// 9% slower at the 1.2B shape and 2.5x slower with normal probes.)
 // Lane l feeds row/column l % 32 and k block l / 32 of each 32x32x16 step.
 //
 // LDS (dynamic, double-buffered, one barrier per K tile): the activation tile
-// [256][72] and the weight tile [128][72] (bf16, rows padded to 144 B so that
+// [TM][72] and the weight tile [128][72] (bf16, rows padded to 144 B so that
 // 16 lanes' 128-bit reads hit distinct banks), and the probe tile: Rademacher
 // sign bits [128][2] words, expanded to bf16 +-1 by each wave, or normal
 // values in bf16 [128][72]. The next K tile's global loads and probe
@@ -36,11 +38,17 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int NT = 512;      // threads per workgroup (8 waves)
-constexpr int TM = 256;      // rows per workgroup
 constexpr int TN = 128;      // columns per workgroup
 constexpr int TK = 64;       // K per tile
 constexpr int LDB = TK + 8;  // LDS row stride in bf16 elements (144 B)
+constexpr int TM = 256;              // rows per workgroup
+constexpr int WAVES_M = TM / 64;     // waves along the rows
+constexpr int NWAVES = 2 * WAVES_M;  // x 2 along the columns
+constexpr int NT = 64 * NWAVES;      // threads per workgroup
+constexpr int WCHUNKS = TN * 8 / NT; // 16-byte weight chunks per thread and K tile
+constexpr int ZROW_T = NT / TN;      // threads per probe-tile row (normal probes)
+constexpr int ZVALS = TK / ZROW_T;   // probe values per thread and K tile (normal probes)
+static_assert(NT >= 256 && TM * 8 / NT == 4, "loader layout");
 
 static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole number of row tiles");
 static_assert(TN == kVocabTile, "head vocabulary tile");
@@ -107,26 +115,26 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
   auto sz = [&](int b) { return sm + b * kStage + kATile + kWTile; };
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
-  const int wm = wave & 3, wn = wave >> 2;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
 
   // loader roles
-  //   A: chunks idx = t + 512 q (q < 4): row idx >> 3, 8 bf16 at 8 (idx & 7)
-  //   W: chunks idx = t + 512 q (q < 2): row idx >> 3, 8 bf16 at 8 (idx & 7)
+  //   A: chunks idx = t + NT q (q < 4): row idx >> 3, 8 bf16 at 8 (idx & 7)
+  //   W: chunks idx = t + NT q (q < WCHUNKS): row idx >> 3, 8 bf16 at 8 (idx & 7)
   //   probe: Rademacher, threads t < 256: row t >> 1, one 32-k word at 32 (t & 1);
-  //          normal, all threads: row t >> 2, 16 k at 16 (t & 3)
-  int wrow[2];
-  bool wok[2];
+  //          normal, all threads: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
+  int wrow[WCHUNKS];
+  bool wok[WCHUNKS];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) wok[q] = colmap((t + 512 * q) >> 3, wrow[q]);
-  const int zr = kind == ZO_RADEMACHER ? (t >> 1) & 127 : t >> 2;
-  const int zpart = kind == ZO_RADEMACHER ? (t & 1) : (t & 3);
+  for (int q = 0; q < WCHUNKS; ++q) wok[q] = colmap((t + NT * q) >> 3, wrow[q]);
+  const int zr = kind == ZO_RADEMACHER ? (t >> 1) & 127 : t / ZROW_T;
+  const int zpart = kind == ZO_RADEMACHER ? (t & 1) : (t % ZROW_T);
   int zn;
   const bool zok = colmap(zr, zn);
   const bool zthread = kind != ZO_RADEMACHER || t < 256;
 
-  u4 ra[4], rw[2], rz[2];
+  u4 ra[4], rw[WCHUNKS], rz[ZVALS / 8];
   uint32_t rbits = 0u;
   Words zcache{{0u, 0u, 0u, 0u}};
   int seg = 0, k0 = 0;
@@ -135,12 +143,12 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
     const SegB sg = seg == 0 ? s0 : s1;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = t + 512 * q;
+      const int idx = t + NT * q;
       ra[q] = *(const u4*)(sg.A + (int64_t)(idx >> 3) * sg.lda + k0 + 8 * (idx & 7));
     }
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = t + 512 * q;
+    for (int q = 0; q < WCHUNKS; ++q) {
+      const int idx = t + NT * q;
       rw[q] = wok[q] ? *(const u4*)(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + 8 * (idx & 7))
                      : u4{0u, 0u, 0u, 0u};
     }
@@ -161,9 +169,9 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
         rbits = zok ? unshuffle_bits(~word) : 0xFFFFFFFFu;
       }
     } else {
-      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 16 * zpart;
+      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + ZVALS * zpart;
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
+      for (int q = 0; q < ZVALS / 8; ++q) {
         float za[4], zb[4];
         gauss_block(key, probe, (j0 >> 2) + 2 * q, za);
         gauss_block(key, probe, (j0 >> 2) + 2 * q + 1, zb);
@@ -182,19 +190,19 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
   auto store = [&](int b) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = t + 512 * q;
+      const int idx = t + NT * q;
       *(u4*)(sa(b) + (idx >> 3) * LDB + 8 * (idx & 7)) = ra[q];
     }
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int idx = t + 512 * q;
+    for (int q = 0; q < WCHUNKS; ++q) {
+      const int idx = t + NT * q;
       *(u4*)(sw(b) + (idx >> 3) * LDB + 8 * (idx & 7)) = rw[q];
     }
     if constexpr (kind == ZO_RADEMACHER) {
       if (zthread) ((uint32_t*)sz(b))[zr * 2 + zpart] = rbits;
     } else {
 #pragma unroll
-      for (int q = 0; q < 2; ++q) *(u4*)(sz(b) + zr * LDB + 16 * zpart + 8 * q) = rz[q];
+      for (int q = 0; q < ZVALS / 8; ++q) *(u4*)(sz(b) + zr * LDB + ZVALS * zpart + 8 * q) = rz[q];
     }
   };
 
@@ -281,7 +289,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
 __device__ __forceinline__ float tanh_(float x) { return 1.0f - 2.0f / (__expf(2.0f * x) + 1.0f); }
 
-// Row (within the workgroup's 256) of accumulator element v of row tile mt
+// Row (within the workgroup's TM) of accumulator element v of row tile mt
 // for this lane: 32x32 MFMA output layout.
 __device__ __forceinline__ int acc_row(int wm, int mt, int lg, int v) {
   return 64 * wm + 32 * mt + 8 * (v >> 2) + 4 * lg + (v & 3);
@@ -311,15 +319,15 @@ struct GateArgsB {
   RowMap rm;
 };
 
-// Workgroup: 256 rows x 32 hidden units; LDS column rho = gate * 32 + unit.
+// Workgroup: TM rows x 32 hidden units; LDS column rho = gate * 32 + unit.
 // Waves wn = 0 hold gates i, f and waves wn = 1 gates g, o of the same units;
 // after the main loop the wn = 1 waves pass their pre-activations through
 // LDS and the wn = 0 waves update the cell.
 template <int kind>
-__global__ __launch_bounds__(NT) void gate_bf16_kernel(GateArgsB g) {
+__global__ __launch_bounds__(NT, 512 / NT) void gate_bf16_kernel(GateArgsB g) {
   extern __shared__ __align__(16) uint16_t smem[];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave & 3, wn = wave >> 2;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   const int u0 = blockIdx.x * 32;
   const int64_t m0 = (int64_t)blockIdx.y * TM;
@@ -346,7 +354,7 @@ __global__ __launch_bounds__(NT) void gate_bf16_kernel(GateArgsB g) {
     zz[nt] = g.zb[(int64_t)pair * 4 * H + gate * H + u];
   }
   __syncthreads();  // the main loop's LDS buffers are free from here on
-  float* xg = (float*)smem;  // [256 rows][32 units][2]: pre-activations of gates g, o
+  float* xg = (float*)smem;  // [TM rows][32 units][2]: pre-activations of gates g, o
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -402,10 +410,10 @@ struct HeadArgsB {
 };
 
 template <int kind>
-__global__ __launch_bounds__(NT) void head_bf16_kernel(HeadArgsB g) {
+__global__ __launch_bounds__(NT, 512 / NT) void head_bf16_kernel(HeadArgsB g) {
   extern __shared__ __align__(16) uint16_t smem[];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave & 3, wn = wave >> 2;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   const int vt = blockIdx.x;
   const int v0 = vt * TN;
@@ -437,8 +445,8 @@ __global__ __launch_bounds__(NT) void head_bf16_kernel(HeadArgsB g) {
     zz[nt] = cok[nt] ? g.zbo[(int64_t)pair * V + col[nt]] : 0.f;
   }
   __syncthreads();  // reuse the main loop's LDS for the cross-wave reduction
-  float* red_m = (float*)smem;   // [2][256]
-  float* red_s = red_m + 2 * TM;  // [2][256]
+  float* red_m = (float*)smem;   // [2][TM]
+  float* red_s = red_m + 2 * TM;  // [2][TM]
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
