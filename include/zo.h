@@ -128,9 +128,10 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
 
 /* The update of Eq. 7 in its general form (Algorithm 1's closing loop):
  *   c_n = fp32( (lr / N) * (L+_n - L-_n) / (2 eps) )  (computed in double)
- *   theta_j <- theta_j - sum_{n=0}^{N-1} c_n z_{i0+n}[j]  (fp32, ascending n;
- *   bf16 storage rounds the fp32 result to nearest even)
- * theta is read and written once, in place. Lplus and Lminus are device fp32
+ *   theta_j <- theta_j - sum_{n=0}^{N-1} c_n z_{i0+n}[j]  (summed in fp32:
+ *   Rademacher probes by groups of 8 in probe order, normal probes in
+ *   ascending n; bf16 storage rounds the fp32 result to nearest even)
+ * theta is read and written once, in place, and must be 16-byte aligned. Lplus and Lminus are device fp32
  * [N]. If any of them is not finite the update is skipped on the device,
  * theta is left bit-unchanged and, when skipped_out (device int32, may be
  * NULL) is given, *skipped_out is set to 1 (0 otherwise).

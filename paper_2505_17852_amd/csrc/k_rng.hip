@@ -83,56 +83,163 @@ __device__ __forceinline__ void store4(T* theta, uint64_t j, uint64_t P, const f
   }
 }
 
-// Rademacher update. A workgroup owns 1024 consecutive parameters (8 Philox
-// blocks per probe); for each group of 32 probes every thread computes one
-// Philox block into LDS, then each thread applies the 32 signed step sizes to
-// its 4 parameters in ascending probe order.
-constexpr int kUpdChunk = 1024;
+// Rademacher update. sum_n c_n z_n[j] with z = +-1 is, for each group of 8
+// probes, a table lookup: T_g[m] = sum over the group of (bit n of m ? +c_n :
+// -c_n) for the 256 sign patterns m (built once per workgroup and group).
+// A workgroup owns 8192 consecutive parameters (256 Philox words per probe);
+// each thread loads its 4 sets of 8 parameters up front (four 16-byte loads
+// in flight per thread), then for each group of up to 16 probes the
+// workgroup computes their Philox blocks into LDS (4 per thread), and each
+// thread takes, for each set of 8 parameters, one byte of sign bits from
+// each of 8 probes, transposes that 8x8 bit block (three swap stages) so that
+// byte e holds parameter e's signs, and adds one table entry per parameter
+// and group of 8. theta is read and written once.
+constexpr int kUpdChunk = 8192;   // parameters per workgroup (32 per thread, 4 sets of 8)
+constexpr int kUpdWords = kUpdChunk / 32;
+constexpr int kUpdGroup = 16;     // probes per pass over the LDS tables
+
+// 8x8 bit transpose of the bytes of (lo, hi) (byte j = row j): byte e of the
+// result holds bit e of every input byte.
+__device__ __forceinline__ void transpose8x8(uint32_t& lo, uint32_t& hi) {
+  uint32_t t;
+  t = (lo ^ (lo >> 7)) & 0x00AA00AAu;
+  lo = lo ^ t ^ (t << 7);
+  t = (hi ^ (hi >> 7)) & 0x00AA00AAu;
+  hi = hi ^ t ^ (t << 7);
+  t = (lo ^ (lo >> 14)) & 0x0000CCCCu;
+  lo = lo ^ t ^ (t << 14);
+  t = (hi ^ (hi >> 14)) & 0x0000CCCCu;
+  hi = hi ^ t ^ (t << 14);
+  t = (lo ^ (hi << 4)) & 0xF0F0F0F0u;
+  lo = lo ^ t;
+  hi = hi ^ (t >> 4);
+}
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* theta, uint64_t j, uint64_t P, float v[8]) {
+  if (j + 8 <= P) {
+    if constexpr (sizeof(T) == 2) {
+      const uint4 q = *(const uint4*)(theta + j);
+      const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] = bf16_to_f32((uint16_t)w[e]);
+        v[2 * e + 1] = bf16_to_f32((uint16_t)(w[e] >> 16));
+      }
+    } else {
+      const float4 a = *(const float4*)(theta + j), b = *(const float4*)(theta + j + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+      v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    }
+  } else {
+    load4(theta, j, P, v);
+    load4(theta, j + 4, P, v + 4);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T* theta, uint64_t j, uint64_t P, const float v[8]) {
+  if (j + 8 <= P) {
+    if constexpr (sizeof(T) == 2) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)bf16_rne(v[2 * e]) | ((uint32_t)bf16_rne(v[2 * e + 1]) << 16);
+      *(uint4*)(theta + j) = uint4{w[0], w[1], w[2], w[3]};
+    } else {
+      *(float4*)(theta + j) = float4{v[0], v[1], v[2], v[3]};
+      *(float4*)(theta + j + 4) = float4{v[4], v[5], v[6], v[7]};
+    }
+  } else {
+    store4(theta, j, P, v);
+    store4(theta, j + 4, P, v + 4);
+  }
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void update_rademacher_kernel(T* theta, uint64_t P, Key key,
                                                                 float eps, float lr, int N,
                                                                 uint32_t i0, const float* Lp,
                                                                 const float* Lm, int32_t* skipped) {
-  __shared__ uint32_t words[32][8][4];
-  __shared__ float coef[32];
+  // sign words laid out [word][probe] (rows padded by 4 words) so that one
+  // thread reads 8 probes' words of its parameters with two 128-bit loads
+  constexpr int kRow = kUpdGroup + 4;
+  constexpr int kSets = kUpdChunk / (8 * 256);
+  __shared__ uint32_t words[kUpdWords * kRow];     // 20 KiB
+  __shared__ float table[kUpdGroup / 8][256];      // signed-sum tables
+  __shared__ float half_table[kUpdGroup / 8][32];  // 4-probe partial sums
+  __shared__ float coef[kUpdGroup];
   __shared__ int flag;
   const bool ok = losses_finite(Lp, Lm, N, &flag);
   if (blockIdx.x == 0 && threadIdx.x == 0 && skipped) *skipped = ok ? 0 : 1;
   if (!ok) return;
   const int t = threadIdx.x;
   const uint64_t base = (uint64_t)blockIdx.x * kUpdChunk;
-  const uint64_t j = base + 4u * (uint64_t)t;
-  float th[4];
-  load4(theta, j, P, th);
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  const int wsel_blk = t >> 5;        // which of the 8 blocks holds this thread's elements
-  const int wsel_word = (t >> 3) & 3;  // which word of that block
-  const int shift = (t & 7) * 4;       // bit position of the first of the 4 elements
-  for (int n0 = 0; n0 < N; n0 += 32) {
-    __syncthreads();
-    {
-      const int pn = t >> 3, pb = t & 7;
-      if (n0 + pn < N) {
-        const Words x = stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
+  float th[kSets][8];
 #pragma unroll
-        for (int w = 0; w < 4; ++w) words[pn][pb][w] = x.w[w];
-      }
-      if (t < 32 && n0 + t < N) coef[t] = update_coeff(lr, N, Lp[n0 + t], Lm[n0 + t], eps);
+  for (int q = 0; q < kSets; ++q) load8(theta, base + 2048u * q + 8u * t, P, th[q]);
+  float acc[kSets][8];
+#pragma unroll
+  for (int q = 0; q < kSets; ++q)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
+  const uint32_t k = (uint32_t)(t & 3);  // this thread's byte within each of its words
+  // byte-gather selectors for v_perm: byte k of the low and high source -> bytes 0, 1
+  const uint32_t sel = k | ((4u + k) << 8) | 0x0C0C0000u;
+  for (int n0 = 0; n0 < N; n0 += kUpdGroup) {
+    const int cnt = N - n0 < kUpdGroup ? N - n0 : kUpdGroup;
+    const int ngroups = (cnt + 7) / 8;
+    __syncthreads();
+    if (t < kUpdGroup) coef[t] = t < cnt ? update_coeff(lr, N, Lp[n0 + t], Lm[n0 + t], eps) : 0.f;
+    // Philox blocks: cnt probes x 64 blocks (probes past cnt only ever meet zero coefficients)
+    for (int q = t; q < cnt * (kUpdWords / 4); q += 256) {
+      const int pn = q / (kUpdWords / 4), pb = q % (kUpdWords / 4);
+      const Words x = stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) words[(4 * pb + w) * kRow + pn] = x.w[w];
     }
     __syncthreads();
-    const int cnt = N - n0 < 32 ? N - n0 : 32;
-    for (int pn = 0; pn < cnt; ++pn) {
-      const uint32_t w = words[pn][wsel_blk][wsel_word] >> shift;
-      const float c = coef[pn];
+    // 4-probe partial tables, then T[m] = low[m & 15] + high[m >> 4]
+    if (t < ngroups * 32) {
+      const int g = t >> 5, h = (t >> 4) & 1, m = t & 15;
+      float v = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] += ((w >> e) & 1u) ? c : -c;
+      for (int b = 0; b < 4; ++b) {
+        const float c = coef[8 * g + 4 * h + b];
+        v += ((m >> b) & 1) ? c : -c;
+      }
+      half_table[g][16 * h + m] = v;
+    }
+    __syncthreads();
+    for (int q = t; q < ngroups * 256; q += 256) {
+      const int g = q >> 8, m = q & 255;
+      table[g][m] = half_table[g][m & 15] + half_table[g][16 + (m >> 4)];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kSets; ++q) {
+      const uint32_t* wrow = words + (64 * q + (t >> 2)) * kRow;
+      for (int g = 0; g < ngroups; ++g) {
+        const uint4 a = *(const uint4*)(wrow + 8 * g);
+        const uint4 b = *(const uint4*)(wrow + 8 * g + 4);
+        // byte k of each of the 8 probes' words, probe order, into (lo, hi)
+        uint32_t lo = __builtin_amdgcn_perm(a.y, a.x, sel) | (__builtin_amdgcn_perm(a.w, a.z, sel) << 16);
+        uint32_t hi = __builtin_amdgcn_perm(b.y, b.x, sel) | (__builtin_amdgcn_perm(b.w, b.z, sel) << 16);
+        transpose8x8(lo, hi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[q][e] += table[g][(lo >> (8 * e)) & 0xFFu];
+          acc[q][4 + e] += table[g][(hi >> (8 * e)) & 0xFFu];
+        }
+      }
     }
   }
-  float out[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) out[e] = th[e] - acc[e];
-  store4(theta, j, P, out);
+  for (int q = 0; q < kSets; ++q) {
+    float out[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = th[q][e] - acc[q][e];
+    store8(theta, base + 2048u * q + 8u * t, P, out);
+  }
 }
 
 // Normal-probe update: each thread owns one Philox block (4 parameters) and

@@ -122,6 +122,7 @@ int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float
   int st = check_config(cfg);
   if (st) return st;
   if (!theta || !Lplus || !Lminus) return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (!aligned16(theta)) return fail(ZO_EINVAL, "theta must be 16-byte aligned");
   if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
   if (!std::isfinite(lr)) return fail(ZO_EINVAL, "lr must be finite");
   if (N < 1) return fail(ZO_EINVAL, "N must be >= 1");
