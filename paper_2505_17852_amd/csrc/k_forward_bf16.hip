@@ -3,29 +3,32 @@
 //
 // A bf16 weight cannot carry a perturbation of eps = 1e-3 (its spacing near
 // |w| = 1/64 is 6e-5, and a rounded w + eps z would lose several percent of
-// eps z). So every product keeps the two terms apart, as two MFMA streams
-// that share the activation fragment:
-//     accW = A . W        (bf16 x bf16, fp32 accumulate)
-//     accZ = A . z        (z = +-1 exactly, or the bf16 of a normal value)
-//     a    = accW + s eps accZ   (fp32, in the epilogue)
-// so the probe term is formed at fp32 precision relative to itself.
+// eps z). So every product is two MFMAs into one fp32 accumulator that share
+// the activation fragment:
+//     acc += A . W                (bf16 x bf16)
+//     acc += A . (s eps z)        (s eps z in bf16: +-bf16(eps) for signs,
+//                                  bf16(s eps z) for normal values)
+// The probe term is formed exactly apart from the bf16 rounding of eps z
+// (relative 2^-9), and accumulates in fp32 next to A . W.
 //
-// Tiles: a workgroup of 8 waves computes TM = 256 rows x 128 columns with K
-// tiles of 64; wave (wm, wn) owns rows 64 wm .. +63 and columns 64 wn .. +63
-// as 2 x 2 tiles of v_mfma_f32_32x32x16_bf16 per stream (128 accumulator
-// registers, under 256 VGPRs), so two waves share each SIMD and one wave's
-// LDS reads, probe expansion and address work run under the other's matrix
-// instructions. (Measured alternative: 128-row workgroups, two per CU, are
-// 9% slower at the 1.2B shape and 2.5x slower with normal probes.)
-// Lane l feeds row/column l % 32 and k block l / 32 of each 32x32x16 step.
+// Tiles: a workgroup of 8 waves computes TM = 256 rows x TN columns with K
+// tiles of 64: TN = 256 with sign probes (waves 2 x 4, wave tiles 128 x 64),
+// TN = 128 with normal probes (waves 4 x 2, wave tiles 64 x 64; the probe
+// tile then needs LDS of its own). A wave tile is MT x 2 tiles of
+// v_mfma_f32_32x32x16_bf16 (MT = 4 or 2); two waves share each SIMD, so one
+// wave's LDS reads, probe expansion and address work run under the other's
+// matrix instructions. Lane l feeds row/column l % 32 and k block l / 32.
 //
-// LDS (dynamic, double-buffered, one barrier per K tile): the activation tile
-// [TM][72] and the weight tile [128][72] (bf16, rows padded to 144 B so that
-// 16 lanes' 128-bit reads hit distinct banks), and the probe tile: Rademacher
-// sign bits [128][2] words, expanded to bf16 +-1 by each wave, or normal
-// values in bf16 [128][72]. The next K tile's global loads and probe
-// generation are issued before the current tile's MFMAs.
+// LDS (static, two stages, one barrier per K tile): per stage the
+// activation tile [TM][64] and the weight tile [TN][64] (bf16, 128-byte rows,
+// 16-byte chunks XOR-swizzled by row), copied from global memory straight
+// into LDS without passing through registers, and the probe tile: sign bits
+// [TN][2] words, expanded to bf16 +-eps by each wave, or bf16(eps z) [TN][64]
+// (swizzled like the weights), generated in registers. The next K tile's
+// copies and probe tile are issued before the current tile's MFMAs.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "zo_kernels.hpp"
 #include "zo_profile.hpp"
@@ -38,20 +41,57 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int TN = 128;      // columns per workgroup
-constexpr int TK = 64;       // K per tile
-constexpr int LDB = TK + 8;  // LDS row stride in bf16 elements (144 B)
-constexpr int TM = 256;              // rows per workgroup
-constexpr int WAVES_M = TM / 64;     // waves along the rows
-constexpr int NWAVES = 2 * WAVES_M;  // x 2 along the columns
-constexpr int NT = 64 * NWAVES;      // threads per workgroup
-constexpr int WCHUNKS = TN * 8 / NT; // 16-byte weight chunks per thread and K tile
-constexpr int ZROW_T = NT / TN;      // threads per probe-tile row (normal probes)
-constexpr int ZVALS = TK / ZROW_T;   // probe values per thread and K tile (normal probes)
-static_assert(NT >= 256 && TM * 8 / NT == 4, "loader layout");
+constexpr int TK = 64;          // K per tile
+constexpr int TM = 256;         // rows per workgroup
+constexpr int NWAVES = 8;
+constexpr int NT = 64 * NWAVES;  // threads per workgroup
+constexpr int kRowBytes = TK * 2;
+constexpr int kABytes = TM * kRowBytes;
+constexpr int kACopies = kABytes / (NT * 16);  // 16-byte global->LDS copies per thread
 
+// Per probe kind: workgroup columns, wave grid, MFMA tiles per wave, LDS.
+template <int kind>
+struct Tiles {
+  static constexpr int TN = kind == ZO_RADEMACHER ? kVocabTileWide : kVocabTile;
+  static constexpr int WAVES_N = TN / 64;  // wave tiles are 64 columns wide
+  static constexpr int WAVES_M = NWAVES / WAVES_N;
+  static constexpr int WROWS = TM / WAVES_M;  // rows per wave tile
+  static constexpr int MT = WROWS / 32;
+  static constexpr int WBytes = TN * kRowBytes;
+  static constexpr int ZBytes = kind == ZO_RADEMACHER ? TN * 8 : TN * kRowBytes;
+  static constexpr int WCopies = WBytes / (NT * 16);
+  static constexpr int Copies = kACopies + WCopies;
+  static constexpr int ZROW_T = NT / TN;     // threads per probe-tile row (normal probes)
+  static constexpr int ZVALS = TK / ZROW_T;  // probe values per thread and K tile (normal probes)
+  static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
+  static_assert(WCopies * NT * 16 == WBytes && kACopies * NT * 16 == kABytes, "copy split");
+  static_assert(kind != ZO_RADEMACHER || TN * 2 == NT, "one sign word per thread");
+  static_assert(kind == ZO_RADEMACHER || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
+  static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
+};
 static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole number of row tiles");
-static_assert(TN == kVocabTile, "head vocabulary tile");
+
+// Two LDS stages per probe kind (static, so that every offset is a constant).
+__shared__ __align__(16) uint8_t lds_r0[kABytes + Tiles<ZO_RADEMACHER>::WBytes];
+__shared__ __align__(16) uint8_t lds_r1[kABytes + Tiles<ZO_RADEMACHER>::WBytes];
+__shared__ __align__(16) uint32_t lds_b0[Tiles<ZO_RADEMACHER>::ZBytes / 4];
+__shared__ __align__(16) uint32_t lds_b1[Tiles<ZO_RADEMACHER>::ZBytes / 4];
+__shared__ __align__(16) uint8_t lds_g0[kABytes + Tiles<ZO_GAUSSIAN>::WBytes + Tiles<ZO_GAUSSIAN>::ZBytes];
+__shared__ __align__(16) uint8_t lds_g1[kABytes + Tiles<ZO_GAUSSIAN>::WBytes + Tiles<ZO_GAUSSIAN>::ZBytes];
+static_assert(2 * (sizeof(lds_r0) + sizeof(lds_b0)) <= 160 * 1024, "LDS");
+static_assert(2 * sizeof(lds_g0) <= 160 * 1024, "LDS");
+
+template <int kind, int S>
+__device__ __forceinline__ uint8_t* stage() {
+  if constexpr (kind == ZO_RADEMACHER)
+    return S == 0 ? lds_r0 : lds_r1;
+  else
+    return S == 0 ? lds_g0 : lds_g1;
+}
+template <int S>
+__device__ __forceinline__ uint32_t* sign_bits() {
+  return S == 0 ? lds_b0 : lds_b1;
+}
 
 __device__ __forceinline__ bf8 as_bf8(u4 v) { return __builtin_bit_cast(bf8, v); }
 
@@ -63,9 +103,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // consecutive k holds the negative-sign flags (1 = -1) of the even elements
 // 0, 2, .., 30 in bits 0..15 and of the odd elements 1, 3, .., 31 in bits
 // 16..31. The two elements of one packed bf16 pair then sit 16 bits apart,
-// so one shift and one mask-or turn them into the pair (+-1, +-1): the flag
-// of the even element lands on bit 15 and that of the odd one on bit 31 over
-// the constant 0x3F803F80 (= +1, +1).
+// so one shift, one mask and one xor turn them into the pair (+-e, +-e): the
+// flag of the even element lands on bit 15 and that of the odd one on bit
+// 31, and flip the sign bits of the constant pair (e, e).
 __device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
   uint32_t t;
   t = (x ^ (x >> 1)) & 0x22222222u;
@@ -79,6 +119,26 @@ __device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
   return x;
 }
 
+// 16 bytes per lane from global memory straight into LDS: the wave's 64
+// lanes fill the 1 KB at lds (wave-uniform), lane L at lds + 16 L. Written as
+// an asm statement, so the compiler inserts no waits of its own for these
+// copies; the K-tile loop waits for them explicitly (vmcnt) before each barrier.
+__device__ __forceinline__ void copy_to_lds(const void* src, uint8_t* lds) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+
+// Wait until this thread's global->LDS copies and LDS writes are complete
+// (s_waitcnt vmcnt(0) lgkmcnt(0)), then a workgroup barrier without a memory
+// fence. The empty asm statements keep the compiler from moving memory
+// accesses across either.
+__device__ __forceinline__ void wait_and_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x70);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 struct SegB {
   const uint16_t* A;  // first row of this workgroup's activation tile; row r at A + r * lda
   int64_t lda;
@@ -88,96 +148,90 @@ struct SegB {
   int K;
 };
 
-// LDS stage layout (bf16 element offsets): A tile, weight tile, probe tile.
-constexpr int kATile = TM * LDB;
-constexpr int kWTile = TN * LDB;
-constexpr int kZTileGauss = TN * LDB;
-constexpr int kZTileBits = TN * 2 * 2;  // TN rows x 2 words, in bf16 units
-template <int kind>
-constexpr int stage_elems() {
-  return kATile + kWTile + (kind == ZO_RADEMACHER ? kZTileBits : kZTileGauss);
-}
-template <int kind>
-constexpr size_t smem_bytes() {
-  return (size_t)2 * stage_elems<kind>() * 2;
-}
-
-// accW / accZ: [2 row tiles][2 column tiles] of 32x32 fp32 for this wave.
-// colmap(rho, &n) -> true if LDS column rho (0..127) maps to a real weight row n.
+// acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave.
+// colmap(rho, &n) maps LDS column rho (0..TN-1) to a weight row n inside the
+// matrix (columns beyond the matrix map to a valid row; they are never
+// scored). neg: this wave's rows are the -eps pass; eps_b: bf16 bits of eps.
 template <int kind, typename ColMap>
-__device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2][2], const SegB s0,
-                                              const SegB s1, int nseg, ColMap colmap, Key key,
-                                              uint32_t probe, uint16_t* sm) {
-  constexpr int kStage = stage_elems<kind>();
-  // plain offsets from the shared-memory base keep every access a DS instruction
-  auto sa = [&](int b) { return sm + b * kStage; };
-  auto sw = [&](int b) { return sm + b * kStage + kATile; };
-  auto sz = [&](int b) { return sm + b * kStage + kATile + kWTile; };
+__device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
+                                              int nseg, ColMap colmap, Key key, uint32_t probe, bool neg,
+                                              float eps, uint16_t eps_b) {
+  using T = Tiles<kind>;
+  constexpr int MT = T::MT;
   const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
-  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
 
-  // loader roles
-  //   A: chunks idx = t + NT q (q < 4): row idx >> 3, 8 bf16 at 8 (idx & 7)
-  //   W: chunks idx = t + NT q (q < WCHUNKS): row idx >> 3, 8 bf16 at 8 (idx & 7)
-  //   probe: Rademacher, threads t < 256: row t >> 1, one 32-k word at 32 (t & 1);
-  //          normal, all threads: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
-  int wrow[WCHUNKS];
-  bool wok[WCHUNKS];
+  // copy roles: copy q of wave w fills rows 8 (q NWAVES + w) .. +7 of the
+  // activation (q < kACopies) or weight tile, 1 KB lane-linear in LDS: lane
+  // L writes row + L / 8, slot L % 8, which holds chunk (L % 8) ^ ((row >> 1) & 7)
+  const int crow = lane >> 3;
+  int arow[kACopies], wrow[T::WCopies];
+  uint32_t aoff[kACopies], woff[T::WCopies];  // element offsets of the chunk inside the row
 #pragma unroll
-  for (int q = 0; q < WCHUNKS; ++q) wok[q] = colmap((t + NT * q) >> 3, wrow[q]);
-  const int zr = kind == ZO_RADEMACHER ? (t >> 1) & 127 : t / ZROW_T;
-  const int zpart = kind == ZO_RADEMACHER ? (t & 1) : (t % ZROW_T);
+  for (int q = 0; q < kACopies; ++q) {
+    const int r = 8 * (q * NWAVES + wave) + crow;
+    arow[q] = r;
+    aoff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+  }
+#pragma unroll
+  for (int q = 0; q < T::WCopies; ++q) {
+    const int r = 8 * (q * NWAVES + wave) + crow;
+    colmap(r, wrow[q]);
+    woff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+  }
+  // probe roles: signs, every thread: row t >> 1, one 32-k word at 32 (t & 1);
+  //              normal, every thread: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
+  const int zr = kind == ZO_RADEMACHER ? t >> 1 : t / T::ZROW_T;
+  const int zpart = kind == ZO_RADEMACHER ? (t & 1) : (t % T::ZROW_T);
   int zn;
-  const bool zok = colmap(zr, zn);
-  const bool zthread = kind != ZO_RADEMACHER || t < 256;
+  colmap(zr, zn);
 
-  u4 ra[4], rw[WCHUNKS], rz[ZVALS / 8];
-  uint32_t rbits = 0u;
   Words zcache{{0u, 0u, 0u, 0u}};
   int seg = 0, k0 = 0;
 
-  auto fetch = [&]() {
+  // Issue the next K tile into stage S: the global->LDS copies of the
+  // activation and weight rows, then the probe tile computed in registers
+  // and written to LDS.
+  auto issue = [&](auto stage_tag) {
+    constexpr int S = decltype(stage_tag)::value;
+    uint8_t* base = stage<kind, S>();
     const SegB sg = seg == 0 ? s0 : s1;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int idx = t + NT * q;
-      ra[q] = *(const u4*)(sg.A + (int64_t)(idx >> 3) * sg.lda + k0 + 8 * (idx & 7));
-    }
+    for (int q = 0; q < kACopies; ++q)
+      copy_to_lds(sg.A + (int64_t)arow[q] * sg.lda + k0 + aoff[q], base + (q * NWAVES + wave) * 1024);
 #pragma unroll
-    for (int q = 0; q < WCHUNKS; ++q) {
-      const int idx = t + NT * q;
-      rw[q] = wok[q] ? *(const u4*)(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + 8 * (idx & 7))
-                     : u4{0u, 0u, 0u, 0u};
-    }
+    for (int q = 0; q < T::WCopies; ++q)
+      copy_to_lds(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
+                  base + kABytes + (q * NWAVES + wave) * 1024);
     if constexpr (kind == ZO_RADEMACHER) {
-      if (zthread) {
-        const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 32 * zpart;
-        uint32_t word;
-        const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
-        if (aligned) {
-          if ((k0 & 127) == 0) zcache = stream_block(key, j0 >> 7, probe, kTagRademacher);
-          const int q = (int)((j0 >> 5) & 3u);
-          word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
-        } else {
-          word = rademacher_word(key, probe, j0 >> 5);
-        }
-        // negative-sign flags in unshuffled order; padding columns: all -1
-        // against zero weights, never scored
-        rbits = zok ? unshuffle_bits(~word) : 0xFFFFFFFFu;
+      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 32 * zpart;
+      uint32_t word;
+      const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
+      if (aligned) {
+        if ((k0 & 127) == 0) zcache = stream_block(key, j0 >> 7, probe, kTagRademacher);
+        const int q = (int)((j0 >> 5) & 3u);
+        word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
+      } else {
+        word = rademacher_word(key, probe, j0 >> 5);
       }
+      // negative-sign flags in unshuffled order
+      sign_bits<S>()[zr * 2 + zpart] = unshuffle_bits(~word);
     } else {
-      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + ZVALS * zpart;
+      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
+      uint8_t* zrow = base + kABytes + T::WBytes + zr * kRowBytes;
 #pragma unroll
-      for (int q = 0; q < ZVALS / 8; ++q) {
+      for (int q = 0; q < T::ZVALS / 8; ++q) {
         float za[4], zb[4];
         gauss_block(key, probe, (j0 >> 2) + 2 * q, za);
         gauss_block(key, probe, (j0 >> 2) + 2 * q + 1, zb);
-        rz[q] = zok ? u4{pack_bf16x2(za[0], za[1]), pack_bf16x2(za[2], za[3]),
-                         pack_bf16x2(zb[0], zb[1]), pack_bf16x2(zb[2], zb[3])}
-                    : u4{0u, 0u, 0u, 0u};
+        const int chunk = (T::ZVALS / 8) * zpart + q;
+        *(u4*)(zrow + 16 * (chunk ^ ((zr >> 1) & 7))) =
+            u4{pack_bf16x2(eps * za[0], eps * za[1]), pack_bf16x2(eps * za[2], eps * za[3]),
+               pack_bf16x2(eps * zb[0], eps * zb[1]), pack_bf16x2(eps * zb[2], eps * zb[3])};
       }
     }
     k0 += TK;
@@ -187,35 +241,26 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
     }
   };
 
-  auto store = [&](int b) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int idx = t + NT * q;
-      *(u4*)(sa(b) + (idx >> 3) * LDB + 8 * (idx & 7)) = ra[q];
-    }
-#pragma unroll
-    for (int q = 0; q < WCHUNKS; ++q) {
-      const int idx = t + NT * q;
-      *(u4*)(sw(b) + (idx >> 3) * LDB + 8 * (idx & 7)) = rw[q];
-    }
-    if constexpr (kind == ZO_RADEMACHER) {
-      if (zthread) ((uint32_t*)sz(b))[zr * 2 + zpart] = rbits;
-    } else {
-#pragma unroll
-      for (int q = 0; q < ZVALS / 8; ++q) *(u4*)(sz(b) + zr * LDB + ZVALS * zpart + 8 * q) = rz[q];
-    }
-  };
-
-  // Fragments of one 16-k step: activations (2 row tiles), weights and probe
-  // values (2 column tiles). The next step's LDS reads and sign expansion are
-  // issued between the current step's MFMAs (software pipelining within the
-  // K tile), so the matrix pipe is fed while the VALU and LDS work proceeds.
+  // Fragments of one 16-k step: activations (MT row tiles), weights and
+  // probe values (2 column tiles). The next step's LDS reads and sign
+  // expansion are issued between the current step's MFMAs (software
+  // pipelining within the K tile). Lane (lr, lg) reads chunk 2 s + lg of its
+  // rows, in slot (2 s) ^ y with y = lg ^ ((lr >> 1) & 7) (every row offset
+  // below is a multiple of 16).
+  const uint32_t y = (uint32_t)(lg ^ ((lr >> 1) & 7));
+  const uint32_t a_lane = (uint32_t)(T::WROWS * wm + lr) * kRowBytes;
+  const uint32_t w_lane = (uint32_t)(64 * wn + lr) * kRowBytes;
+  // the pair (s eps, s eps) in bf16 (signs), or the sign flip of -eps rows (normal)
+  const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
+  const uint32_t zc = kind == ZO_RADEMACHER ? (neg ? ebits ^ 0x80008000u : ebits) : (neg ? 0x80008000u : 0u);
   struct Frag {
-    bf8 a[2], w[2], z[2];
+    bf8 a[MT], w[2], z[2];
   };
-  auto compute = [&](int b) {
-    const uint16_t* pa = sa(b) + (64 * wm + lr) * LDB + 8 * lg;
-    const uint16_t* pw = sw(b) + (64 * wn + lr) * LDB + 8 * lg;
+  auto compute = [&](auto stage_tag) {
+    constexpr int S = decltype(stage_tag)::value;
+    const uint8_t* base = stage<kind, S>();
+    const uint8_t* pa = base + a_lane;
+    const uint8_t* pw = base + kABytes + w_lane;
     // per lane, the flags of its k block pre-shifted so that a constant shift
     // per (k step, pair) brings them to bits 15 / 31 (see unshuffle_bits)
     uint32_t bits[2][2];
@@ -223,26 +268,29 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
       const uint32_t pre = 4u * (uint32_t)(1 - lg);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const uint2 v = *(const uint2*)((const uint32_t*)sz(b) + (64 * wn + 32 * nt + lr) * 2);
+        const uint2 v = *(const uint2*)(sign_bits<S>() + (64 * wn + 32 * nt + lr) * 2);
         bits[nt][0] = v.x << pre;
         bits[nt][1] = v.y << pre;
       }
     }
     auto load = [&](int s, Frag& f) {
+      const uint32_t so = 16u * ((uint32_t)(2 * s) ^ y);
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * LDB + 16 * s));
+      for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * kRowBytes + so));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * LDB + 16 * s));
+        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * kRowBytes + so));
+        u4 v;
         if constexpr (kind == ZO_RADEMACHER) {
           const uint32_t x = bits[nt][s >> 1];
-          u4 v;
 #pragma unroll
-          for (int d = 0; d < 4; ++d) v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) | 0x3F803F80u;
-          f.z[nt] = as_bf8(v);
+          for (int d = 0; d < 4; ++d) v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) ^ zc;
         } else {
-          f.z[nt] = as_bf8(*(const u4*)(sz(b) + (64 * wn + 32 * nt + lr) * LDB + 16 * s + 8 * lg));
+          v = *(const u4*)(pw + T::WBytes + 32 * nt * kRowBytes + so);
+#pragma unroll
+          for (int d = 0; d < 4; ++d) v[d] ^= zc;
         }
+        f.z[nt] = as_bf8(v);
       }
     };
     Frag f[2];
@@ -251,39 +299,46 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&accW)[2][2], f16v (&accZ)[2
     for (int s = 0; s < TK / 16; ++s) {
       const Frag& c = f[s & 1];
       if (s + 1 < TK / 16) load(s + 1, f[(s + 1) & 1]);
+      // weight products of every accumulator first, then the probe products,
+      // so that two MFMAs into one accumulator are 2 MT apart
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          accW[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], accW[mt][nt], 0, 0, 0);
-          accZ[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], accZ[mt][nt], 0, 0, 0);
-        }
-      }
+        for (int nt = 0; nt < 2; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], acc[mt][nt], 0, 0, 0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
       if (s + 1 < TK / 16) {
         // per step: the next step's LDS reads first, then each MFMA followed by
-        // a few VALU instructions of the next step's sign expansion
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        // a few VALU instructions of the next step's probe fragments
+        __builtin_amdgcn_sched_group_barrier(0x100, MT + 2 + (kind == ZO_RADEMACHER ? 0 : 2), 0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < 4 * MT; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
       }
     }
   };
 
-  fetch();
-  store(0);
-  __syncthreads();
-  if (ntiles > 1) fetch();
-  for (int it = 0; it < ntiles; ++it) {
-    compute(it & 1);
-    if (it + 1 < ntiles) {
-      store((it + 1) & 1);
-      __syncthreads();
-      if (it + 2 < ntiles) fetch();
-    }
+  // K tile it lives in stage it % 2. Per tile: wait for this thread's copies
+  // and LDS writes of tile it; barrier (tile it complete for every wave, and
+  // the other stage, computed at it - 1, free); issue tile it + 1; compute it.
+  auto step = [&](auto stage_tag, int it) {
+    constexpr int S = decltype(stage_tag)::value;
+    wait_and_barrier();
+    if (it + 1 < ntiles) issue(std::integral_constant<int, 1 - S>{});
+    compute(stage_tag);
+  };
+  issue(std::integral_constant<int, 0>{});
+  for (int it = 0; it < ntiles; it += 2) {
+    step(std::integral_constant<int, 0>{}, it);
+    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
+  __syncthreads();  // every wave done with the stages before they are reused
 }
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
@@ -291,16 +346,17 @@ __device__ __forceinline__ float tanh_(float x) { return 1.0f - 2.0f / (__expf(2
 
 // Row (within the workgroup's TM) of accumulator element v of row tile mt
 // for this lane: 32x32 MFMA output layout.
+template <int kind>
 __device__ __forceinline__ int acc_row(int wm, int mt, int lg, int v) {
-  return 64 * wm + 32 * mt + 8 * (v >> 2) + 4 * lg + (v & 3);
+  return Tiles<kind>::WROWS * wm + 32 * mt + 8 * (v >> 2) + 4 * lg + (v & 3);
 }
 
-template <typename T>
-__device__ __forceinline__ void zero_acc(T (&acc)[2][2]) {
+template <int MT>
+__device__ __forceinline__ void zero_acc(f16v (&acc)[MT][2]) {
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = T{};
+    for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = f16v{};
 }
 
 // ---------------------------------------------------------------------------
@@ -316,76 +372,65 @@ struct GateArgsB {
   Key key;
   uint32_t i0;
   float eps;
+  uint16_t eps_b;
   RowMap rm;
 };
 
-// Workgroup: TM rows x 32 hidden units; LDS column rho = gate * 32 + unit.
-// Waves wn = 0 hold gates i, f and waves wn = 1 gates g, o of the same units;
-// after the main loop the wn = 1 waves pass their pre-activations through
-// LDS and the wn = 0 waves update the cell.
+// Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
+// is gate c / 16 of unit 16 wn + c % 16, so lane lr holds gates i, g (lr < 16)
+// or f, o (lr >= 16) of unit lr % 16 in its two column tiles, and one
+// exchange with lane lr ^ 16 brings all four gates of a (row, unit) together.
 template <int kind>
-__global__ __launch_bounds__(NT, 512 / NT) void gate_bf16_kernel(GateArgsB g) {
-  extern __shared__ __align__(16) uint16_t smem[];
+__global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
+  using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
-  const int u0 = blockIdx.x * 32;
+  const int u0 = blockIdx.x * (T::TN / 4);
   const int64_t m0 = (int64_t)blockIdx.y * TM;
   const int pair = (int)(m0 / g.rm.pair_rows);
+  const bool neg = (m0 + T::WROWS * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
   const int H = g.H;
   auto colmap = [&](int rho, int& n) {
-    n = (rho >> 5) * H + u0 + (rho & 31);
-    return true;
+    const int c = rho & 63;
+    n = (c >> 4) * H + u0 + 16 * (rho >> 6) + (c & 15);
   };
-  f16v accW[2][2], accZ[2][2];
-  zero_acc(accW);
-  zero_acc(accZ);
+  f16v acc[T::MT][2];
+  zero_acc(acc);
   const SegB s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
   const SegB s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
-  mainloop_bf16<kind>(accW, accZ, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, smem);
+  mainloop_bf16<kind>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
 
-  // pre-activations of this wave's two gates (2 wn, 2 wn + 1) for unit u
-  const int u = u0 + lr;
-  float bb[2], zz[2];
+  const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
+  const int u = u0 + 16 * wn + (lr & 15);
+  float bias[2];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
-    const int gate = 2 * wn + nt;
-    bb[nt] = bf16_to_f32(g.theta[g.off_b + (uint64_t)(gate * H + u)]);
-    zz[nt] = g.zb[(int64_t)pair * 4 * H + gate * H + u];
+    const int gate = 2 * nt + hi;
+    const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)(gate * H + u)]);
+    const float z = g.zb[(int64_t)pair * 4 * H + gate * H + u];
+    bias[nt] = neg ? b - z : b + z;
   }
-  __syncthreads();  // the main loop's LDS buffers are free from here on
-  float* xg = (float*)smem;  // [TM rows][32 units][2]: pre-activations of gates g, o
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
+  for (int mt = 0; mt < T::MT; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int lrow = acc_row(wm, mt, lg, v);
-      const bool neg = (m0 + lrow - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
-      const float se = neg ? -g.eps : g.eps;
-      float pre[2];
+    for (int v = 0; v < 16; v += 2) {
+      // lanes lr < 16 update row element v, lanes lr >= 16 element v + 1
+      float mine[2], send[2], got[2];
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-        pre[nt] = accW[mt][nt][v] + se * accZ[mt][nt][v] + (neg ? bb[nt] - zz[nt] : bb[nt] + zz[nt]);
-      if (wn == 1) *(float2*)(xg + (lrow * 32 + lr) * 2) = float2{pre[0], pre[1]};
-      accW[mt][0][v] = pre[0];  // keep i, f (wn == 0) for the cell update
-      accW[mt][1][v] = pre[1];
-    }
-  }
-  __syncthreads();
-  if (wn == 0) {
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int lrow = acc_row(wm, mt, lg, v);
-        const float2 go = *(const float2*)(xg + (lrow * 32 + lr) * 2);
-        const float ig = sigm(accW[mt][0][v]), fg = sigm(accW[mt][1][v]);
-        const float gg = tanh_(go.x), og = sigm(go.y);
-        const int64_t o = (m0 + lrow) * H + u;
-        const float c = fg * g.cst[o] + ig * gg;
-        g.cst[o] = c;
-        g.hout[o] = bf16_rne(og * tanh_(c));
+      for (int nt = 0; nt < 2; ++nt) {
+        const float p0 = acc[mt][nt][v] + bias[nt], p1 = acc[mt][nt][v + 1] + bias[nt];
+        mine[nt] = hi ? p1 : p0;
+        send[nt] = hi ? p0 : p1;
+        got[nt] = __shfl_xor(send[nt], 16, 64);
       }
+      const float ip = hi ? got[0] : mine[0], fp = hi ? mine[0] : got[0];
+      const float gp = hi ? got[1] : mine[1], op = hi ? mine[1] : got[1];
+      const int lrow = acc_row<kind>(wm, mt, lg, v + hi);
+      const int64_t o = (m0 + lrow) * H + u;
+      const float c = sigm(fp) * g.cst[o] + sigm(ip) * tanh_(gp);
+      g.cst[o] = c;
+      g.hout[o] = bf16_rne(sigm(op) * tanh_(c));
     }
   }
 }
@@ -400,6 +445,7 @@ struct HeadArgsB {
   Key key;
   uint32_t i0;
   float eps;
+  uint16_t eps_b;
   RowMap rm;
   int64_t M, rows;
   const int32_t* tokens;
@@ -410,59 +456,52 @@ struct HeadArgsB {
 };
 
 template <int kind>
-__global__ __launch_bounds__(NT, 512 / NT) void head_bf16_kernel(HeadArgsB g) {
-  extern __shared__ __align__(16) uint16_t smem[];
+__global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
+  using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   const int vt = blockIdx.x;
-  const int v0 = vt * TN;
+  const int v0 = vt * T::TN;
   const int64_t rr0 = (int64_t)blockIdx.y * TM;
   const int tt = (int)(rr0 / g.M);
   const int64_t r0 = rr0 - (int64_t)tt * g.M;
   const int pair = (int)(r0 / g.rm.pair_rows);
+  const bool neg = (r0 + T::WROWS * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
   const int V = g.V;
-  auto colmap = [&](int rho, int& n) {
-    n = v0 + rho;
-    const bool ok = n < V;
-    if (!ok) n = 0;
-    return ok;
-  };
-  f16v accW[2][2], accZ[2][2];
-  zero_acc(accW);
-  zero_acc(accZ);
+  auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
+  f16v acc[T::MT][2];
+  zero_acc(acc);
   const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
-  mainloop_bf16<kind>(accW, accZ, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, smem);
+  mainloop_bf16<kind>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
 
   int col[2];
   bool cok[2];
-  float bb[2], zz[2];
+  float bias[2];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
     col[nt] = v0 + 64 * wn + 32 * nt + lr;
     cok[nt] = col[nt] < V;
-    bb[nt] = cok[nt] ? bf16_to_f32(g.theta[g.off_b + (uint64_t)col[nt]]) : 0.f;
-    zz[nt] = cok[nt] ? g.zbo[(int64_t)pair * V + col[nt]] : 0.f;
+    const float b = cok[nt] ? bf16_to_f32(g.theta[g.off_b + (uint64_t)col[nt]]) : 0.f;
+    const float z = cok[nt] ? g.zbo[(int64_t)pair * V + col[nt]] : 0.f;
+    bias[nt] = neg ? b - z : b + z;
   }
-  __syncthreads();  // reuse the main loop's LDS for the cross-wave reduction
-  float* red_m = (float*)smem;   // [2][TM]
-  float* red_s = red_m + 2 * TM;  // [2][TM]
+  // cross-wave reduction in the first stage buffer (free after the loop)
+  float* red_m = (float*)stage<kind, 0>();         // [WAVES_N][TM]
+  float* red_s = red_m + T::WAVES_N * TM;          // [WAVES_N][TM]
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
+  for (int mt = 0; mt < T::MT; ++mt) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int lrow = acc_row(wm, mt, lg, v);
+      const int lrow = acc_row<kind>(wm, mt, lg, v);
       const int64_t r = r0 + lrow;
       const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
-      const bool neg = loc >= g.rm.Bp;
       const int b = neg ? loc - g.rm.Bp : loc;
-      const float se = neg ? -g.eps : g.eps;
       float y[2];
       float mx = -INFINITY;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        y[nt] = cok[nt] ? accW[mt][nt][v] + se * accZ[mt][nt][v] + (neg ? bb[nt] - zz[nt] : bb[nt] + zz[nt])
-                        : -INFINITY;
+        y[nt] = cok[nt] ? acc[mt][nt][v] + bias[nt] : -INFINITY;
         mx = fmaxf(mx, y[nt]);
       }
       if (b < g.B) {
@@ -474,25 +513,30 @@ __global__ __launch_bounds__(NT, 512 / NT) void head_bf16_kernel(HeadArgsB g) {
       // the row's 64 columns of this wave sit in the 32 lanes of this lane half
 #pragma unroll
       for (int off = 1; off < 32; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-      float se2 = 0.f;
+      float se = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) se2 += cok[nt] ? __expf(y[nt] - mx) : 0.f;
+      for (int nt = 0; nt < 2; ++nt) se += cok[nt] ? __expf(y[nt] - mx) : 0.f;
 #pragma unroll
-      for (int off = 1; off < 32; off <<= 1) se2 += __shfl_xor(se2, off, 64);
+      for (int off = 1; off < 32; off <<= 1) se += __shfl_xor(se, off, 64);
       if (lr == 0) {
         red_m[wn * TM + lrow] = mx;
-        red_s[wn * TM + lrow] = se2;
+        red_s[wn * TM + lrow] = se;
       }
     }
   }
   __syncthreads();
   if (t < TM) {
-    const float m_a = red_m[t], m_b = red_m[TM + t];
-    const float mx = fmaxf(m_a, m_b);
-    const float sa = m_a == -INFINITY ? 0.f : red_s[t] * __expf(m_a - mx);
-    const float sb = m_b == -INFINITY ? 0.f : red_s[TM + t] * __expf(m_b - mx);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < T::WAVES_N; ++w) mx = fmaxf(mx, red_m[w * TM + t]);
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < T::WAVES_N; ++w) {
+      const float m = red_m[w * TM + t];
+      sum += m == -INFINITY ? 0.f : red_s[w * TM + t] * __expf(m - mx);
+    }
     g.pmax[(int64_t)vt * g.rows + rr0 + t] = mx;
-    g.psum[(int64_t)vt * g.rows + rr0 + t] = sa + sb;
+    g.psum[(int64_t)vt * g.rows + rr0 + t] = sum;
   }
 }
 
@@ -534,16 +578,6 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
   *(uint2*)(x0 + r * E + e) = uint2{lo, hi};
 }
 
-template <typename K>
-hipError_t allow_smem(K kernel, size_t bytes) {
-  static bool done = false;  // set once per kernel instantiation (same value on every device)
-  if (done) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)bytes);
-  if (e == hipSuccess) done = true;
-  return e;
-}
-
 }  // namespace
 
 hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
@@ -583,19 +617,16 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.key = make_key(a.seed);
   g.i0 = a.i0;
   g.eps = a.eps;
+  g.eps_b = bf16_rne(a.eps);
   g.rm = RowMap{R.Bp, R.pair_rows};
-  const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / TM));
-  hipError_t e;
   if (a.cfg.probe == ZO_RADEMACHER) {
-    constexpr size_t sb = smem_bytes<ZO_RADEMACHER>();
-    if ((e = allow_smem(gate_bf16_kernel<ZO_RADEMACHER>, sb)) != hipSuccess) return e;
+    const dim3 grid((unsigned)(g.H / (Tiles<ZO_RADEMACHER>::TN / 4)), (unsigned)(R.M / TM));
     ProfScope ps(kKGate, st);
-    gate_bf16_kernel<ZO_RADEMACHER><<<grid, NT, sb, st>>>(g);
+    gate_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(g);
   } else {
-    constexpr size_t sb = smem_bytes<ZO_GAUSSIAN>();
-    if ((e = allow_smem(gate_bf16_kernel<ZO_GAUSSIAN>, sb)) != hipSuccess) return e;
+    const dim3 grid((unsigned)(g.H / (Tiles<ZO_GAUSSIAN>::TN / 4)), (unsigned)(R.M / TM));
     ProfScope ps(kKGate, st);
-    gate_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, sb, st>>>(g);
+    gate_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(g);
   }
   return hipGetLastError();
 }
@@ -614,6 +645,7 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.key = make_key(a.seed);
   h.i0 = a.i0;
   h.eps = a.eps;
+  h.eps_b = bf16_rne(a.eps);
   h.rm = RowMap{R.Bp, R.pair_rows};
   h.M = R.M;
   h.rows = (int64_t)Tc * R.M;
@@ -625,17 +657,12 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.psum = psum;
   h.ptgt = ptgt;
   const dim3 grid((unsigned)a.ws.nvt, (unsigned)(h.rows / TM));
-  hipError_t e;
   if (a.cfg.probe == ZO_RADEMACHER) {
-    constexpr size_t sb = smem_bytes<ZO_RADEMACHER>();
-    if ((e = allow_smem(head_bf16_kernel<ZO_RADEMACHER>, sb)) != hipSuccess) return e;
     ProfScope ps(kKHead, st);
-    head_bf16_kernel<ZO_RADEMACHER><<<grid, NT, sb, st>>>(h);
+    head_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(h);
   } else {
-    constexpr size_t sb = smem_bytes<ZO_GAUSSIAN>();
-    if ((e = allow_smem(head_bf16_kernel<ZO_GAUSSIAN>, sb)) != hipSuccess) return e;
     ProfScope ps(kKHead, st);
-    head_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, sb, st>>>(h);
+    head_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(h);
   }
   return hipGetLastError();
 }

@@ -90,8 +90,13 @@ inline Rows make_rows(int32_t N, int32_t B, int granule) {
 // Time steps whose top-layer states are kept for one batched output-head pass.
 constexpr int kTimeChunk = 16;
 
-// Output-head vocabulary tile (columns per workgroup).
+// Output-head vocabulary tile (columns per workgroup): 256 on the bf16 path
+// with sign probes, 128 otherwise.
 constexpr int kVocabTile = 128;
+constexpr int kVocabTileWide = 256;
+inline int vocab_tile(const zo_config& c) {
+  return c.wdtype == ZO_WBF16 && c.probe == ZO_RADEMACHER ? kVocabTileWide : kVocabTile;
+}
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -118,7 +123,8 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
   const size_t L = (size_t)c.n_layers;
   const size_t el = c.wdtype == ZO_WBF16 ? 2 : 4;  // activation operand element size
   w.T = C < kTimeChunk ? C : kTimeChunk;
-  w.nvt = (int)((V + kVocabTile - 1) / kVocabTile);
+  const size_t vt = (size_t)vocab_tile(c);
+  w.nvt = (int)((V + vt - 1) / vt);
   size_t p = 0;
   auto take = [&](size_t bytes) {
     size_t o = p;
