@@ -47,7 +47,12 @@ constexpr int NWAVES = 8;
 constexpr int NT = 64 * NWAVES;  // threads per workgroup
 constexpr int kRowBytes = TK * 2;
 constexpr int kABytes = TM * kRowBytes;
-constexpr int kACopies = kABytes / (NT * 16);  // 16-byte global->LDS copies per thread
+// Global->LDS copies: each copy instruction moves 1 KB (64 lanes x 16 B).
+// kCopyWaves of the 8 waves issue them, spread over the first kCopySteps k
+// steps of the previous K tile.
+constexpr int kCopyWaves = 4;
+constexpr int kCopySteps = 1;
+constexpr int kACopies = kABytes / 1024 / kCopyWaves;  // activation copies per copying wave
 
 // Per probe kind: workgroup columns, wave grid, MFMA tiles per wave, LDS.
 template <int kind>
@@ -59,12 +64,13 @@ struct Tiles {
   static constexpr int MT = WROWS / 32;
   static constexpr int WBytes = TN * kRowBytes;
   static constexpr int ZBytes = kind == ZO_RADEMACHER ? TN * 8 : TN * kRowBytes;
-  static constexpr int WCopies = WBytes / (NT * 16);
+  static constexpr int WCopies = WBytes / 1024 / kCopyWaves;  // weight copies per copying wave
   static constexpr int Copies = kACopies + WCopies;
   static constexpr int ZROW_T = NT / TN;     // threads per probe-tile row (normal probes)
   static constexpr int ZVALS = TK / ZROW_T;  // probe values per thread and K tile (normal probes)
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
-  static_assert(WCopies * NT * 16 == WBytes && kACopies * NT * 16 == kABytes, "copy split");
+  static_assert(WCopies * kCopyWaves * 1024 == WBytes && kACopies * kCopyWaves * 1024 == kABytes,
+                "copy split");
   static_assert(kind != ZO_RADEMACHER || TN * 2 == NT, "one sign word per thread");
   static_assert(kind == ZO_RADEMACHER || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
@@ -165,7 +171,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   const int lr = lane & 31, lg = lane >> 5;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
 
-  // copy roles: copy q of wave w fills rows 8 (q NWAVES + w) .. +7 of the
+  // copy roles: copy q of copying wave w fills rows 8 (q kCopyWaves + w) .. +7 of the
   // activation (q < kACopies) or weight tile, 1 KB lane-linear in LDS: lane
   // L writes row + L / 8, slot L % 8, which holds chunk (L % 8) ^ ((row >> 1) & 7)
   const int crow = lane >> 3;
@@ -173,13 +179,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   uint32_t aoff[kACopies], woff[T::WCopies];  // element offsets of the chunk inside the row
 #pragma unroll
   for (int q = 0; q < kACopies; ++q) {
-    const int r = 8 * (q * NWAVES + wave) + crow;
+    const int r = 8 * (q * kCopyWaves + wave % kCopyWaves) + crow;
     arow[q] = r;
     aoff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
   }
 #pragma unroll
   for (int q = 0; q < T::WCopies; ++q) {
-    const int r = 8 * (q * NWAVES + wave) + crow;
+    const int r = 8 * (q * kCopyWaves + wave % kCopyWaves) + crow;
     colmap(r, wrow[q]);
     woff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
   }
@@ -193,21 +199,27 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   Words zcache{{0u, 0u, 0u, 0u}};
   int seg = 0, k0 = 0;
 
-  // Issue the next K tile into stage S: the global->LDS copies of the
-  // activation and weight rows, then the probe tile computed in registers
-  // and written to LDS.
-  auto issue = [&](auto stage_tag) {
+  // Issue the next K tile into stage S, in four parts spread over the
+  // current tile's k steps (so that no wave stalls on a burst of copies):
+  // parts 0 and 1 the global->LDS copies of the activation and weight rows,
+  // half each; part 2 the probe tile, computed in registers and written to
+  // LDS; part 3 advances to the following tile.
+  auto issue = [&](auto stage_tag, auto part_tag) {
     constexpr int S = decltype(stage_tag)::value;
+    constexpr int P = decltype(part_tag)::value;
     uint8_t* base = stage<kind, S>();
     const SegB sg = seg == 0 ? s0 : s1;
+    if (wave < kCopyWaves) {
 #pragma unroll
-    for (int q = 0; q < kACopies; ++q)
-      copy_to_lds(sg.A + (int64_t)arow[q] * sg.lda + k0 + aoff[q], base + (q * NWAVES + wave) * 1024);
-#pragma unroll
-    for (int q = 0; q < T::WCopies; ++q)
-      copy_to_lds(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
-                  base + kABytes + (q * NWAVES + wave) * 1024);
-    if constexpr (kind == ZO_RADEMACHER) {
+      for (int c = P * T::Copies / kCopySteps; c < (P < kCopySteps ? (P + 1) * T::Copies / kCopySteps : 0); ++c) {
+        if (c < kACopies)
+          copy_to_lds(sg.A + (int64_t)arow[c] * sg.lda + k0 + aoff[c], base + (c * kCopyWaves + wave) * 1024);
+        else
+          copy_to_lds(sg.W + (int64_t)wrow[c - kACopies] * sg.ldw + k0 + woff[c - kACopies],
+                      base + kABytes + ((c - kACopies) * kCopyWaves + wave) * 1024);
+      }
+    }
+    if constexpr (P == 2 && kind == ZO_RADEMACHER) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 32 * zpart;
       uint32_t word;
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
@@ -220,7 +232,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       }
       // negative-sign flags in unshuffled order
       sign_bits<S>()[zr * 2 + zpart] = unshuffle_bits(~word);
-    } else {
+    } else if constexpr (P == 2) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
       uint8_t* zrow = base + kABytes + T::WBytes + zr * kRowBytes;
 #pragma unroll
@@ -234,11 +246,19 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
                pack_bf16x2(eps * zb[0], eps * zb[1]), pack_bf16x2(eps * zb[2], eps * zb[3])};
       }
     }
-    k0 += TK;
-    if (k0 == sg.K) {
-      k0 = 0;
-      ++seg;
+    if constexpr (P == 3) {
+      k0 += TK;
+      if (k0 == sg.K) {
+        k0 = 0;
+        ++seg;
+      }
     }
+  };
+  auto issue_all = [&](auto stage_tag) {
+    issue(stage_tag, std::integral_constant<int, 0>{});
+    issue(stage_tag, std::integral_constant<int, 1>{});
+    issue(stage_tag, std::integral_constant<int, 2>{});
+    issue(stage_tag, std::integral_constant<int, 3>{});
   };
 
   // Fragments of one 16-k step: activations (MT row tiles), weights and
@@ -256,7 +276,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   struct Frag {
     bf8 a[MT], w[2], z[2];
   };
-  auto compute = [&](auto stage_tag) {
+  auto compute = [&](auto stage_tag, bool more) {
     constexpr int S = decltype(stage_tag)::value;
     const uint8_t* base = stage<kind, S>();
     const uint8_t* pa = base + a_lane;
@@ -311,6 +331,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
           acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
+      if (more) {
+        constexpr std::integral_constant<int, 1 - S> next{};
+        if (s == 0) issue(next, std::integral_constant<int, 0>{});
+        if (s == 1) issue(next, std::integral_constant<int, 1>{});
+        if (s == 2) issue(next, std::integral_constant<int, 2>{});
+        if (s == 3) issue(next, std::integral_constant<int, 3>{});
+      }
       if (s + 1 < TK / 16) {
         // per step: the next step's LDS reads first, then each MFMA followed by
         // a few VALU instructions of the next step's probe fragments
@@ -326,19 +353,38 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
 
   // K tile it lives in stage it % 2. Per tile: wait for this thread's copies
   // and LDS writes of tile it; barrier (tile it complete for every wave, and
-  // the other stage, computed at it - 1, free); issue tile it + 1; compute it.
+  // the other stage, computed at it - 1, free); compute it while issuing
+  // tile it + 1.
   auto step = [&](auto stage_tag, int it) {
-    constexpr int S = decltype(stage_tag)::value;
     wait_and_barrier();
-    if (it + 1 < ntiles) issue(std::integral_constant<int, 1 - S>{});
-    compute(stage_tag);
+    compute(stage_tag, it + 1 < ntiles);
   };
-  issue(std::integral_constant<int, 0>{});
+  issue_all(std::integral_constant<int, 0>{});
   for (int it = 0; it < ntiles; it += 2) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
   }
   __syncthreads();  // every wave done with the stages before they are reused
+}
+
+// Tile (row block m, column block n) of workgroup L of a 1-D grid of nm x nn
+// tiles. Workgroups are dispatched to the 8 XCDs in turn (L % 8), each XCD
+// with its own L2: XCD x takes the row blocks [x nm/8, (x+1) nm/8) and sweeps
+// the column blocks in groups of R row blocks, so that the 32 workgroups an
+// XCD runs at a time share R activation and 32 / R weight tiles, and all
+// XCDs read the same weight columns at the same time. Shapes with nm not a
+// multiple of 8 take the plain row-major order. Any order is correct.
+__device__ __forceinline__ void tile_of(int L, int nm, int nn, int& m, int& n) {
+  if (nm % 8 != 0) {
+    m = L / nn;
+    n = L - m * nn;
+    return;
+  }
+  const int x = L & 7, j = L >> 3, per = nm >> 3;
+  const int R = per % 4 == 0 ? 4 : per % 2 == 0 ? 2 : 1;
+  const int g = j / (R * nn), rem = j - g * (R * nn);
+  n = rem / R;
+  m = x * per + g * R + (rem - n * R);
 }
 
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
@@ -374,6 +420,7 @@ struct GateArgsB {
   float eps;
   uint16_t eps_b;
   RowMap rm;
+  int n_row_blocks;  // M / TM
 };
 
 // Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
@@ -386,8 +433,10 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
-  const int u0 = blockIdx.x * (T::TN / 4);
-  const int64_t m0 = (int64_t)blockIdx.y * TM;
+  int mb, nb;
+  tile_of(blockIdx.x, g.n_row_blocks, g.H / (T::TN / 4), mb, nb);
+  const int u0 = nb * (T::TN / 4);
+  const int64_t m0 = (int64_t)mb * TM;
   const int pair = (int)(m0 / g.rm.pair_rows);
   const bool neg = (m0 + T::WROWS * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
   const int H = g.H;
@@ -453,6 +502,7 @@ struct HeadArgsB {
   float* pmax;
   float* psum;
   float* ptgt;
+  int nvt;  // vocabulary tiles
 };
 
 template <int kind>
@@ -461,9 +511,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
-  const int vt = blockIdx.x;
+  int mb, vt;
+  tile_of(blockIdx.x, (int)(g.rows / TM), g.nvt, mb, vt);
   const int v0 = vt * T::TN;
-  const int64_t rr0 = (int64_t)blockIdx.y * TM;
+  const int64_t rr0 = (int64_t)mb * TM;
   const int tt = (int)(rr0 / g.M);
   const int64_t r0 = rr0 - (int64_t)tt * g.M;
   const int pair = (int)(r0 / g.rm.pair_rows);
@@ -619,12 +670,13 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.eps = a.eps;
   g.eps_b = bf16_rne(a.eps);
   g.rm = RowMap{R.Bp, R.pair_rows};
+  g.n_row_blocks = (int)(R.M / TM);
   if (a.cfg.probe == ZO_RADEMACHER) {
-    const dim3 grid((unsigned)(g.H / (Tiles<ZO_RADEMACHER>::TN / 4)), (unsigned)(R.M / TM));
+    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_RADEMACHER>::TN / 4))));
     ProfScope ps(kKGate, st);
     gate_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(g);
   } else {
-    const dim3 grid((unsigned)(g.H / (Tiles<ZO_GAUSSIAN>::TN / 4)), (unsigned)(R.M / TM));
+    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_GAUSSIAN>::TN / 4))));
     ProfScope ps(kKGate, st);
     gate_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(g);
   }
@@ -656,7 +708,8 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.pmax = pmax;
   h.psum = psum;
   h.ptgt = ptgt;
-  const dim3 grid((unsigned)a.ws.nvt, (unsigned)(h.rows / TM));
+  h.nvt = a.ws.nvt;
+  const dim3 grid((unsigned)((int64_t)a.ws.nvt * (h.rows / TM)));
   if (a.cfg.probe == ZO_RADEMACHER) {
     ProfScope ps(kKHead, st);
     head_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(h);
