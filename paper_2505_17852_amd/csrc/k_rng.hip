@@ -85,15 +85,18 @@ __device__ __forceinline__ void store4(T* theta, uint64_t j, uint64_t P, const f
 
 // Rademacher update. sum_n c_n z_n[j] with z = +-1 is, for each group of 8
 // probes, a table lookup: T_g[m] = sum over the group of (bit n of m ? +c_n :
-// -c_n) for the 256 sign patterns m (built once per workgroup and group).
-// A workgroup owns 8192 consecutive parameters (256 Philox words per probe);
-// each thread loads its 4 sets of 8 parameters up front (four 16-byte loads
-// in flight per thread), then for each group of up to 16 probes the
+// -c_n) for the 256 sign patterns m. Persistent workgroups (as many as fit
+// at once) walk chunks of 8192 consecutive parameters (256 Philox words per
+// probe); a thread owns 4 sets of 8 parameters of a chunk, and the next
+// chunk's theta loads are issued when the current chunk starts, so they run
+// during its probe work. With at most 16 probes the coefficients and tables
+// are built once per workgroup. Per chunk and group of up to 16 probes, the
 // workgroup computes their Philox blocks into LDS (4 per thread), and each
 // thread takes, for each set of 8 parameters, one byte of sign bits from
 // each of 8 probes, transposes that 8x8 bit block (three swap stages) so that
 // byte e holds parameter e's signs, and adds one table entry per parameter
-// and group of 8. theta is read and written once.
+// and group of 8. theta is read and written once. The kernel is bound by
+// these VALU instructions (about 23 per parameter at 16 probes), not by HBM.
 constexpr int kUpdChunk = 8192;   // parameters per workgroup (32 per thread, 4 sets of 8)
 constexpr int kUpdWords = kUpdChunk / 32;
 constexpr int kUpdGroup = 16;     // probes per pass over the LDS tables
@@ -137,13 +140,21 @@ __device__ __forceinline__ void load8(const T* theta, uint64_t j, uint64_t P, fl
   }
 }
 
+// Two fp32 values to packed bf16 (round to nearest even) with one
+// v_cvt_pk_bf16_f32; the same rounding as bf16_rne for finite values.
+__device__ __forceinline__ uint32_t pack_bf16x2_rne(float lo, float hi) {
+  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){lo, hi}, bf2));
+}
+
 template <typename T>
 __device__ __forceinline__ void store8(T* theta, uint64_t j, uint64_t P, const float v[8]) {
   if (j + 8 <= P) {
     if constexpr (sizeof(T) == 2) {
       uint32_t w[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)bf16_rne(v[2 * e]) | ((uint32_t)bf16_rne(v[2 * e + 1]) << 16);
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2_rne(v[2 * e], v[2 * e + 1]);
       *(uint4*)(theta + j) = uint4{w[0], w[1], w[2], w[3]};
     } else {
       *(float4*)(theta + j) = float4{v[0], v[1], v[2], v[3]};
@@ -155,11 +166,60 @@ __device__ __forceinline__ void store8(T* theta, uint64_t j, uint64_t P, const f
   }
 }
 
+// Eight parameters j .. j + 7 as stored (bf16 or fp32 bit patterns; zeros
+// past P). Whole-workgroup chunks inside theta take plain 16-byte loads
+// with no bounds checks, so that a thread's loads issue back to back.
 template <typename T>
-__global__ __launch_bounds__(256) void update_rademacher_kernel(T* theta, uint64_t P, Key key,
-                                                                float eps, float lr, int N,
-                                                                uint32_t i0, const float* Lp,
-                                                                const float* Lm, int32_t* skipped) {
+struct Raw8 {
+  uint4 w[8 * sizeof(T) / 16];
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load_raw8(const T* theta, uint64_t j, uint64_t P, bool full) {
+  Raw8<T> r;
+  constexpr int kW = 8 * sizeof(T) / 16, kPer = 16 / sizeof(T);
+  if (full) {
+#pragma unroll
+    for (int w = 0; w < kW; ++w) r.w[w] = *(const uint4*)(theta + j + (uint64_t)w * kPer);
+  } else {
+    T v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = j + e < P ? theta[j + e] : (T)0;
+    __builtin_memcpy(&r, v, sizeof(v));
+  }
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void decode_raw8(const Raw8<T>& r, float v[8]) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t x = w == 0 ? r.w[0].x : w == 1 ? r.w[0].y : w == 2 ? r.w[0].z : r.w[0].w;
+      v[2 * w] = bf16_to_f32((uint16_t)x);
+      v[2 * w + 1] = bf16_to_f32((uint16_t)(x >> 16));
+    }
+  } else {
+    __builtin_memcpy(v, &r, 32);
+  }
+}
+
+// Workgroup barrier for LDS data only: waits for this thread's LDS accesses
+// (lgkmcnt(0)), not for its global loads, which stay in flight across it.
+// The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt, expcnt at their maxima; lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ theta, uint64_t P, Key key,
+                                                                float eps, float lr, int N, uint32_t i0,
+                                                                const float* __restrict__ Lp,
+                                                                const float* __restrict__ Lm,
+                                                                int32_t* __restrict__ skipped,
+                                                                uint64_t nchunks) {
   // sign words laid out [word][probe] (rows padded by 4 words) so that one
   // thread reads 8 probes' words of its parameters with two 128-bit loads
   constexpr int kRow = kUpdGroup + 4;
@@ -168,59 +228,108 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* theta, uint64
   __shared__ float table[kUpdGroup / 8][256];      // signed-sum tables
   __shared__ float half_table[kUpdGroup / 8][32];  // 4-probe partial sums
   __shared__ float coef[kUpdGroup];
-  __shared__ int flag;
-  const bool ok = losses_finite(Lp, Lm, N, &flag);
-  if (blockIdx.x == 0 && threadIdx.x == 0 && skipped) *skipped = ok ? 0 : 1;
-  if (!ok) return;
+  __shared__ int bad;  // some loss is not finite
   const int t = threadIdx.x;
-  const uint64_t base = (uint64_t)blockIdx.x * kUpdChunk;
-  float th[kSets][8];
-#pragma unroll
-  for (int q = 0; q < kSets; ++q) load8(theta, base + 2048u * q + 8u * t, P, th[q]);
-  float acc[kSets][8];
-#pragma unroll
-  for (int q = 0; q < kSets; ++q)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
   const uint32_t k = (uint32_t)(t & 3);  // this thread's byte within each of its words
   // byte-gather selectors for v_perm: byte k of the low and high source -> bytes 0, 1
   const uint32_t sel = k | ((4u + k) << 8) | 0x0C0C0000u;
-  for (int n0 = 0; n0 < N; n0 += kUpdGroup) {
-    const int cnt = N - n0 < kUpdGroup ? N - n0 : kUpdGroup;
-    const int ngroups = (cnt + 7) / 8;
-    __syncthreads();
-    if (t < kUpdGroup) coef[t] = t < cnt ? update_coeff(lr, N, Lp[n0 + t], Lm[n0 + t], eps) : 0.f;
-    // Philox blocks: cnt probes x 64 blocks (probes past cnt only ever meet zero coefficients)
-    for (int q = t; q < cnt * (kUpdWords / 4); q += 256) {
-      const int pn = q / (kUpdWords / 4), pb = q % (kUpdWords / 4);
-      const Words x = stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
+  const bool one_group = N <= kUpdGroup;  // coefficients and tables built once
+
+  // The workgroup walks its chunks (8192 parameters each) blockIdx.x,
+  // blockIdx.x + gridDim.x, ...; the next chunk's theta loads are issued at
+  // the start of the current one, so they run during its probe work.
+  auto load_chunk = [&](uint64_t chunk, Raw8<T> (&r)[kSets]) {
+    const uint64_t base = chunk * kUpdChunk;
+    if (base + kUpdChunk <= P) {  // the same for the whole workgroup
 #pragma unroll
-      for (int w = 0; w < 4; ++w) words[(4 * pb + w) * kRow + pn] = x.w[w];
+      for (int q = 0; q < kSets; ++q) r[q] = load_raw8(theta, base + 2048u * q + 8u * t, P, true);
+    } else {
+#pragma unroll
+      for (int q = 0; q < kSets; ++q) r[q] = load_raw8(theta, base + 2048u * q + 8u * t, P, false);
     }
-    __syncthreads();
-    // 4-probe partial tables, then T[m] = low[m & 15] + high[m >> 4]
+  };
+  // coefficients of probes n0 .. n0 + cnt - 1 into LDS and the finite flag
+  // (threads t < cnt; needs a barrier after)
+  auto coefficients = [&](int n0, int cnt, float lp, float lm) {
+    if (t < kUpdGroup) {
+      coef[t] = t < cnt ? update_coeff(lr, N, lp, lm, eps) : 0.f;
+      if (t < cnt && !(isfinite(lp) && isfinite(lm))) atomicOr(&bad, 1);
+    }
+  };
+  // signed-sum tables of the current coefficients: 4-probe partial tables,
+  // then T[m] = low[m & 15] + high[m >> 4] (two barriers)
+  auto tables = [&](int ngroups) {
     if (t < ngroups * 32) {
       const int g = t >> 5, h = (t >> 4) & 1, m = t & 15;
       float v = 0.f;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        const float c = coef[8 * g + 4 * h + b];
-        v += ((m >> b) & 1) ? c : -c;
+        const float cb = coef[8 * g + 4 * h + b];
+        v += ((m >> b) & 1) ? cb : -cb;
       }
       half_table[g][16 * h + m] = v;
     }
-    __syncthreads();
+    lds_barrier();
     for (int q = t; q < ngroups * 256; q += 256) {
       const int g = q >> 8, m = q & 255;
       table[g][m] = half_table[g][m & 15] + half_table[g][16 + (m >> 4)];
     }
-    __syncthreads();
+    lds_barrier();
+  };
+
+  // the first group's losses, then the first chunk's theta: loads complete
+  // in issue order, so waiting for the losses leaves theta in flight
+  float lp = 0.f, lm = 0.f;
+  if (t < kUpdGroup && t < N) {
+    lp = Lp[t];
+    lm = Lm[t];
+  }
+  uint64_t chunk = blockIdx.x;
+  Raw8<T> raw[kSets];
+  if (chunk < nchunks) load_chunk(chunk, raw);
+  if (t == 0) bad = 0;  // set before the first barrier
+  if (one_group) {
+    lds_barrier();
+    coefficients(0, N, lp, lm);
+    lds_barrier();
+    tables((N + 7) / 8);
+  }
+  for (; chunk < nchunks; chunk += gridDim.x) {
+    const uint64_t base = chunk * kUpdChunk;
+    Raw8<T> next[kSets];
+    const uint64_t nxt = chunk + gridDim.x;
+    if (nxt < nchunks) load_chunk(nxt, next);
+    float acc[kSets][8];
 #pragma unroll
-    for (int q = 0; q < kSets; ++q) {
-      const uint32_t* wrow = words + (64 * q + (t >> 2)) * kRow;
-      for (int g = 0; g < ngroups; ++g) {
-        const uint4 a = *(const uint4*)(wrow + 8 * g);
-        const uint4 b = *(const uint4*)(wrow + 8 * g + 4);
+    for (int q = 0; q < kSets; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
+    for (int n0 = 0; n0 < N; n0 += kUpdGroup) {
+      const int cnt = N - n0 < kUpdGroup ? N - n0 : kUpdGroup;
+      const int ngroups = (cnt + 7) / 8;
+      if (!one_group && t < cnt) {
+        lp = Lp[n0 + t];
+        lm = Lm[n0 + t];
+      }
+      lds_barrier();  // the previous lookups no longer read the words or tables
+      if (!one_group) coefficients(n0, cnt, lp, lm);
+      // Philox blocks: cnt probes x 64 blocks (probes past cnt only ever meet zero coefficients)
+      for (int q = t; q < cnt * (kUpdWords / 4); q += 256) {
+        const int pn = q / (kUpdWords / 4), pb = q % (kUpdWords / 4);
+        const Words x = stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) words[(4 * pb + w) * kRow + pn] = x.w[w];
+      }
+      lds_barrier();
+      if (!one_group) tables(ngroups);
+      // lookups: for each set of 8 parameters and group of 8 probes, byte k
+      // of each probe's word, transposed so that byte e holds parameter e's
+      // 8 signs, then one table entry per parameter (groups of a full pass
+      // of 16 probes unrolled)
+      auto lookup = [&](int q, int g) {
+        const uint32_t* wrow = words + (64 * q + (t >> 2)) * kRow + 8 * g;
+        const uint4 a = *(const uint4*)(wrow);
+        const uint4 b = *(const uint4*)(wrow + 4);
         // byte k of each of the 8 probes' words, probe order, into (lo, hi)
         uint32_t lo = __builtin_amdgcn_perm(a.y, a.x, sel) | (__builtin_amdgcn_perm(a.w, a.z, sel) << 16);
         uint32_t hi = __builtin_amdgcn_perm(b.y, b.x, sel) | (__builtin_amdgcn_perm(b.w, b.z, sel) << 16);
@@ -230,15 +339,34 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* theta, uint64
           acc[q][e] += table[g][(lo >> (8 * e)) & 0xFFu];
           acc[q][4 + e] += table[g][(hi >> (8 * e)) & 0xFFu];
         }
+      };
+      if (ngroups == kUpdGroup / 8) {
+#pragma unroll
+        for (int q = 0; q < kSets; ++q)
+#pragma unroll
+          for (int g = 0; g < kUpdGroup / 8; ++g) lookup(q, g);
+      } else {
+#pragma unroll
+        for (int q = 0; q < kSets; ++q)
+          for (int g = 0; g < ngroups; ++g) lookup(q, g);
       }
     }
-  }
+    // a non-finite loss leaves theta untouched (every workgroup decides
+    // alike; the flag was last written before a barrier already passed)
+    const bool finite = bad == 0;
+    if (chunk == 0 && t == 0 && skipped) *skipped = finite ? 0 : 1;
+    if (finite) {
 #pragma unroll
-  for (int q = 0; q < kSets; ++q) {
-    float out[8];
+      for (int q = 0; q < kSets; ++q) {
+        float th[8], out[8];
+        decode_raw8(raw[q], th);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) out[e] = th[q][e] - acc[q][e];
-    store8(theta, base + 2048u * q + 8u * t, P, out);
+        for (int e = 0; e < 8; ++e) out[e] = th[e] - acc[q][e];
+        store8(theta, base + 2048u * q + 8u * t, P, out);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kSets; ++q) raw[q] = next[q];
   }
 }
 
@@ -315,13 +443,25 @@ hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t
   const Key key = make_key(seed);
   ProfScope ps(kKUpdate, s);
   if (kind == ZO_RADEMACHER) {
-    const uint64_t grid = (P + kUpdChunk - 1) / kUpdChunk;
+    // persistent workgroups: as many as fit on the device at once, each
+    // walking chunks of kUpdChunk parameters
+    const uint64_t nchunks = (P + kUpdChunk - 1) / kUpdChunk;
+    int dev = 0, cus = 0, per_cu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+      e = wdtype == ZO_WBF16
+              ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<uint16_t>, 256, 0)
+              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<float>, 256, 0);
+    if (e != hipSuccess) return e;
+    const uint64_t slots = (uint64_t)(cus > 0 ? cus : 1) * (uint64_t)(per_cu > 0 ? per_cu : 1);
+    const unsigned grid = (unsigned)(nchunks < slots ? nchunks : slots);
     if (wdtype == ZO_WBF16)
-      update_rademacher_kernel<uint16_t><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped);
+      update_rademacher_kernel<uint16_t><<<dim3(grid), dim3(256), 0, s>>>(
+          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks);
     else
-      update_rademacher_kernel<float><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped);
+      update_rademacher_kernel<float><<<dim3(grid), dim3(256), 0, s>>>(
+          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks);
   } else {
     const uint64_t grid = ((P + 3) / 4 + 255) / 256;
     if (wdtype == ZO_WBF16)
