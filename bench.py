@@ -24,6 +24,7 @@ if ROOT not in sys.path:
 
 METRIC = "perturbed-forward tokens/sec per CD-RGE step (2N·B·C/s); % MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
+HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
 DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 1), "c4": (1, 1), "c5": (1, 3)}
 DESCRIPTION = {
     "c1": "1-layer LSTM V=256 E=32 H=64 fp32; B=4 C=32 uniform tokens; N=8 Rademacher",
@@ -70,6 +71,18 @@ def measured_traffic(name, dtype):
             if len(parts) == 5 and parts[0] == "traffic" and parts[1] == name and parts[2] == want:
                 return float(parts[3]) + float(parts[4])
     return None
+
+
+def update_hbm(P, w, upd):
+    """Algorithmic HBM rate of the update kernel (theta read and written
+    once) from its HIP-event time, against the 8 TB/s HBM3E peak."""
+    ms, n = upd
+    if n == 0 or ms <= 0:
+        return None
+    t = ms / n * 1e-3
+    gbps = 2 * P * w / t / 1e9
+    return {"bytes": 2 * P * w, "ms_per_launch": ms / n, "GBps": gbps, "peak_GBps": HBM_PEAK_GBPS,
+            "frac": gbps / HBM_PEAK_GBPS}
 
 
 def cpu_baseline(name, budget_s=20.0):
@@ -209,6 +222,8 @@ def main():
                      # streams: executed matrix work is twice the algorithmic work
                      "executed_frac": None if achieved is None else achieved * mult / peak},
         "step_mfma_frac_algorithmic": fwd_flops / (dt / K) / 1e12 / peak,
+        # the parameter update reads and writes theta once: 2 P w bytes
+        "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"]),
         "kernels": kernels,
         "losses_finite": losses_ok,
     }

@@ -1,0 +1,75 @@
+"""Multi-step CD-RGE training on the GPU (paper_2505_17852_amd.train):
+a few steps against the same steps run by the CPU oracle, and a convergence
+smoke test (the loss of a fixed batch falls under CD-RGE steps, the paper's
+overfitting experiment in miniature)."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from paper_2505_17852_amd import workloads as wl  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def zo():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_17852_amd import zo as z
+    z.lib()
+    return z
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+@pytest.mark.parametrize("probe", [wl.RADEMACHER, wl.GAUSSIAN], ids=["rademacher", "gaussian"])
+def test_training_steps_match_oracle(zo, oracle, probe):
+    """Four steps of the c1 shape (fp32): per-step loss estimates within
+    1e-5 relative of the oracle's, and theta after the four steps within
+    the fp32 update tolerance. The oracle runs its own trajectory (its own
+    losses feed its own updates)."""
+    from paper_2505_17852_amd import train
+    cfg = wl.model_cfg("c1", probe=probe)
+    w = wl.CONFIGS["c1"]
+    tok, _ = wl.batch("c1")
+    steps, seed0 = 4, 700
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 21)
+    hist = train.train(cfg, theta, torch.from_numpy(tok).cuda(), None, N=w["N"], eps=w["eps"], lr=w["lr"],
+                       steps=steps, seed0=seed0).numpy()
+    ref = oracle.init(cfg, 21)
+    ref_hist = []
+    for k in range(steps):
+        lp, lm = oracle.perturbed_losses(cfg, ref, seed0 + k, w["eps"], w["N"], tok)
+        ref_hist.append(0.5 * (float(lp.astype(np.float64).mean()) + float(lm.astype(np.float64).mean())))
+        assert oracle.update(cfg, ref, seed0 + k, w["eps"], w["lr"], lp, lm) == 0
+    ref_hist = np.array(ref_hist)
+    say(f"gpu {hist}\noracle {ref_hist}")
+    assert np.all(np.abs(hist - ref_hist) <= 1e-5 * np.abs(ref_hist))
+    got = theta.cpu().numpy()
+    tol = 1e-5 * np.abs(ref) + 1e-5 * np.abs(ref).mean()
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= tol)
+
+
+@pytest.mark.parametrize("probe", [wl.RADEMACHER, wl.GAUSSIAN], ids=["rademacher", "gaussian"])
+def test_training_lowers_the_loss(zo, probe):
+    """300 steps on one fixed batch (1 layer, V=64, E=32, H=64, fp32; B=8,
+    C=32; N=64, eps=1e-2, lr=0.3): the loss estimate falls by more than 0.1
+    nats (measured: 4.170 -> 4.034) and the curve trends down."""
+    from paper_2505_17852_amd import train
+    cfg = dict(n_layers=1, vocab=64, embed=32, hidden=64, wdtype=wl.FP32, probe=probe)
+    tok = wl.uniform_tokens(np.random.default_rng(5), 8, 32, 64)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 11)
+    hist = train.train(cfg, theta, torch.from_numpy(tok).cuda(), None, N=64, eps=1e-2, lr=0.3,
+                       steps=300, seed0=100).numpy()
+    say(f"loss: first {hist[:3]}, last {hist[-3:]}")
+    assert np.all(np.isfinite(hist))
+    first, last = hist[:20].mean(), hist[-20:].mean()
+    assert last < first - 0.1
+    # mostly downhill: the mean of each successive 50-step window decreases
+    win = hist.reshape(6, 50).mean(axis=1)
+    assert np.all(np.diff(win) < 0)
