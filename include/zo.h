@@ -62,7 +62,7 @@ typedef enum {
     ZO_EINVAL = -1,     /* a null pointer, a non-positive size, eps <= 0, a non-finite lr ... */
     ZO_ESHAPE = -2,     /* a model shape the kernels do not support (see zo_config) */
     ZO_EDEVICE = -3,    /* a HIP runtime error, or no gfx950 device */
-    ZO_ENOMEM = -4,     /* the workspace is smaller than zo_workspace_bytes() */
+    ZO_ENOMEM = -4,     /* the workspace is smaller than zo_workspace_bytes_min() */
     ZO_ENONFINITE = -5  /* reserved: a non-finite loss (zo_update reports it through skipped_out) */
 } zo_status;
 
@@ -87,10 +87,20 @@ typedef struct {
  * configuration is invalid. Host only. */
 size_t zo_param_count(const zo_config* cfg);
 
-/* Bytes of device workspace zo_perturbed_losses needs for N probes and a
+/* Bytes of device workspace zo_perturbed_losses uses for N probes and a
  * batch of B sequences of C positions; 0 if the arguments are invalid.
- * Host only. */
+ * Host only. With normal probes this includes the probe cache: N * P_g
+ * values of eps z (fp32 weights) or bf16(eps z) (bf16 weights) for the
+ * weight matrices (every W_ih, W_hh and W_out; P_g their total size), written
+ * once per call and read by every timestep instead of regenerating the probe
+ * in every tile (the results are bit-identical either way). With sign probes
+ * it equals zo_workspace_bytes_min. */
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
+
+/* The smallest workspace zo_perturbed_losses accepts: without the probe
+ * cache (normal probes are then regenerated in every tile). A workspace of
+ * at least zo_workspace_bytes() enables the cache. Host only. */
+size_t zo_workspace_bytes_min(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
 
 /* Initialisation: every parameter ~ U(-1/sqrt(H), 1/sqrt(H)), drawn from
  * Philox tag 2, block j>>2, word j&3 (m = word>>8, value (2m+1-2^24) 2^-24
@@ -115,7 +125,9 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
  *   Lplus, Lminus  device fp32 [N]: the masked mean over (b, t) of the
  *            next-token cross-entropy in nats at theta + eps z and at
  *            theta - eps z (0 when the mask selects nothing)
- *   workspace, ws_bytes  device scratch of at least zo_workspace_bytes()
+ *   workspace, ws_bytes  device scratch of at least zo_workspace_bytes_min()
+ *            (normal probes: at least zo_workspace_bytes() to use the probe
+ *            cache; same results, fewer probe regenerations)
  * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_ENOMEM or ZO_EDEVICE.
  * fp32 weights: each matrix product uses the perturbed weight tile
  * w +- eps z formed in LDS (one fp32 rounding); with the environment variable
@@ -159,7 +171,7 @@ int zo_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out, vo
  * zo_profile_enable(0) stops recording. zo_profile_read() waits for the
  * recorded events and returns, for one class, the summed kernel time in
  * milliseconds and the number of launches since the last enable. */
-enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4 };
+enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4, ZO_K_PROBE_CACHE = 5 };
 int zo_profile_enable(int32_t on);
 int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches);
 

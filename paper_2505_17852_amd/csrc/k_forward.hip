@@ -130,6 +130,7 @@ struct Seg {
   int64_t ldw;
   uint64_t zoff;   // offset of W inside theta (probe coordinates)
   int K;
+  const float* Z;  // kGaussCached: eps z of this probe and matrix, laid out like W
 };
 
 struct Smem {
@@ -183,6 +184,14 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
       word >>= 16 * half;
 #pragma unroll
       for (int e = 0; e < 16; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
+    } else if constexpr (kind == kGaussCached) {
+      const float* zp = sg.Z + (int64_t)wn * sg.ldw + k0 + 16 * half;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f4 v = wok ? *(const f4*)(zp + 4 * q) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) zv[4 * q + e] = v[e];
+      }
     } else {
       const uint64_t j0 = jrow + 16 * half;
 #pragma unroll
@@ -287,6 +296,9 @@ struct GateArgs {
   uint32_t i0;
   float eps;
   RowMap rm;
+  const float* zc_ih;  // probe cache: W_ih's and W_hh's values of probe 0; probe n at + n * zc_stride
+  const float* zc_hh;
+  uint64_t zc_stride;
 };
 
 template <int kind, bool kSplit>
@@ -313,8 +325,11 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
     for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
 
   const uint32_t probe = g.i0 + (uint32_t)pair;
-  const Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
-  const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
+  const uint64_t zpos = (uint64_t)pair * g.zc_stride;
+  const Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El,
+               kind == kGaussCached ? g.zc_ih + zpos : nullptr};
+  const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
+               kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   mainloop_f32<kind, kSplit>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
 
   // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
@@ -370,6 +385,8 @@ struct HeadArgs {
   float* pmax;  // [nvt][rows]
   float* psum;
   float* ptgt;  // [rows]
+  const float* zc_out;  // probe cache: W_out's values of probe 0; probe n at + n * zc_stride
+  uint64_t zc_stride;
 };
 
 template <int kind, bool kSplit>
@@ -401,7 +418,8 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[mt][q] = f4{0.f, 0.f, 0.f, 0.f};
   const uint32_t probe = g.i0 + (uint32_t)pair;
-  const Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
+  const Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
+               kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   mainloop_f32<kind, kSplit>(acc, s0, s0, 1, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
 
   const float* bout = g.theta + g.off_b;
@@ -536,9 +554,76 @@ __global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int
   }
 }
 
+// Probe cache fill: eps z (fp32 weights) or bf16(eps z) (bf16 weights) of
+// every weight matrix for probes i0 .. i0+N-1 (layout: ZCacheMap). The values
+// are the ones the forward kernels compute when they regenerate the probe:
+// fp32(eps * z) and bf16_rne(eps * z) of the same normal value z. One thread
+// per Philox block (4 values); the matrices are listed by their start in a
+// probe's block and in theta.
+struct ZSegs {
+  int n;
+  uint64_t cstart[2 * kMaxLayers + 2];  // start of matrix m in a probe's block; cstart[n] = P_g
+  uint64_t toff[2 * kMaxLayers + 1];    // offset of matrix m in theta
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void zcache_fill_kernel(T* zc, ZSegs segs, Key key, uint32_t i0, int N,
+                                                          float eps) {
+  const uint64_t pg = segs.cstart[segs.n];
+  const uint64_t nb = pg >> 2;
+  for (int n = blockIdx.y; n < N; n += gridDim.y) {
+    T* zp = zc + (uint64_t)n * pg;
+    for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb;
+         b += (uint64_t)gridDim.x * blockDim.x) {
+      const uint64_t u = b << 2;
+      int m = 0;
+      while (m + 1 < segs.n && u >= segs.cstart[m + 1]) ++m;
+      const uint64_t j = segs.toff[m] + (u - segs.cstart[m]);
+      float z[4];
+      gauss_block(key, i0 + (uint32_t)n, j >> 2, z);
+      if constexpr (sizeof(T) == 2) {
+        const uint32_t lo = (uint32_t)bf16_rne(eps * z[0]) | ((uint32_t)bf16_rne(eps * z[1]) << 16);
+        const uint32_t hi = (uint32_t)bf16_rne(eps * z[2]) | ((uint32_t)bf16_rne(eps * z[3]) << 16);
+        *(uint2*)(zp + u) = uint2{lo, hi};
+      } else {
+        *(f4*)(zp + u) = f4{fmul(eps, z[0]), fmul(eps, z[1]), fmul(eps, z[2]), fmul(eps, z[3])};
+      }
+    }
+  }
+}
+
 }  // namespace
 
 namespace {
+
+hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
+  const zo_config& c = a.cfg;
+  ZSegs segs{};
+  int m = 0;
+  for (int l = 0; l < c.n_layers; ++l) {
+    segs.cstart[m] = a.zmap.ih[l];
+    segs.toff[m++] = a.lay.w_ih[l];
+    segs.cstart[m] = a.zmap.hh[l];
+    segs.toff[m++] = a.lay.w_hh[l];
+  }
+  segs.cstart[m] = a.zmap.out;
+  segs.toff[m++] = a.lay.w_out;
+  segs.n = m;
+  segs.cstart[m] = a.zmap.pg;
+  const uint64_t nb = a.zmap.pg / 4;
+  uint64_t gx = (nb + 255) / 256;
+  if (gx > 4096) gx = 4096;
+  const unsigned gy = (unsigned)(a.rows.N < 65535 ? a.rows.N : 65535);
+  const Key key = make_key(a.seed);
+  ProfScope ps(kKProbeCache, st);
+  if (c.wdtype == ZO_WBF16)
+    zcache_fill_kernel<uint16_t><<<dim3((unsigned)gx, gy), 256, 0, st>>>((uint16_t*)a.zc, segs, key, a.i0,
+                                                                         a.rows.N, a.eps);
+  else
+    zcache_fill_kernel<float><<<dim3((unsigned)gx, gy), 256, 0, st>>>((float*)a.zc, segs, key, a.i0,
+                                                                      a.rows.N, a.eps);
+  return hipGetLastError();
+}
 
 hipError_t launch_embed_f32(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
   const Rows& R = a.rows;
@@ -578,12 +663,18 @@ hipError_t launch_gate_f32(const ForwardArgs& a, int l, const void* x, const voi
   g.i0 = a.i0;
   g.eps = a.eps;
   g.rm = RowMap{R.Bp, R.pair_rows};
+  g.zc_ih = a.zc ? (const float*)a.zc + a.zmap.ih[l] : nullptr;
+  g.zc_hh = a.zc ? (const float*)a.zc + a.zmap.hh[l] : nullptr;
+  g.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / BM));
   const bool split = a.fp32_split;
   ProfScope ps(kKGate, st);
   if (a.cfg.probe == ZO_RADEMACHER) {
     if (split) gate_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(g);
     else gate_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(g);
+  } else if (a.zc) {
+    if (split) gate_f32_kernel<kGaussCached, true><<<grid, 256, 0, st>>>(g);
+    else gate_f32_kernel<kGaussCached, false><<<grid, 256, 0, st>>>(g);
   } else {
     if (split) gate_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(g);
     else gate_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(g);
@@ -615,12 +706,17 @@ hipError_t launch_head_f32(const ForwardArgs& a, const void* hist, int t0, int T
   h.pmax = pmax;
   h.psum = psum;
   h.ptgt = ptgt;
+  h.zc_out = a.zc ? (const float*)a.zc + a.zmap.out : nullptr;
+  h.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)a.ws.nvt, (unsigned)(h.rows / BM));
   const bool split = a.fp32_split;
   ProfScope ps(kKHead, st);
   if (a.cfg.probe == ZO_RADEMACHER) {
     if (split) head_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(h);
     else head_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(h);
+  } else if (a.zc) {
+    if (split) head_f32_kernel<kGaussCached, true><<<grid, 256, 0, st>>>(h);
+    else head_f32_kernel<kGaussCached, false><<<grid, 256, 0, st>>>(h);
   } else {
     if (split) head_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(h);
     else head_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(h);
@@ -669,6 +765,9 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   ZO_TRY(hipMemsetAsync(hist, 0, (size_t)W.T * state, st));
   ZO_TRY(hipMemsetAsync(cbuf, 0, (size_t)L * M * H * 4, st));
   ZO_TRY(hipMemsetAsync(row_loss, 0, (size_t)M * 8, st));
+
+  // probe cache (normal probes, when the workspace holds it)
+  if (a.zc) ZO_TRY(launch_zcache_fill(a, st));
 
   // bias probes
   {

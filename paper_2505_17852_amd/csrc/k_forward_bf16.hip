@@ -65,7 +65,9 @@ struct Tiles {
   static constexpr int WBytes = TN * kRowBytes;
   static constexpr int ZBytes = kind == ZO_RADEMACHER ? TN * 8 : TN * kRowBytes;
   static constexpr int WCopies = WBytes / 1024 / kCopyWaves;  // weight copies per copying wave
-  static constexpr int Copies = kACopies + WCopies;
+  // cached normal probes: the probe tile is copied like the weight tile
+  static constexpr int ZCopies = kind == kGaussCached ? WCopies : 0;
+  static constexpr int Copies = kACopies + WCopies + ZCopies;
   static constexpr int ZROW_T = NT / TN;     // threads per probe-tile row (normal probes)
   static constexpr int ZVALS = TK / ZROW_T;  // probe values per thread and K tile (normal probes)
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
@@ -152,6 +154,7 @@ struct SegB {
   int64_t ldw;
   uint64_t zoff;      // offset of W inside theta (probe coordinates)
   int K;
+  const uint16_t* Z;  // kGaussCached: bf16(eps z) of this probe and matrix, laid out like W
 };
 
 // acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave.
@@ -212,11 +215,17 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     if (wave < kCopyWaves) {
 #pragma unroll
       for (int c = P * T::Copies / kCopySteps; c < (P < kCopySteps ? (P + 1) * T::Copies / kCopySteps : 0); ++c) {
-        if (c < kACopies)
+        if (c < kACopies) {
           copy_to_lds(sg.A + (int64_t)arow[c] * sg.lda + k0 + aoff[c], base + (c * kCopyWaves + wave) * 1024);
-        else
-          copy_to_lds(sg.W + (int64_t)wrow[c - kACopies] * sg.ldw + k0 + woff[c - kACopies],
-                      base + kABytes + ((c - kACopies) * kCopyWaves + wave) * 1024);
+        } else if (c < kACopies + T::WCopies) {
+          const int q = c - kACopies;
+          copy_to_lds(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
+                      base + kABytes + (q * kCopyWaves + wave) * 1024);
+        } else {  // cached probe rows: the same rows and chunk order as the weight copy q
+          const int q = c - kACopies - T::WCopies;
+          copy_to_lds(sg.Z + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
+                      base + kABytes + T::WBytes + (q * kCopyWaves + wave) * 1024);
+        }
       }
     }
     if constexpr (P == 2 && kind == ZO_RADEMACHER) {
@@ -232,7 +241,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       }
       // negative-sign flags in unshuffled order
       sign_bits<S>()[zr * 2 + zpart] = unshuffle_bits(~word);
-    } else if constexpr (P == 2) {
+    } else if constexpr (P == 2 && kind == ZO_GAUSSIAN) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
       uint8_t* zrow = base + kABytes + T::WBytes + zr * kRowBytes;
 #pragma unroll
@@ -421,6 +430,9 @@ struct GateArgsB {
   uint16_t eps_b;
   RowMap rm;
   int n_row_blocks;  // M / TM
+  const uint16_t* zc_ih;  // probe cache: W_ih's and W_hh's values of probe 0; probe n at + n * zc_stride
+  const uint16_t* zc_hh;
+  uint64_t zc_stride;
 };
 
 // Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
@@ -446,8 +458,11 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   };
   f16v acc[T::MT][2];
   zero_acc(acc);
-  const SegB s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El};
-  const SegB s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H};
+  const uint64_t zpos = (uint64_t)pair * g.zc_stride;
+  const SegB s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El,
+                kind == kGaussCached ? g.zc_ih + zpos : nullptr};
+  const SegB s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
+                kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   mainloop_bf16<kind>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
 
   const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
@@ -503,6 +518,8 @@ struct HeadArgsB {
   float* psum;
   float* ptgt;
   int nvt;  // vocabulary tiles
+  const uint16_t* zc_out;  // probe cache: W_out's values of probe 0; probe n at + n * zc_stride
+  uint64_t zc_stride;
 };
 
 template <int kind>
@@ -523,7 +540,8 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
   f16v acc[T::MT][2];
   zero_acc(acc);
-  const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H};
+  const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
+                kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   mainloop_bf16<kind>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
 
   int col[2];
@@ -671,10 +689,17 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.eps_b = bf16_rne(a.eps);
   g.rm = RowMap{R.Bp, R.pair_rows};
   g.n_row_blocks = (int)(R.M / TM);
+  g.zc_ih = a.zc ? (const uint16_t*)a.zc + a.zmap.ih[l] : nullptr;
+  g.zc_hh = a.zc ? (const uint16_t*)a.zc + a.zmap.hh[l] : nullptr;
+  g.zc_stride = a.zmap.pg;
   if (a.cfg.probe == ZO_RADEMACHER) {
     const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_RADEMACHER>::TN / 4))));
     ProfScope ps(kKGate, st);
     gate_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(g);
+  } else if (a.zc) {
+    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<kGaussCached>::TN / 4))));
+    ProfScope ps(kKGate, st);
+    gate_bf16_kernel<kGaussCached><<<grid, NT, 0, st>>>(g);
   } else {
     const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_GAUSSIAN>::TN / 4))));
     ProfScope ps(kKGate, st);
@@ -709,10 +734,15 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.psum = psum;
   h.ptgt = ptgt;
   h.nvt = a.ws.nvt;
+  h.zc_out = a.zc ? (const uint16_t*)a.zc + a.zmap.out : nullptr;
+  h.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)((int64_t)a.ws.nvt * (h.rows / TM)));
   if (a.cfg.probe == ZO_RADEMACHER) {
     ProfScope ps(kKHead, st);
     head_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(h);
+  } else if (a.zc) {
+    ProfScope ps(kKHead, st);
+    head_bf16_kernel<kGaussCached><<<grid, NT, 0, st>>>(h);
   } else {
     ProfScope ps(kKHead, st);
     head_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(h);

@@ -63,6 +63,12 @@ size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C)
   return zo::plan_workspace(*cfg, r, C).total;
 }
 
+size_t zo_workspace_bytes_min(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
+  if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1) return 0;
+  const zo::Rows r = zo::make_rows(N, B, zo::row_granule(*cfg));
+  return zo::plan_workspace(*cfg, r, C).min_total;
+}
+
 int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
   int st = check_config(cfg);
   if (st) return st;
@@ -94,8 +100,8 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   const zo::Rows rows = zo::make_rows(N, B, zo::row_granule(*cfg));
   if (rows.M > (int64_t)1 << 30) return fail(ZO_ESHAPE, "2N*B rows too large");
   const zo::WsPlan plan = zo::plan_workspace(*cfg, rows, C);
-  if (ws_bytes < plan.total)
-    return fail(ZO_ENOMEM, "workspace of %zu bytes < %zu required", ws_bytes, plan.total);
+  if (ws_bytes < plan.min_total)
+    return fail(ZO_ENOMEM, "workspace of %zu bytes < %zu required", ws_bytes, plan.min_total);
   zo::ForwardArgs a;
   a.cfg = *cfg;
   a.lay = zo::make_layout(*cfg);
@@ -113,6 +119,9 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   a.work = (char*)workspace;
   const char* split = std::getenv("ZO_FP32_SPLIT");
   a.fp32_split = split && split[0] == '1';
+  // the probe cache is used when the workspace has room for it
+  a.zc = (zo::probe_cache_kind(*cfg) && ws_bytes >= plan.total) ? (char*)workspace + plan.zcache : nullptr;
+  a.zmap = zo::make_zcache_map(*cfg);
   return device_status(zo::launch_forward(a, (hipStream_t)stream), "zo_perturbed_losses");
 }
 

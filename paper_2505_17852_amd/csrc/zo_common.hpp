@@ -100,6 +100,44 @@ inline int vocab_tile(const zo_config& c) {
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Probe cache (normal probes only): the 2N forward passes read the probe
+// terms of every weight matrix (W_ih, W_hh of each layer and W_out) at every
+// timestep and row tile, while each value is the same for the whole call.
+// With a large enough workspace the call first writes, once, the values the
+// kernels would otherwise regenerate: eps z in fp32 (fp32 weights) or
+// bf16(eps z) (bf16 weights), for probes i0 .. i0+N-1. Layout: probe n's
+// block of P_g values (the matrices in theta order, each row-major like the
+// matrix itself) at n * P_g. Sign probes are cheap to regenerate and are
+// never cached.
+struct ZCacheMap {
+  uint64_t pg;              // values per probe: the matrices' total size
+  uint64_t ih[kMaxLayers];  // offsets of each matrix inside a probe's block
+  uint64_t hh[kMaxLayers];
+  uint64_t out;
+};
+
+inline ZCacheMap make_zcache_map(const zo_config& c) {
+  ZCacheMap m{};
+  const uint64_t E = (uint64_t)c.embed, H = (uint64_t)c.hidden, V = (uint64_t)c.vocab;
+  uint64_t p = 0;
+  for (int l = 0; l < c.n_layers; ++l) {
+    m.ih[l] = p;
+    p += 4 * H * (l == 0 ? E : H);
+    m.hh[l] = p;
+    p += 4 * H * H;
+  }
+  m.out = p;
+  p += V * H;
+  m.pg = p;
+  return m;
+}
+
+inline bool probe_cache_kind(const zo_config& c) { return c.probe == ZO_GAUSSIAN; }
+
+// Kernel variant for normal probes read from the probe cache (next to the
+// probe kinds ZO_RADEMACHER and ZO_GAUSSIAN, which regenerate them).
+constexpr int kGaussCached = 2;
+
 // Workspace plan (byte offsets from the workspace base, 256-aligned).
 struct WsPlan {
   size_t x0;         // f32 [M][E]         perturbed embeddings of one timestep
@@ -112,7 +150,9 @@ struct WsPlan {
   size_t psum;       // f32 [nvt][T*M]     per vocabulary tile: sum of exp(y - max)
   size_t ptgt;       // f32 [T*M]          target logit
   size_t row_loss;   // f64 [M]            masked loss sum of each row
-  size_t total;
+  size_t min_total;  // bytes without the probe cache
+  size_t zcache;     // probe cache [N][P_g] (normal probes; see ZCacheMap)
+  size_t total;      // bytes with the probe cache (= min_total for sign probes)
   int nvt;           // vocabulary tiles
   int T;             // time chunk
 };
@@ -141,6 +181,9 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
   w.psum = take((size_t)w.nvt * w.T * M * 4);
   w.ptgt = take((size_t)w.T * M * 4);
   w.row_loss = take(M * 8);
+  w.min_total = p;
+  w.zcache = p;
+  if (probe_cache_kind(c)) take((size_t)r.N * make_zcache_map(c).pg * (c.wdtype == ZO_WBF16 ? 2 : 4));
   w.total = p;
   return w;
 }

@@ -36,6 +36,8 @@ struct ForwardArgs {
   float* Lminus;
   char* work;
   bool fp32_split;  // fp32 path: separate W.h and probe MFMA streams (measurement variant)
+  void* zc;         // probe cache inside work, or nullptr (probes regenerated in every tile)
+  ZCacheMap zmap;
 };
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);
 

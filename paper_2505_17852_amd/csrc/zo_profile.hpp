@@ -9,7 +9,8 @@
 
 namespace zo {
 
-enum KernelClass { kKGate = 0, kKHead = 1, kKEmbed = 2, kKCombine = 3, kKUpdate = 4, kKClasses = 5 };
+enum KernelClass { kKGate = 0, kKHead = 1, kKEmbed = 2, kKCombine = 3, kKUpdate = 4, kKProbeCache = 5,
+                   kKClasses = 6 };
 
 extern std::atomic<int> g_profile_on;
 

@@ -6,8 +6,8 @@ kernels. PyTorch supplies device memory (torch.cuda tensors) and the stream
 built (paper_2505_17852_amd/build.py); there is no fallback of any kind.
 
 Function names follow the C ABI in include/zo.h:
-    param_count, workspace_bytes, init, perturbed_losses, update,
-    debug_probe, debug_gauss_pairs
+    param_count, workspace_bytes, workspace_bytes_min, init, perturbed_losses,
+    update, debug_probe, debug_gauss_pairs
 A model configuration is a dict with the keys n_layers, vocab, embed,
 hidden, wdtype (0 fp32, 1 bf16) and probe (0 Rademacher, 1 normal).
 """
@@ -53,6 +53,8 @@ def lib():
         L.zo_param_count.restype = C.c_size_t
         L.zo_workspace_bytes.argtypes = [cfgp, C.c_int32, C.c_int32, C.c_int32]
         L.zo_workspace_bytes.restype = C.c_size_t
+        L.zo_workspace_bytes_min.argtypes = [cfgp, C.c_int32, C.c_int32, C.c_int32]
+        L.zo_workspace_bytes_min.restype = C.c_size_t
         L.zo_init.argtypes = [cfgp, vp, C.c_uint64, vp]
         L.zo_perturbed_losses.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
                                           vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, vp]
@@ -121,8 +123,15 @@ def init(cfg, theta: torch.Tensor, seed: int, stream=None):
     _check(lib().zo_init(C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, _stream(stream)))
 
 
-def new_workspace(cfg, N: int, B: int, C_: int, device="cuda") -> torch.Tensor:
-    n = workspace_bytes(cfg, N, B, C_)
+def workspace_bytes_min(cfg, N: int, B: int, C_: int) -> int:
+    c = _cfg(cfg)
+    return int(lib().zo_workspace_bytes_min(C.byref(c), N, B, C_))
+
+
+def new_workspace(cfg, N: int, B: int, C_: int, device="cuda", probe_cache: bool = True) -> torch.Tensor:
+    """Device workspace for zo_perturbed_losses; probe_cache=False gives the
+    smallest one (normal probes then regenerated in every tile)."""
+    n = workspace_bytes(cfg, N, B, C_) if probe_cache else workspace_bytes_min(cfg, N, B, C_)
     if n == 0:
         raise ValueError("invalid workspace request")
     return torch.empty(n, dtype=torch.uint8, device=device)
@@ -198,9 +207,9 @@ def debug_gauss_pairs(words: torch.Tensor, stream=None) -> torch.Tensor:
     return out
 
 
-K_GATE, K_HEAD, K_EMBED, K_COMBINE, K_UPDATE = 0, 1, 2, 3, 4
+K_GATE, K_HEAD, K_EMBED, K_COMBINE, K_UPDATE, K_PROBE_CACHE = 0, 1, 2, 3, 4, 5
 KERNEL_CLASSES = {"gate": K_GATE, "head": K_HEAD, "embed": K_EMBED, "combine": K_COMBINE,
-                  "update": K_UPDATE}
+                  "update": K_UPDATE, "probe_cache": K_PROBE_CACHE}
 
 
 def profile_enable(on: bool = True):

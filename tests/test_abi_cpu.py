@@ -65,6 +65,25 @@ def test_workspace_bytes(zo):
     assert zo.workspace_bytes(cfg, 0, 64, 256) == 0
     bad = dict(cfg, n_layers=0)
     assert zo.workspace_bytes(bad, 4, 4, 4) == 0
+    assert zo.workspace_bytes_min(bad, 4, 4, 4) == 0
+
+
+@pytest.mark.parametrize("name", wl.CONFIG_ORDER)
+def test_workspace_probe_cache_size(zo, name):
+    """Normal probes: the preferred workspace adds exactly the probe cache,
+    N values of the weight matrices' size in the weight type (rounded up to
+    the 256-byte allocation granule); sign probes cache nothing."""
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    full = zo.workspace_bytes(cfg, w["N"], w["B"], w["C"])
+    small = zo.workspace_bytes_min(cfg, w["N"], w["B"], w["C"])
+    if cfg["probe"] == wl.GAUSSIAN:
+        L, E, H, V = cfg["n_layers"], cfg["embed"], cfg["hidden"], cfg["vocab"]
+        pg = sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + V * H
+        el = 2 if cfg["wdtype"] == wl.BF16 else 4
+        assert full - small == (w["N"] * pg * el + 255) // 256 * 256
+    else:
+        assert full == small
 
 
 def _call_losses(zo, cfg, eps=1e-3, N=2, B=2, Cn=4, ptrs=True):

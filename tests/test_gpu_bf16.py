@@ -99,12 +99,13 @@ def test_bf16_slice_and_determinism(zo):
     assert torch.equal(sp, Lp[3:5]) and torch.equal(sm, Lm[3:5])
 
 
-def test_c4_full_size_sampled(zo, oracle):
-    """c4 at its full launch configuration (N=16, B=256, C=1024) with a mask
-    that scores only the first positions of two sequences; causality makes
-    those losses computable by the oracle on the 2-sequence, 3-position
-    prefix. Probes 0 and 15 (first and last row block) are checked."""
-    name = "c4"
+@pytest.mark.parametrize("name", ["c4", "c3"])
+def test_full_size_sampled(zo, oracle, name):
+    """The workload at its full launch configuration (c4: N=16, c3: N=64 with
+    the probe cache; B=256, C=1024) with a mask that scores only the first
+    positions of two sequences; causality makes those losses computable by
+    the oracle on the 2-sequence, 3-position prefix. The first and last
+    probes (first and last row blocks) are checked."""
     w = wl.CONFIGS[name]
     cfg = wl.model_cfg(name)
     sd = wl.seeds(name)
@@ -113,7 +114,7 @@ def test_c4_full_size_sampled(zo, oracle):
     mask = np.zeros((B, C), np.uint8)
     mask[0, :3] = 1
     mask[1, :2] = 1
-    say(f"c4 full size N={w['N']} B={B} C={C}, sampled positions")
+    say(f"{name} full size N={w['N']} B={B} C={C}, sampled positions")
     theta = zo.new_theta(cfg)
     zo.init(cfg, theta, sd["init"])
     td = torch.from_numpy(tok).cuda()

@@ -278,3 +278,55 @@ def test_delta_loss_matches_oracle(zo, oracle, name, B, C):
     assert np.all(np.abs(dr) > 0)
     tol = 8 * 2.0 ** -24 * np.abs(rp) + 1e-4 * np.abs(dr)
     assert np.all(np.abs(dg - dr) <= tol)
+
+
+@pytest.mark.parametrize("cfg", [
+    dict(n_layers=2, vocab=200, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.GAUSSIAN),
+    dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.GAUSSIAN),
+], ids=["fp32", "bf16"])
+def test_probe_cache_is_bit_identical(zo, cfg):
+    """Normal probes: the losses with the probe cache (default workspace) and
+    without it (the smallest workspace: probes regenerated in every tile) are
+    bit-identical, for a slice i0 > 0 and a ragged batch."""
+    N, B, C = 3, 5, 13
+    say(f"probe cache {cfg} N={N} B={B} C={C}")
+    rng = np.random.default_rng(23)
+    tok = torch.from_numpy(wl.uniform_tokens(rng, B, C, cfg["vocab"])).cuda()
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 4)
+    assert zo.workspace_bytes(cfg, N, B, C) > zo.workspace_bytes_min(cfg, N, B, C)
+    ws_full = zo.new_workspace(cfg, N, B, C)
+    ws_min = zo.new_workspace(cfg, N, B, C, probe_cache=False)
+    a = zo.perturbed_losses(cfg, theta, 77, 1e-2, N, tok, i0=5, workspace=ws_full)
+    b = zo.perturbed_losses(cfg, theta, 77, 1e-2, N, tok, i0=5, workspace=ws_min)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_c5_full_size_sampled(zo, oracle):
+    """c5 at its full launch configuration (N=1024 normal probes with the
+    probe cache, B=32, C=128), scoring only the first positions of two
+    sequences so that the oracle can compute the losses on the 2-sequence,
+    3-position prefix; probes 0, 511 and 1023 are checked at the fp32 bar."""
+    name = "c5"
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tok, _ = wl.batch(name)
+    B, C = tok.shape[0], tok.shape[1] - 1
+    mask = np.zeros((B, C), np.uint8)
+    mask[0, :3] = 1
+    mask[1, :2] = 1
+    say(f"{name} full size N={w['N']} B={B} C={C}, sampled positions")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    td, md = dev_tokens(tok, mask)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, sd["step"], w["eps"], w["N"], td, md)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    ref_theta = oracle.init(cfg, sd["init"])
+    ref_tok = np.ascontiguousarray(tok[:2, :4])
+    ref_mask = np.ascontiguousarray(mask[:2, :3])
+    for i in (0, 511, w["N"] - 1):
+        rp, rm = oracle.perturbed_losses(cfg, ref_theta, sd["step"], w["eps"], 1, ref_tok, ref_mask, i0=i)
+        say(f"probe {i}: gpu {gp[i]} {gm[i]} oracle {rp[0]} {rm[0]}")
+        assert abs(gp[i] - rp[0]) <= LOSS_RTOL * abs(rp[0])
+        assert abs(gm[i] - rm[0]) <= LOSS_RTOL * abs(rm[0])
