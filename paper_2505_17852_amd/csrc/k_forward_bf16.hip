@@ -161,7 +161,12 @@ struct SegB {
 // colmap(rho, &n) maps LDS column rho (0..TN-1) to a weight row n inside the
 // matrix (columns beyond the matrix map to a valid row; they are never
 // scored). neg: this wave's rows are the -eps pass; eps_b: bf16 bits of eps.
-template <int kind, typename ColMap>
+// kTrans: accumulate the transposed product (weight columns on the rows of
+// each 32x32 tile, activation rows on its columns): both operands of
+// v_mfma_f32_32x32x16_bf16 have the same fragment layout, so only their order
+// changes. Lane (lr, lg) then holds, for activation row lr of a tile, the 16
+// columns 8 (v >> 2) + 4 lg + (v & 3), v < 16.
+template <int kind, bool kTrans = false, typename ColMap>
 __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
                                               int nseg, ColMap colmap, Key key, uint32_t probe, bool neg,
                                               float eps, uint16_t eps_b) {
@@ -334,12 +339,14 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], acc[mt][nt], 0, 0, 0);
+          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.w[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
+                               : __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], acc[mt][nt], 0, 0, 0);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
+          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.z[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
+                               : __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
       if (more) {
         constexpr std::integral_constant<int, 1 - S> next{};
         if (s == 0) issue(next, std::integral_constant<int, 0>{});
@@ -542,55 +549,66 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   zero_acc(acc);
   const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
-  mainloop_bf16<kind>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
+  mainloop_bf16<kind, true>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
 
-  int col[2];
-  bool cok[2];
-  float bias[2];
+  // transposed tiles: acc[mt][nt][v] is the logit of activation row
+  // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
+  const int cbase = v0 + 64 * wn;
+  auto vcol = [&](int v) { return 8 * (v >> 2) + 4 * lg + (v & 3); };
+  // bias and bias probe of each column held (-inf past the vocabulary)
+  float add[2][16];
 #pragma unroll
   for (int nt = 0; nt < 2; ++nt) {
-    col[nt] = v0 + 64 * wn + 32 * nt + lr;
-    cok[nt] = col[nt] < V;
-    const float b = cok[nt] ? bf16_to_f32(g.theta[g.off_b + (uint64_t)col[nt]]) : 0.f;
-    const float z = cok[nt] ? g.zbo[(int64_t)pair * V + col[nt]] : 0.f;
-    bias[nt] = neg ? b - z : b + z;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int col = cbase + 32 * nt + vcol(v);
+      float a = -INFINITY;
+      if (col < V) {
+        const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)col]);
+        const float z = g.zbo[(int64_t)pair * V + col];
+        a = neg ? b - z : b + z;
+      }
+      add[nt][v] = a;
+    }
   }
   // cross-wave reduction in the first stage buffer (free after the loop)
   float* red_m = (float*)stage<kind, 0>();         // [WAVES_N][TM]
   float* red_s = red_m + T::WAVES_N * TM;          // [WAVES_N][TM]
 #pragma unroll
   for (int mt = 0; mt < T::MT; ++mt) {
+    const int lrow = T::WROWS * wm + 32 * mt + lr;
+    const int64_t r = r0 + lrow;
+    const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
+    const int b = neg ? loc - g.rm.Bp : loc;
+    const int tgt = b < g.B ? g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1] - cbase : -1;
+    float mx = -INFINITY, yt = 0.f;
+    bool has_t = false;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int lrow = acc_row<kind>(wm, mt, lg, v);
-      const int64_t r = r0 + lrow;
-      const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
-      const int b = neg ? loc - g.rm.Bp : loc;
-      float y[2];
-      float mx = -INFINITY;
+    for (int nt = 0; nt < 2; ++nt) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        y[nt] = cok[nt] ? acc[mt][nt][v] + bias[nt] : -INFINITY;
-        mx = fmaxf(mx, y[nt]);
+      for (int v = 0; v < 16; ++v) {
+        const float y = acc[mt][nt][v] + add[nt][v];
+        acc[mt][nt][v] = y;
+        mx = fmaxf(mx, y);
+        const bool hit = tgt == 32 * nt + vcol(v);
+        yt = hit ? y : yt;
+        has_t = has_t || hit;
       }
-      if (b < g.B) {
-        const int tgt = g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1];
+    }
+    if (has_t) g.ptgt[rr0 + lrow] = yt;
+    // the row's 64 columns of this wave: 32 here, 32 in lane lr + 32
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float se = 0.f;
+    if (mx != -INFINITY) {
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          if (col[nt] == tgt) g.ptgt[rr0 + lrow] = y[nt];
-      }
-      // the row's 64 columns of this wave sit in the 32 lanes of this lane half
+      for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-      for (int off = 1; off < 32; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-      float se = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) se += cok[nt] ? __expf(y[nt] - mx) : 0.f;
-#pragma unroll
-      for (int off = 1; off < 32; off <<= 1) se += __shfl_xor(se, off, 64);
-      if (lr == 0) {
-        red_m[wn * TM + lrow] = mx;
-        red_s[wn * TM + lrow] = se;
-      }
+        for (int v = 0; v < 16; ++v) se += __expf(acc[mt][nt][v] - mx);
+    }
+    se += __shfl_xor(se, 32, 64);
+    if (lg == 0) {
+      red_m[wn * TM + lrow] = mx;
+      red_s[wn * TM + lrow] = se;
     }
   }
   __syncthreads();
