@@ -85,6 +85,22 @@ def update_hbm(P, w, upd):
             "frac": gbps / HBM_PEAK_GBPS}
 
 
+def embed_hbm(cfg, N, B, w, emb):
+    """Algorithmic HBM rate of the perturbed-embedding kernel: per launch it
+    writes the 2N*B rows of E activations (w bytes each; padding rows
+    included, as written) and reads B rows of EMB."""
+    ms, n = emb
+    if n == 0 or ms <= 0:
+        return None
+    from paper_2505_17852_amd import workloads as wl  # noqa: F401
+    gran = 128 if w == 2 else 32
+    Bp = (B + gran - 1) // gran * gran
+    E = cfg["embed"]
+    byt = 2 * N * Bp * E * w + B * E * w
+    gbps = byt / (ms / n * 1e-3) / 1e9
+    return {"bytes_per_launch": byt, "ms_per_launch": ms / n, "GBps": gbps, "frac": gbps / HBM_PEAK_GBPS}
+
+
 def cpu_baseline(name, budget_s=20.0):
     """The oracle on the host cores, on a bounded sample of the workload:
     the full batch with the first N' probes (N' doubling until the budget is
@@ -224,6 +240,9 @@ def main():
         "step_mfma_frac_algorithmic": fwd_flops / (dt / K) / 1e12 / peak,
         # the parameter update reads and writes theta once: 2 P w bytes
         "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"]),
+        # the perturbed embedding writes 2N*B rows of E activations per timestep
+        # (and gathers B rows of EMB): algorithmic bytes over its event time
+        "embed_hbm": embed_hbm(cfg, N, B, 2 if dtype == "bf16" else 4, prof["embed"]),
         "kernels": kernels,
         "losses_finite": losses_ok,
     }

@@ -665,24 +665,65 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
   *(uint2*)(x0 + r * E + e) = uint2{lo, hi};
 }
 
+// Sign probes: one thread per 32 consecutive elements of a row, which share
+// one Philox word (bit k of the word for element k), so a row costs E / 128
+// Philox blocks instead of E / 4.
+__global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* theta, uint64_t emb_off, int E,
+                                                             const int32_t* tokens, int C, int t, int B,
+                                                             RowMap rm, int64_t M, Key key, uint32_t i0,
+                                                             float eps, uint16_t* x0) {
+  const int E32 = E >> 5;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= M * E32) return;
+  const int64_t r = idx / E32;
+  const int e = (int)(idx - r * E32) * 32;
+  const int pair = (int)(r / rm.pair_rows);
+  const int loc = (int)(r - pair * rm.pair_rows);
+  const int sidx = loc >= rm.Bp;
+  const int b = loc - sidx * rm.Bp;
+  u4 out[4] = {u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}};
+  if (b < B) {
+    const int tok = tokens[(int64_t)b * (C + 1) + t];
+    const uint64_t j = emb_off + (uint64_t)tok * E + e;  // a multiple of 32: one whole word
+    const uint32_t word = rademacher_word(key, i0 + pair, j >> 5);
+    const float se = sidx ? -eps : eps;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const u4 wv = *(const u4*)(theta + j + 8 * q);
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const int k = 8 * q + 2 * d;
+        const float w0 = bf16_to_f32((uint16_t)wv[d]), w1 = bf16_to_f32((uint16_t)(wv[d] >> 16));
+        const float z0 = ((word >> k) & 1u) ? 1.0f : -1.0f, z1 = ((word >> (k + 1)) & 1u) ? 1.0f : -1.0f;
+        out[q][d] = pack_bf16x2(w0 + se * z0, w1 + se * z1);
+      }
+    }
+  }
+  u4* dst = (u4*)(x0 + r * E + e);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) dst[q] = out[q];
+}
+
 }  // namespace
 
 hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
   const Rows& R = a.rows;
   const int E = a.cfg.embed;
   const RowMap rm{R.Bp, R.pair_rows};
-  const int64_t n = R.M * (E / 4);
-  const unsigned grid = (unsigned)((n + 255) / 256);
   const Key key = make_key(a.seed);
   ProfScope ps(kKEmbed, st);
-  if (a.cfg.probe == ZO_RADEMACHER)
-    embed_bf16_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E,
-                                                           a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
-                                                           a.eps, (uint16_t*)x0);
-  else
+  if (a.cfg.probe == ZO_RADEMACHER) {
+    const int64_t n = R.M * (E / 32);
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    embed_bf16_rad_kernel<<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E, a.tokens, a.C, t, R.B,
+                                                rm, R.M, key, a.i0, a.eps, (uint16_t*)x0);
+  } else {
+    const int64_t n = R.M * (E / 4);
+    const unsigned grid = (unsigned)((n + 255) / 256);
     embed_bf16_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E,
                                                          a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
                                                          a.eps, (uint16_t*)x0);
+  }
   return hipGetLastError();
 }
 
