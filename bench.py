@@ -9,8 +9,10 @@ time), the roofline position of the dominant kernel (the fused gate kernel,
 timed live with HIP events over the timed region) and the CPU oracle timed on
 a bounded sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
-(default workload c4, the 1.2B-parameter model; c2 is the fp32 transduction shape)
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--estimator cd]
+(default workload c4, the 1.2B-parameter model; c2 is the fp32 transduction shape;
+--estimator fd times the forward-difference step instead: N + 1 passes,
+zo_fd_losses and zo_fd_update)
 """
 import argparse
 import json
@@ -23,6 +25,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "perturbed-forward tokens/sec per CD-RGE step (2N·B·C/s); % MFMA peak"
+METRIC_FD = "forward tokens/sec per FD-RGE step ((N+1)·B·C/s); % MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
 HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
 DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 1), "c4": (1, 1), "c5": (1, 3)}
@@ -37,11 +40,12 @@ DESCRIPTION = {
 }
 
 
-def gate_flops(cfg, N, B):
+def gate_flops(cfg, passes, B):
     """Algorithmic flops of all gate products of one timestep (every layer):
-    2 * (2N B rows) * 4H * (E_l + H) per layer."""
+    2 * (passes * B rows) * 4H * (E_l + H) per layer (2N passes for central
+    differences, N + 1 for forward differences)."""
     L, E, H = cfg["n_layers"], cfg["embed"], cfg["hidden"]
-    rows = 2 * N * B
+    rows = passes * B
     return sum(2 * rows * 4 * H * ((E if l == 0 else H) + H) for l in range(L))
 
 
@@ -85,26 +89,26 @@ def update_hbm(P, w, upd):
             "frac": gbps / HBM_PEAK_GBPS}
 
 
-def embed_hbm(cfg, N, B, w, emb):
+def embed_hbm(cfg, passes, B, w, emb, fd=False):
     """Algorithmic HBM rate of the perturbed-embedding kernel: per launch it
-    writes the 2N*B rows of E activations (w bytes each; padding rows
+    writes the passes*B rows of E activations (w bytes each; padding rows
     included, as written) and reads B rows of EMB."""
     ms, n = emb
     if n == 0 or ms <= 0:
         return None
-    from paper_2505_17852_amd import workloads as wl  # noqa: F401
-    gran = 128 if w == 2 else 32
+    gran = (128 if w == 2 else 32) * (2 if fd else 1)
     Bp = (B + gran - 1) // gran * gran
     E = cfg["embed"]
-    byt = 2 * N * Bp * E * w + B * E * w
+    byt = passes * Bp * E * w + B * E * w
     gbps = byt / (ms / n * 1e-3) / 1e9
     return {"bytes_per_launch": byt, "ms_per_launch": ms / n, "GBps": gbps, "frac": gbps / HBM_PEAK_GBPS}
 
 
-def cpu_baseline(name, budget_s=20.0):
+def cpu_baseline(name, budget_s=20.0, fd=False):
     """The oracle on the host cores, on a bounded sample of the workload:
     the full batch with the first N' probes (N' doubling until the budget is
-    used), losses and update. Rate = 2 N' B C / time."""
+    used), losses and update. Rate = 2 N' B C / time (central differences) or
+    (N' + 1) B C / time (forward differences)."""
     import numpy as np  # noqa: F401
     from oracle import oracle as ref
     from paper_2505_17852_amd import workloads as wl
@@ -121,12 +125,17 @@ def cpu_baseline(name, budget_s=20.0):
     while True:
         th = theta.copy()
         t0 = time.perf_counter()
-        lp, lm = ref.perturbed_losses(cfg, th, sd["step"], w["eps"], n, tokens, mask)
-        ref.update(cfg, th, sd["step"], w["eps"], w["lr"], lp, lm)
+        if fd:
+            L, L0 = ref.fd_losses(cfg, th, sd["step"], w["eps"], n, tokens, mask)
+            ref.fd_update(cfg, th, sd["step"], w["eps"], w["lr"], L, L0)
+        else:
+            lp, lm = ref.perturbed_losses(cfg, th, sd["step"], w["eps"], n, tokens, mask)
+            ref.update(cfg, th, sd["step"], w["eps"], w["lr"], lp, lm)
         dt = time.perf_counter() - t0
         spent += dt
-        rate = 2 * n * B * C / dt
-        sample = f"{name} with the first {n} of {w['N']} probes, B={B} C={C} (losses + update)"
+        rate = (n + 1 if fd else 2 * n) * B * C / dt
+        what = "forward-difference losses + update" if fd else "losses + update"
+        sample = f"{name} with the first {n} of {w['N']} probes, B={B} C={C} ({what})"
         if spent + 2.2 * dt > budget_s or n >= w["N"]:
             break
         n *= 2
@@ -141,6 +150,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="c4", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--estimator", default="cd", choices=["cd", "fd"],
+                    help="cd: central differences, 2N passes (default); fd: forward "
+                         "differences, N perturbed passes and one clean pass")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs one GPU's share of the step; --gpus {args.gpus} is not supported "
@@ -175,14 +187,21 @@ def main():
     md = None if mask is None else torch.from_numpy(mask).to(dev)
     assert int(td.min()) >= 0 and int(td.max()) < cfg["vocab"]
     ws = zo.new_workspace(cfg, N, B, C, dev)
+    fd = args.estimator == "fd"
+    passes = N + 1 if fd else 2 * N
     Lp = torch.empty(N, dtype=torch.float32, device=dev)
-    Lm = torch.empty(N, dtype=torch.float32, device=dev)
+    Lm = torch.empty(1 if fd else N, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(k):
-        zo.perturbed_losses(cfg, theta, sd["step"] + k, eps, N, td, md, Lplus=Lp, Lminus=Lm,
-                            workspace=ws, stream=stream, check_tokens=False)
-        zo.update(cfg, theta, sd["step"] + k, eps, lr, Lp, Lm, stream=stream)
+        if fd:
+            zo.fd_losses(cfg, theta, sd["step"] + k, eps, N, td, md, L=Lp, L0=Lm, workspace=ws,
+                         stream=stream, check_tokens=False)
+            zo.fd_update(cfg, theta, sd["step"] + k, eps, lr, Lp, Lm, stream=stream)
+        else:
+            zo.perturbed_losses(cfg, theta, sd["step"] + k, eps, N, td, md, Lplus=Lp, Lminus=Lm,
+                                workspace=ws, stream=stream, check_tokens=False)
+            zo.update(cfg, theta, sd["step"] + k, eps, lr, Lp, Lm, stream=stream)
 
     for k in range(W):
         step(k)
@@ -203,19 +222,19 @@ def main():
     losses_ok = bool(torch.isfinite(Lp).all() and torch.isfinite(Lm).all())
 
     ms_per_step = dt / K * 1e3
-    tokens_per_step = 2 * N * B * C
+    tokens_per_step = passes * B * C
     value = tokens_per_step / (dt / K)
     dtype = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"
     peak = PEAK_TFLOPS[dtype]
     gate_ms, gate_n = prof["gate"]
-    fl_step = gate_flops(cfg, N, B) * C  # algorithmic gate flops per step
+    fl_step = gate_flops(cfg, passes, B) * C  # algorithmic gate flops per step
     fl_launch = fl_step / (cfg["n_layers"] * C)
     achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
     fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
     mult = 2 if dtype == "bf16" else 1
     kernels = {k: {"ms_per_step": v[0] / K, "launches_per_step": v[1] / K} for k, v in prof.items()}
     out = {
-        "metric": METRIC,
+        "metric": METRIC_FD if fd else METRIC,
         "value": value,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -227,12 +246,13 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic",
-        "config": {"workload": f"{name}: {DESCRIPTION[name]}", "N": N, "B": B, "C": C,
+        "config": {"workload": f"{name}: {DESCRIPTION[name]}", "estimator": args.estimator,
+                   "N": N, "B": B, "C": C,
                    "params": zo.param_count(cfg), "eps": eps, "lr": lr},
         "roofline": {"bound": "mfma", "kernel": "gate (fused LSTM layer step)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": None if achieved is None else achieved / peak,
-                     "traffic": measured_traffic(name, dtype),
+                     "traffic": None if fd else measured_traffic(name, dtype),
                      "flops_per_launch": fl_launch,
                      # the bf16 kernels run the weight and probe products as two MFMA
                      # streams: executed matrix work is twice the algorithmic work
@@ -242,13 +262,13 @@ def main():
         "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"]),
         # the perturbed embedding writes 2N*B rows of E activations per timestep
         # (and gathers B rows of EMB): algorithmic bytes over its event time
-        "embed_hbm": embed_hbm(cfg, N, B, 2 if dtype == "bf16" else 4, prof["embed"]),
+        "embed_hbm": embed_hbm(cfg, passes, B, 2 if dtype == "bf16" else 4, prof["embed"], fd),
         "kernels": kernels,
         "losses_finite": losses_ok,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(name)
+        out["cpu_baseline"] = cpu_baseline(name, fd=fd)
     print(json.dumps(out), flush=True)
 
 

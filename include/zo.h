@@ -87,7 +87,7 @@ typedef struct {
  * configuration is invalid. Host only. */
 size_t zo_param_count(const zo_config* cfg);
 
-/* Bytes of device workspace zo_perturbed_losses uses for N probes and a
+/* Bytes of device workspace zo_perturbed_losses (or zo_fd_losses) uses for N probes and a
  * batch of B sequences of C positions; 0 if the arguments are invalid.
  * Host only. With normal probes this includes the probe cache: N * P_g
  * values of eps z (fp32 weights) or bf16(eps z) (bf16 weights) for the
@@ -151,6 +151,26 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
               uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
               void* stream);
+
+/* Forward differences (Eq. 1's one-sided difference; the paper's FD-RGE,
+ * compared with CD-RGE in its appendix): N + 1 passes instead of 2N.
+ *   L   device fp32 [N]: the loss at theta + eps z_{i0+n}, as zo_perturbed_losses'
+ *       Lplus (bit-identical to it)
+ *   L0  device fp32 [1]: the loss at theta itself (the clean pass)
+ * Other arguments, the workspace (zo_workspace_bytes covers both estimators)
+ * and the return codes as for zo_perturbed_losses; with fp32 weights the
+ * clean pass uses the weight tile itself (ZO_FP32_SPLIT does not apply). */
+int zo_fd_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                 uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                 float* L, float* L0, void* workspace, size_t ws_bytes, void* stream);
+
+/* The forward-difference update:
+ *   c_n = fp32( (lr / N) * (L_n - L0) / eps )  (computed in double)
+ *   theta_j <- theta_j - sum_n c_n z_{i0+n}[j]
+ * with the summation, rounding, alignment, skipping (any of L, L0 not
+ * finite) and return codes of zo_update. L device fp32 [N], L0 device fp32 [1]. */
+int zo_fd_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                 uint32_t i0, const float* L, const float* L0, int32_t* skipped_out, void* stream);
 
 /* Writes z_i[j0 .. j0+n) of the probe kind `probe` (ZO_RADEMACHER or
  * ZO_GAUSSIAN) to out (device fp32 [n], n <= 2^30). For checking the regenerated probe

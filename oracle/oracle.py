@@ -77,6 +77,12 @@ def _declare(L):
                                           C.c_uint32, i32p, u8p, C.c_int32, C.c_int32, f32p, f32p]
     L.zo_ref_update_coeff.argtypes = [C.c_float, C.c_int32, C.c_float, C.c_float, C.c_float]
     L.zo_ref_update_coeff.restype = C.c_float
+    L.zo_ref_fd_losses.argtypes = [cfgp, C.c_void_p, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
+                                   C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    L.zo_ref_fd_update_coeff.argtypes = [C.c_float, C.c_int32, C.c_float, C.c_float, C.c_float]
+    L.zo_ref_fd_update_coeff.restype = C.c_float
+    L.zo_ref_fd_update.argtypes = [cfgp, C.c_void_p, C.c_uint64, C.c_float, C.c_float, C.c_int32,
+                                   C.c_uint32, C.c_void_p, C.c_float]
     L.zo_ref_update.argtypes = [cfgp, C.c_void_p, C.c_uint64, C.c_float, C.c_float, C.c_int32,
                                 C.c_uint32, f32p, f32p]
     L.zo_ref_update_sampled.argtypes = [cfgp, C.c_void_p, C.c_uint64, C.c_float, C.c_float, C.c_int32,
@@ -223,6 +229,34 @@ def update(cfg, theta: np.ndarray, seed, eps, lr, Lp, Lm, i0=0) -> int:
     Lm = np.ascontiguousarray(Lm, np.float32)
     return lib().zo_ref_update(C.byref(s), theta.ctypes.data_as(C.c_void_p), seed, eps, lr, Lp.size,
                                i0, _p(Lp, C.c_float), _p(Lm, C.c_float))
+
+
+def fd_losses(cfg, theta, seed, eps, N, tokens, mask=None, i0=0):
+    """Forward differences: (L [N] at theta + eps z_{i0+n}, L0 at theta), fp64."""
+    s = cfg_struct(cfg)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+    B, C1 = tokens.shape
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    L = np.zeros(N, np.float64)
+    L0 = np.zeros(1, np.float64)
+    st = lib().zo_ref_fd_losses(C.byref(s), theta.ctypes.data_as(C.c_void_p), seed, eps, N, i0,
+                                _p(tokens, C.c_int32), None if m is None else _p(m, C.c_uint8), B, C1 - 1,
+                                _p(L, C.c_double), _p(L0, C.c_double))
+    if st != 0:
+        raise ValueError(f"oracle fd_losses status {st}")
+    return L, float(L0[0])
+
+
+def fd_update_coeff(lr, N, L, L0, eps) -> float:
+    return lib().zo_ref_fd_update_coeff(lr, N, L, L0, eps)
+
+
+def fd_update(cfg, theta: np.ndarray, seed, eps, lr, L, L0, i0=0) -> int:
+    """In-place forward-difference update of theta; returns the status code."""
+    s = cfg_struct(cfg)
+    L = np.ascontiguousarray(L, np.float32)
+    return lib().zo_ref_fd_update(C.byref(s), theta.ctypes.data_as(C.c_void_p), seed, eps, lr, L.size, i0,
+                                  _p(L, C.c_float), float(np.float32(L0)))
 
 
 def update_sampled(cfg, theta, seed, eps, lr, Lp, Lm, idx, i0=0) -> np.ndarray:

@@ -511,15 +511,26 @@ static void update_one(const zo_ref_config* cfg, const void* theta_in, void* the
     else ((float*)theta_out)[o] = (float)t;
 }
 
+static int apply_update(const zo_ref_config* cfg, void* theta, uint64_t seed, int32_t N, uint32_t i0,
+                        float* coeff);
+
 int zo_ref_update(const zo_ref_config* cfg, void* theta, uint64_t seed, float eps, float lr,
                   int32_t N, uint32_t i0, const float* Lplus, const float* Lminus) {
     float* coeff = NULL;
     if (!theta) return ZO_REF_EINVAL;
     int st = update_args(cfg, eps, lr, N, Lplus, Lminus, &coeff);
     if (st != ZO_REF_OK) return st;
+    return apply_update(cfg, theta, seed, N, i0, coeff);
+}
+
+/* theta_j <- theta_j - sum_n coeff[n] z_{i0+n}[j] (double, ascending n), one
+ * rounding to the storage type; frees coeff. */
+static int apply_update(const zo_ref_config* cfg, void* theta, uint64_t seed, int32_t N, uint32_t i0,
+                        float* coeff) {
     uint64_t P = zo_ref_param_count(cfg);
     double* acc = calloc(P, sizeof(double));
     float* z = malloc(sizeof(float) * P);
+    if (!acc || !z) { free(acc); free(z); free(coeff); return ZO_REF_ENOMEM; }
     for (int32_t n = 0; n < N; ++n) {
         zo_ref_probe(cfg->probe, seed, i0 + (uint32_t)n, 0, P, z);
 #pragma omp parallel for schedule(static) if (P >= (1u << 16))
@@ -550,6 +561,50 @@ int zo_ref_update_sampled(const zo_ref_config* cfg, const void* theta, uint64_t 
     }
     free(coeff);
     return ZO_REF_OK;
+}
+
+/* ======================================================================= */
+/* Forward differences (Eq. 1, the one-sided difference the paper compares  */
+/* with the central one): one clean loss L0 = L(theta) and N losses          */
+/* L_n = L(theta + eps z_{i0+n}); the update uses                            */
+/*   c_n = (lr / N) (L_n - L0) / eps  (double, rounded to fp32)              */
+/* and the same sum over probes as zo_ref_update.                            */
+/* ======================================================================= */
+int zo_ref_fd_losses(const zo_ref_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                     uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                     double* L, double* L0) {
+    if (!cfg_ok(cfg) || !theta || !tokens || !L || !L0) return ZO_REF_EINVAL;
+    if (N < 1 || B < 1 || C < 1 || !(eps > 0.0f) || !isfinite(eps)) return ZO_REF_EINVAL;
+    if (!tokens_ok(cfg, tokens, B, C)) return ZO_REF_EINVAL;
+    uint64_t P = zo_ref_param_count(cfg);
+    double* w = malloc(sizeof(double) * P);
+    if (!w) return ZO_REF_ENOMEM;
+    for (uint64_t j = 0; j < P; ++j) w[j] = theta_at(cfg, theta, j);
+    *L0 = zo_ref_lstm_loss(cfg, w, tokens, mask, B, C, C + 1, NULL);
+    for (int32_t n = 0; n < N; ++n) {
+        zo_ref_materialise(cfg, theta, seed, i0 + (uint32_t)n, (double)eps, 0, w);
+        L[n] = zo_ref_lstm_loss(cfg, w, tokens, mask, B, C, C + 1, NULL);
+    }
+    free(w);
+    return ZO_REF_OK;
+}
+
+float zo_ref_fd_update_coeff(float lr, int32_t N, float L, float L0, float eps) {
+    double c = ((double)lr / (double)N) * (((double)L - (double)L0) / (double)eps);
+    return (float)c;
+}
+
+int zo_ref_fd_update(const zo_ref_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                     uint32_t i0, const float* L, float L0) {
+    if (!cfg_ok(cfg) || !theta || !L || N < 1) return ZO_REF_EINVAL;
+    if (!(eps > 0.0f) || !isfinite(eps) || !isfinite(lr)) return ZO_REF_EINVAL;
+    if (!isfinite(L0)) return ZO_REF_ENONFINITE;
+    for (int32_t n = 0; n < N; ++n)
+        if (!isfinite(L[n])) return ZO_REF_ENONFINITE;
+    float* c = malloc(sizeof(float) * (size_t)N);
+    if (!c) return ZO_REF_ENOMEM;
+    for (int32_t n = 0; n < N; ++n) c[n] = zo_ref_fd_update_coeff(lr, N, L[n], L0, eps);
+    return apply_update(cfg, theta, seed, N, i0, c);
 }
 
 /* ======================================================================= */

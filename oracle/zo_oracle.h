@@ -90,6 +90,15 @@ int zo_ref_perturbed_losses(const zo_ref_config* cfg, const void* theta, uint64_
 float zo_ref_update_coeff(float lr, int32_t N, float Lplus, float Lminus, float eps);
 int zo_ref_update(const zo_ref_config* cfg, void* theta, uint64_t seed, float eps, float lr,
                   int32_t N, uint32_t i0, const float* Lplus, const float* Lminus);
+
+/* Forward differences (Eq. 1): L[n] = L(theta + eps z_{i0+n}), *L0 = L(theta)
+ * (double). Update: c_n = fp32((lr/N)(L[n] - L0)/eps), then as zo_ref_update. */
+int zo_ref_fd_losses(const zo_ref_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                     uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                     double* L, double* L0);
+float zo_ref_fd_update_coeff(float lr, int32_t N, float L, float L0, float eps);
+int zo_ref_fd_update(const zo_ref_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                     uint32_t i0, const float* L, float L0);
 int zo_ref_update_sampled(const zo_ref_config* cfg, const void* theta, uint64_t seed, float eps,
                           float lr, int32_t N, uint32_t i0, const float* Lplus,
                           const float* Lminus, const uint64_t* idx, uint64_t n_idx, void* out);

@@ -79,10 +79,8 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
   if (idx >= M * E4) return;
   const int64_t r = idx / E4;
   const int e = (int)(idx - r * E4) * 4;
-  const int pair = (int)(r / rm.pair_rows);
-  const int loc = (int)(r - pair * rm.pair_rows);
-  const int sidx = loc >= rm.Bp;
-  const int b = loc - sidx * rm.Bp;
+  const PassOf ps = pass_of(rm, r);
+  const int pair = ps.probe, b = ps.b;
   f4 out = {0.f, 0.f, 0.f, 0.f};
   if (b < B) {
     const int tok = tokens[(int64_t)b * (C + 1) + t];
@@ -96,7 +94,7 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
     } else {
       gauss_block(key, i0 + pair, j >> 2, z);
     }
-    const float se = sidx ? -eps : eps;
+    const float se = (float)ps.sign * eps;  // 0 for the clean pass: out = w
 #pragma unroll
     for (int q = 0; q < 4; ++q) out[q] = w[q] + fmul(se, z[q]);
   }
@@ -140,11 +138,13 @@ struct Smem {
 };
 
 // colmap(rho, &n) -> true if LDS column rho maps to a real weight row n.
+// fd: forward differences: the second tile holds W itself (the clean pass)
+// instead of W - eps z.
 template <int kind, bool kSplit, typename ColMap>
 __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, const Seg s1,
                                              int nseg, ColMap colmap, const int (&wrow)[4], int arow0,
                                              bool wave_neg, Key key, uint32_t probe, float eps,
-                                             Smem& sm) {
+                                             bool fd, Smem& sm) {
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int g4 = lane >> 4;
@@ -228,7 +228,7 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
           vm[e] = z;
         } else {
           vp[e] = fadd(w, z);
-          vm[e] = fadd(w, -z);
+          vm[e] = fadd(w, fd ? 0.0f : -z);
         }
       }
       *(f4*)(&sm.p[rho * LDK + 16 * half + 4 * q]) = vp;
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
   const int wm = wave & 1, wn = wave >> 1;
   const int u0 = blockIdx.x * 32;
   const int64_t m0 = (int64_t)blockIdx.y * BM;
-  const int pair = (int)(m0 / g.rm.pair_rows);
+  const int pair = pass_of(g.rm, m0).probe;
   const int H = g.H;
   auto colmap = [&](int rho, int& n) {
     n = (rho >> 5) * H + u0 + (rho & 31);
@@ -317,7 +317,9 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
   int wrow[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) wrow[q] = q * 32 + 16 * wn + (lane & 15);
-  const bool wave_neg = (m0 + 32 * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
+  // a 32-row wave tile lies inside one pass: one sign (+1, -1, or 0 clean)
+  const int ws = pass_of(g.rm, m0 + 32 * wm).sign;
+  const bool wave_neg = ws <= 0;  // tile W - eps z, or W for the clean pass
   f4 acc[2][4];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
@@ -330,29 +332,28 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
                kind == kGaussCached ? g.zc_ih + zpos : nullptr};
   const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
                kind == kGaussCached ? g.zc_hh + zpos : nullptr};
-  mainloop_f32<kind, kSplit>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
+  mainloop_f32<kind, kSplit>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps,
+                             g.rm.fd != 0, sm);
 
   // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
   const int u = u0 + 16 * wn + (lane & 15);
   const float* bias = g.theta + g.off_b;
   const float* zb = g.zb + (int64_t)pair * 4 * H;
-  float bp[4], bm[4];
+  float bs[4];  // bias + eps z_b, bias - eps z_b, or the bias (clean pass)
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const float bb = bias[q * H + u], zz = zb[q * H + u];
-    bp[q] = bb + zz;
-    bm[q] = bb - zz;
+    bs[q] = ws > 0 ? bb + zz : ws < 0 ? bb - zz : bb;
   }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int64_t r = m0 + 32 * wm + 16 * mt + 4 * (lane >> 4) + v;
-      const bool neg = (r - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
-      const float ai = acc[mt][0][v] + (neg ? bm[0] : bp[0]);
-      const float af = acc[mt][1][v] + (neg ? bm[1] : bp[1]);
-      const float ag = acc[mt][2][v] + (neg ? bm[2] : bp[2]);
-      const float ao = acc[mt][3][v] + (neg ? bm[3] : bp[3]);
+      const float ai = acc[mt][0][v] + bs[0];
+      const float af = acc[mt][1][v] + bs[1];
+      const float ag = acc[mt][2][v] + bs[2];
+      const float ao = acc[mt][3][v] + bs[3];
       const float ig = sigmoidf_(ai), fg = sigmoidf_(af), gg = tanhf_(ag), og = sigmoidf_(ao);
       const int64_t o = r * H + u;
       const float c = fg * g.cst[o] + ig * gg;
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
   const int64_t rr0 = (int64_t)blockIdx.y * BM;
   const int tt = (int)(rr0 / g.M);
   const int64_t r0 = rr0 - (int64_t)tt * g.M;
-  const int pair = (int)(r0 / g.rm.pair_rows);
+  const int pair = pass_of(g.rm, r0).probe;
   const int V = g.V;
   auto colmap = [&](int rho, int& n) {
     n = v0 + rho;
@@ -411,7 +412,9 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
   int wrow[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) wrow[q] = 64 * wn + 16 * q + (lane & 15);
-  const bool wave_neg = (r0 + 32 * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
+  // a 32-row wave tile lies inside one pass: one sign (+1, -1, or 0 clean)
+  const int ws = pass_of(g.rm, r0 + 32 * wm).sign;
+  const bool wave_neg = ws <= 0;
   f4 acc[2][4];
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
@@ -420,11 +423,12 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
   const uint32_t probe = g.i0 + (uint32_t)pair;
   const Seg s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
                kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
-  mainloop_f32<kind, kSplit>(acc, s0, s0, 1, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps, sm);
+  mainloop_f32<kind, kSplit>(acc, s0, s0, 1, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps,
+                             g.rm.fd != 0, sm);
 
   const float* bout = g.theta + g.off_b;
   const float* zbo = g.zbo + (int64_t)pair * V;
-  float bp[4], bmn[4];
+  float bs[4];  // bias + eps z_b, bias - eps z_b, or the bias (clean pass)
   bool cok[4];
   int col[4];
 #pragma unroll
@@ -432,23 +436,19 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
     col[q] = v0 + 64 * wn + 16 * q + (lane & 15);
     cok[q] = col[q] < V;
     const float bb = cok[q] ? bout[col[q]] : 0.f, zz = cok[q] ? zbo[col[q]] : 0.f;
-    bp[q] = bb + zz;
-    bmn[q] = bb - zz;
+    bs[q] = ws > 0 ? bb + zz : ws < 0 ? bb - zz : bb;
   }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int lrow = 32 * wm + 16 * mt + 4 * (lane >> 4) + v;
-      const int64_t r = r0 + lrow;
-      const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
-      const bool neg = loc >= g.rm.Bp;
-      const int b = neg ? loc - g.rm.Bp : loc;
+      const int b = pass_of(g.rm, r0 + lrow).b;
       float y[4];
       float mx = -INFINITY;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        y[q] = cok[q] ? acc[mt][q][v] + (neg ? bmn[q] : bp[q]) : -INFINITY;
+        y[q] = cok[q] ? acc[mt][q][v] + bs[q] : -INFINITY;
         mx = fmaxf(mx, y[q]);
       }
       if (b < g.B) {
@@ -494,8 +494,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* pmax, const f
   if (rr >= rows) return;
   const int tt = (int)(rr / M);
   const int64_t r = rr - (int64_t)tt * M;
-  const int64_t loc = r % rm.pair_rows;
-  const int b = (int)(loc >= rm.Bp ? loc - rm.Bp : loc);
+  const int b = pass_of(rm, r).b;
   if (b >= B || (mask && !mask[(int64_t)b * C + t0 + tt])) {
     ptgt[rr] = 0.f;
     return;
@@ -526,7 +525,9 @@ __global__ __launch_bounds__(256) void accumulate_kernel(const float* ell, int64
   row_loss[r] = acc;
 }
 
-// L+-_n = (sum over the pass's sequences of their row sums) / (scored positions).
+// Loss of each pass = (sum over the pass's sequences of their row sums) /
+// (scored positions). Central differences: pass 2n -> Lp[n], 2n+1 -> Lm[n];
+// forward differences: pass p < N -> Lp[p], the clean pass N -> Lm[0].
 __global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int N, int B, int C,
                                                      RowMap rm, const uint8_t* mask, float* Lp,
                                                      float* Lm) {
@@ -544,13 +545,20 @@ __global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int
     __syncthreads();
   }
   const double total = part[0];
-  for (int p = threadIdx.x; p < 2 * N; p += blockDim.x) {
+  const int npass = rm.fd ? N + 1 : 2 * N;
+  for (int p = threadIdx.x; p < npass; p += blockDim.x) {
     double s = 0.0;
     const double* rl = row_loss + (int64_t)p * rm.Bp;
     for (int b = 0; b < B; ++b) s += rl[b];
     const float L = total > 0.0 ? (float)(s / total) : 0.0f;
-    if (p & 1) Lm[p >> 1] = L;
-    else Lp[p >> 1] = L;
+    if (rm.fd) {
+      if (p < N) Lp[p] = L;
+      else Lm[0] = L;
+    } else if (p & 1) {
+      Lm[p >> 1] = L;
+    } else {
+      Lp[p >> 1] = L;
+    }
   }
 }
 
@@ -628,7 +636,7 @@ hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
 hipError_t launch_embed_f32(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
   const Rows& R = a.rows;
   const int E = a.cfg.embed;
-  const RowMap rm{R.Bp, R.pair_rows};
+  const RowMap rm = row_map(R);
   const int64_t n = R.M * (E / 4);
   const unsigned grid = (unsigned)((n + 255) / 256);
   const Key key = make_key(a.seed);
@@ -662,7 +670,7 @@ hipError_t launch_gate_f32(const ForwardArgs& a, int l, const void* x, const voi
   g.key = make_key(a.seed);
   g.i0 = a.i0;
   g.eps = a.eps;
-  g.rm = RowMap{R.Bp, R.pair_rows};
+  g.rm = row_map(R);
   g.zc_ih = a.zc ? (const float*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const float*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
@@ -696,7 +704,7 @@ hipError_t launch_head_f32(const ForwardArgs& a, const void* hist, int t0, int T
   h.key = make_key(a.seed);
   h.i0 = a.i0;
   h.eps = a.eps;
-  h.rm = RowMap{R.Bp, R.pair_rows};
+  h.rm = row_map(R);
   h.M = R.M;
   h.rows = (int64_t)Tc * R.M;
   h.tokens = a.tokens;
@@ -739,7 +747,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   const int64_t M = R.M;
   const size_t el = bf16 ? 2 : 4;  // activation element size
   const size_t state = (size_t)M * H * el;
-  const RowMap rm{R.Bp, R.pair_rows};
+  const RowMap rm = row_map(R);
   char* ws = a.work;
   char* x0 = ws + W.x0;
   char* hbuf = ws + W.hbuf;

@@ -160,15 +160,16 @@ struct SegB {
 // acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave.
 // colmap(rho, &n) maps LDS column rho (0..TN-1) to a weight row n inside the
 // matrix (columns beyond the matrix map to a valid row; they are never
-// scored). neg: this wave's rows are the -eps pass; eps_b: bf16 bits of eps.
+// scored). sgn: the sign of eps for this wave's rows (+1, -1, or 0 for the
+// clean pass of forward differences, kFD only); eps_b: bf16 bits of eps.
 // kTrans: accumulate the transposed product (weight columns on the rows of
 // each 32x32 tile, activation rows on its columns): both operands of
 // v_mfma_f32_32x32x16_bf16 have the same fragment layout, so only their order
 // changes. Lane (lr, lg) then holds, for activation row lr of a tile, the 16
 // columns 8 (v >> 2) + 4 lg + (v & 3), v < 16.
-template <int kind, bool kTrans = false, typename ColMap>
+template <int kind, bool kTrans = false, bool kFD = false, typename ColMap>
 __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
-                                              int nseg, ColMap colmap, Key key, uint32_t probe, bool neg,
+                                              int nseg, ColMap colmap, Key key, uint32_t probe, int sgn,
                                               float eps, uint16_t eps_b) {
   using T = Tiles<kind>;
   constexpr int MT = T::MT;
@@ -286,7 +287,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   const uint32_t w_lane = (uint32_t)(64 * wn + lr) * kRowBytes;
   // the pair (s eps, s eps) in bf16 (signs), or the sign flip of -eps rows (normal)
   const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
+  const bool neg = sgn < 0;
   const uint32_t zc = kind == ZO_RADEMACHER ? (neg ? ebits ^ 0x80008000u : ebits) : (neg ? 0x80008000u : 0u);
+  // forward differences: the clean pass multiplies its probe fragments by 0
+  const uint32_t zmask = sgn == 0 ? 0u : 0xFFFFFFFFu;
   struct Frag {
     bf8 a[MT], w[2], z[2];
   };
@@ -318,11 +322,17 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         if constexpr (kind == ZO_RADEMACHER) {
           const uint32_t x = bits[nt][s >> 1];
 #pragma unroll
-          for (int d = 0; d < 4; ++d) v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) ^ zc;
+          for (int d = 0; d < 4; ++d) {
+            v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) ^ zc;
+            if constexpr (kFD) v[d] &= zmask;
+          }
         } else {
           v = *(const u4*)(pw + T::WBytes + 32 * nt * kRowBytes + so);
 #pragma unroll
-          for (int d = 0; d < 4; ++d) v[d] ^= zc;
+          for (int d = 0; d < 4; ++d) {
+            v[d] ^= zc;
+            if constexpr (kFD) v[d] &= zmask;
+          }
         }
         f.z[nt] = as_bf8(v);
       }
@@ -446,7 +456,7 @@ struct GateArgsB {
 // is gate c / 16 of unit 16 wn + c % 16, so lane lr holds gates i, g (lr < 16)
 // or f, o (lr >= 16) of unit lr % 16 in its two column tiles, and one
 // exchange with lane lr ^ 16 brings all four gates of a (row, unit) together.
-template <int kind>
+template <int kind, bool kFD>
 __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -456,8 +466,8 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   tile_of(blockIdx.x, g.n_row_blocks, g.H / (T::TN / 4), mb, nb);
   const int u0 = nb * (T::TN / 4);
   const int64_t m0 = (int64_t)mb * TM;
-  const int pair = (int)(m0 / g.rm.pair_rows);
-  const bool neg = (m0 + T::WROWS * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
+  const int pair = pass_of(g.rm, m0).probe;
+  const int sgn = pass_of(g.rm, m0 + T::WROWS * wm).sign;  // a wave tile lies inside one pass
   const int H = g.H;
   auto colmap = [&](int rho, int& n) {
     const int c = rho & 63;
@@ -470,7 +480,7 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
                 kind == kGaussCached ? g.zc_ih + zpos : nullptr};
   const SegB s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
-  mainloop_bf16<kind>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
+  mainloop_bf16<kind, false, kFD>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
 
   const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
   const int u = u0 + 16 * wn + (lr & 15);
@@ -480,7 +490,7 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
     const int gate = 2 * nt + hi;
     const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)(gate * H + u)]);
     const float z = g.zb[(int64_t)pair * 4 * H + gate * H + u];
-    bias[nt] = neg ? b - z : b + z;
+    bias[nt] = b + (float)sgn * z;
   }
 #pragma unroll
   for (int mt = 0; mt < T::MT; ++mt) {
@@ -529,7 +539,7 @@ struct HeadArgsB {
   uint64_t zc_stride;
 };
 
-template <int kind>
+template <int kind, bool kFD>
 __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -541,15 +551,15 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   const int64_t rr0 = (int64_t)mb * TM;
   const int tt = (int)(rr0 / g.M);
   const int64_t r0 = rr0 - (int64_t)tt * g.M;
-  const int pair = (int)(r0 / g.rm.pair_rows);
-  const bool neg = (r0 + T::WROWS * wm - (int64_t)pair * g.rm.pair_rows) >= g.rm.Bp;
+  const int pair = pass_of(g.rm, r0).probe;
+  const int sgn = pass_of(g.rm, r0 + T::WROWS * wm).sign;  // a wave tile lies inside one pass
   const int V = g.V;
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
   f16v acc[T::MT][2];
   zero_acc(acc);
   const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
-  mainloop_bf16<kind, true>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, neg, g.eps, g.eps_b);
+  mainloop_bf16<kind, true, kFD>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
@@ -566,7 +576,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
       if (col < V) {
         const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)col]);
         const float z = g.zbo[(int64_t)pair * V + col];
-        a = neg ? b - z : b + z;
+        a = b + (float)sgn * z;
       }
       add[nt][v] = a;
     }
@@ -577,9 +587,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
 #pragma unroll
   for (int mt = 0; mt < T::MT; ++mt) {
     const int lrow = T::WROWS * wm + 32 * mt + lr;
-    const int64_t r = r0 + lrow;
-    const int loc = (int)(r - (int64_t)pair * g.rm.pair_rows);
-    const int b = neg ? loc - g.rm.Bp : loc;
+    const int b = pass_of(g.rm, r0 + lrow).b;
     const int tgt = b < g.B ? g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1] - cbase : -1;
     float mx = -INFINITY, yt = 0.f;
     bool has_t = false;
@@ -639,10 +647,8 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
   if (idx >= M * E4) return;
   const int64_t r = idx / E4;
   const int e = (int)(idx - r * E4) * 4;
-  const int pair = (int)(r / rm.pair_rows);
-  const int loc = (int)(r - pair * rm.pair_rows);
-  const int sidx = loc >= rm.Bp;
-  const int b = loc - sidx * rm.Bp;
+  const PassOf ps = pass_of(rm, r);
+  const int pair = ps.probe, b = ps.b;
   uint32_t lo = 0u, hi = 0u;
   if (b < B) {
     const int tok = tokens[(int64_t)b * (C + 1) + t];
@@ -658,7 +664,7 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
     } else {
       gauss_block(key, i0 + pair, j >> 2, z);
     }
-    const float se = sidx ? -eps : eps;
+    const float se = (float)ps.sign * eps;  // 0 for the clean pass
     lo = pack_bf16x2(w[0] + se * z[0], w[1] + se * z[1]);
     hi = pack_bf16x2(w[2] + se * z[2], w[3] + se * z[3]);
   }
@@ -677,16 +683,14 @@ __global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* the
   if (idx >= M * E32) return;
   const int64_t r = idx / E32;
   const int e = (int)(idx - r * E32) * 32;
-  const int pair = (int)(r / rm.pair_rows);
-  const int loc = (int)(r - pair * rm.pair_rows);
-  const int sidx = loc >= rm.Bp;
-  const int b = loc - sidx * rm.Bp;
+  const PassOf ps = pass_of(rm, r);
+  const int pair = ps.probe, b = ps.b;
   u4 out[4] = {u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}};
   if (b < B) {
     const int tok = tokens[(int64_t)b * (C + 1) + t];
     const uint64_t j = emb_off + (uint64_t)tok * E + e;  // a multiple of 32: one whole word
     const uint32_t word = rademacher_word(key, i0 + pair, j >> 5);
-    const float se = sidx ? -eps : eps;
+    const float se = (float)ps.sign * eps;  // 0 for the clean pass
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const u4 wv = *(const u4*)(theta + j + 8 * q);
@@ -709,7 +713,7 @@ __global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* the
 hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
   const Rows& R = a.rows;
   const int E = a.cfg.embed;
-  const RowMap rm{R.Bp, R.pair_rows};
+  const RowMap rm = row_map(R);
   const Key key = make_key(a.seed);
   ProfScope ps(kKEmbed, st);
   if (a.cfg.probe == ZO_RADEMACHER) {
@@ -746,24 +750,25 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.i0 = a.i0;
   g.eps = a.eps;
   g.eps_b = bf16_rne(a.eps);
-  g.rm = RowMap{R.Bp, R.pair_rows};
+  g.rm = row_map(R);
   g.n_row_blocks = (int)(R.M / TM);
   g.zc_ih = a.zc ? (const uint16_t*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const uint16_t*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
-  if (a.cfg.probe == ZO_RADEMACHER) {
-    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_RADEMACHER>::TN / 4))));
+  auto go = [&](auto kind_tag, auto fd_tag) {
+    constexpr int kind = decltype(kind_tag)::value;
+    constexpr bool fd = decltype(fd_tag)::value;
+    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<kind>::TN / 4))));
     ProfScope ps(kKGate, st);
-    gate_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(g);
-  } else if (a.zc) {
-    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<kGaussCached>::TN / 4))));
-    ProfScope ps(kKGate, st);
-    gate_bf16_kernel<kGaussCached><<<grid, NT, 0, st>>>(g);
-  } else {
-    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<ZO_GAUSSIAN>::TN / 4))));
-    ProfScope ps(kKGate, st);
-    gate_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(g);
-  }
+    gate_bf16_kernel<kind, fd><<<grid, NT, 0, st>>>(g);
+  };
+  const int kind = a.cfg.probe == ZO_RADEMACHER ? ZO_RADEMACHER : a.zc ? kGaussCached : ZO_GAUSSIAN;
+  using std::integral_constant;
+  using T_ = integral_constant<bool, true>;
+  using F_ = integral_constant<bool, false>;
+  if (kind == ZO_RADEMACHER) R.fd ? go(integral_constant<int, ZO_RADEMACHER>{}, T_{}) : go(integral_constant<int, ZO_RADEMACHER>{}, F_{});
+  else if (kind == kGaussCached) R.fd ? go(integral_constant<int, kGaussCached>{}, T_{}) : go(integral_constant<int, kGaussCached>{}, F_{});
+  else R.fd ? go(integral_constant<int, ZO_GAUSSIAN>{}, T_{}) : go(integral_constant<int, ZO_GAUSSIAN>{}, F_{});
   return hipGetLastError();
 }
 
@@ -782,7 +787,7 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.i0 = a.i0;
   h.eps = a.eps;
   h.eps_b = bf16_rne(a.eps);
-  h.rm = RowMap{R.Bp, R.pair_rows};
+  h.rm = row_map(R);
   h.M = R.M;
   h.rows = (int64_t)Tc * R.M;
   h.tokens = a.tokens;
@@ -796,16 +801,19 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.zc_out = a.zc ? (const uint16_t*)a.zc + a.zmap.out : nullptr;
   h.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)((int64_t)a.ws.nvt * (h.rows / TM)));
-  if (a.cfg.probe == ZO_RADEMACHER) {
+  auto go = [&](auto kind_tag, auto fd_tag) {
+    constexpr int kind = decltype(kind_tag)::value;
+    constexpr bool fd = decltype(fd_tag)::value;
     ProfScope ps(kKHead, st);
-    head_bf16_kernel<ZO_RADEMACHER><<<grid, NT, 0, st>>>(h);
-  } else if (a.zc) {
-    ProfScope ps(kKHead, st);
-    head_bf16_kernel<kGaussCached><<<grid, NT, 0, st>>>(h);
-  } else {
-    ProfScope ps(kKHead, st);
-    head_bf16_kernel<ZO_GAUSSIAN><<<grid, NT, 0, st>>>(h);
-  }
+    head_bf16_kernel<kind, fd><<<grid, NT, 0, st>>>(h);
+  };
+  const int kind = a.cfg.probe == ZO_RADEMACHER ? ZO_RADEMACHER : a.zc ? kGaussCached : ZO_GAUSSIAN;
+  using std::integral_constant;
+  using T_ = integral_constant<bool, true>;
+  using F_ = integral_constant<bool, false>;
+  if (kind == ZO_RADEMACHER) R.fd ? go(integral_constant<int, ZO_RADEMACHER>{}, T_{}) : go(integral_constant<int, ZO_RADEMACHER>{}, F_{});
+  else if (kind == kGaussCached) R.fd ? go(integral_constant<int, kGaussCached>{}, T_{}) : go(integral_constant<int, kGaussCached>{}, F_{});
+  else R.fd ? go(integral_constant<int, ZO_GAUSSIAN>{}, T_{}) : go(integral_constant<int, ZO_GAUSSIAN>{}, F_{});
   return hipGetLastError();
 }
 

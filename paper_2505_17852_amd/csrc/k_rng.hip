@@ -49,12 +49,12 @@ __device__ __forceinline__ float update_coeff(float lr, int N, float lp, float l
 }
 
 // Workgroup-wide check that every loss is finite (all workgroups agree).
-__device__ bool losses_finite(const float* Lp, const float* Lm, int N, int* flag) {
+__device__ bool losses_finite(const float* Lp, const float* Lm, int N, int lm_stride, int* flag) {
   if (threadIdx.x == 0) *flag = 0;
   __syncthreads();
   int bad = 0;
   for (int n = threadIdx.x; n < N; n += blockDim.x)
-    bad |= !(isfinite(Lp[n]) && isfinite(Lm[n]));
+    bad |= !(isfinite(Lp[n]) && isfinite(Lm[n * lm_stride]));
   if (bad) atomicOr(flag, 1);
   __syncthreads();
   return *flag == 0;
@@ -219,7 +219,7 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ 
                                                                 const float* __restrict__ Lp,
                                                                 const float* __restrict__ Lm,
                                                                 int32_t* __restrict__ skipped,
-                                                                uint64_t nchunks) {
+                                                                uint64_t nchunks, int lm_stride) {
   // sign words laid out [word][probe] (rows padded by 4 words) so that one
   // thread reads 8 probes' words of its parameters with two 128-bit loads
   constexpr int kRow = kUpdGroup + 4;
@@ -282,7 +282,7 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ 
   float lp = 0.f, lm = 0.f;
   if (t < kUpdGroup && t < N) {
     lp = Lp[t];
-    lm = Lm[t];
+    lm = Lm[t * lm_stride];
   }
   uint64_t chunk = blockIdx.x;
   Raw8<T> raw[kSets];
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ 
       const int ngroups = (cnt + 7) / 8;
       if (!one_group && t < cnt) {
         lp = Lp[n0 + t];
-        lm = Lm[n0 + t];
+        lm = Lm[(n0 + t) * lm_stride];
       }
       lds_barrier();  // the previous lookups no longer read the words or tables
       if (!one_group) coefficients(n0, cnt, lp, lm);
@@ -376,10 +376,11 @@ template <typename T>
 __global__ __launch_bounds__(256) void update_gaussian_kernel(T* theta, uint64_t P, Key key,
                                                               float eps, float lr, int N,
                                                               uint32_t i0, const float* Lp,
-                                                              const float* Lm, int32_t* skipped) {
+                                                              const float* Lm, int32_t* skipped,
+                                                              int lm_stride) {
   __shared__ float coef[256];
   __shared__ int flag;
-  const bool ok = losses_finite(Lp, Lm, N, &flag);
+  const bool ok = losses_finite(Lp, Lm, N, lm_stride, &flag);
   if (blockIdx.x == 0 && threadIdx.x == 0 && skipped) *skipped = ok ? 0 : 1;
   if (!ok) return;
   const int t = threadIdx.x;
@@ -390,7 +391,7 @@ __global__ __launch_bounds__(256) void update_gaussian_kernel(T* theta, uint64_t
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int n0 = 0; n0 < N; n0 += 256) {
     __syncthreads();
-    if (n0 + t < N) coef[t] = update_coeff(lr, N, Lp[n0 + t], Lm[n0 + t], eps);
+    if (n0 + t < N) coef[t] = update_coeff(lr, N, Lp[n0 + t], Lm[(n0 + t) * lm_stride], eps);
     __syncthreads();
     const int cnt = N - n0 < 256 ? N - n0 : 256;
     if (j < P) {
@@ -439,7 +440,7 @@ hipError_t launch_init(int wdtype, void* theta, uint64_t P, uint64_t seed, float
 
 hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t seed, float eps,
                          float lr, int32_t N, uint32_t i0, const float* Lp, const float* Lm,
-                         int32_t* skipped, hipStream_t s) {
+                         int32_t* skipped, hipStream_t s, int lm_stride) {
   const Key key = make_key(seed);
   ProfScope ps(kKUpdate, s);
   if (kind == ZO_RADEMACHER) {
@@ -458,18 +459,18 @@ hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t
     const unsigned grid = (unsigned)(nchunks < slots ? nchunks : slots);
     if (wdtype == ZO_WBF16)
       update_rademacher_kernel<uint16_t><<<dim3(grid), dim3(256), 0, s>>>(
-          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks);
+          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks, lm_stride);
     else
       update_rademacher_kernel<float><<<dim3(grid), dim3(256), 0, s>>>(
-          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks);
+          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks, lm_stride);
   } else {
     const uint64_t grid = ((P + 3) / 4 + 255) / 256;
     if (wdtype == ZO_WBF16)
       update_gaussian_kernel<uint16_t><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped);
+          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
     else
       update_gaussian_kernel<float><<<dim3((unsigned)grid), dim3(256), 0, s>>>(
-          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped);
+          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
   }
   return hipGetLastError();
 }

@@ -2,6 +2,7 @@
 // on the caller's stream. Nothing here allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -57,16 +58,19 @@ size_t zo_param_count(const zo_config* cfg) {
   return (size_t)zo::make_layout(*cfg).total;
 }
 
+// Both estimators' passes fit: central (2N passes) and forward (N + 1) differences.
+static zo::WsPlan plan_for(const zo_config* cfg, int32_t N, int32_t B, int32_t C, bool fd) {
+  return zo::plan_workspace(*cfg, zo::make_rows(N, B, zo::row_granule(*cfg, fd), fd), C);
+}
+
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
   if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1) return 0;
-  const zo::Rows r = zo::make_rows(N, B, zo::row_granule(*cfg));
-  return zo::plan_workspace(*cfg, r, C).total;
+  return std::max(plan_for(cfg, N, B, C, false).total, plan_for(cfg, N, B, C, true).total);
 }
 
 size_t zo_workspace_bytes_min(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
   if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1) return 0;
-  const zo::Rows r = zo::make_rows(N, B, zo::row_granule(*cfg));
-  return zo::plan_workspace(*cfg, r, C).min_total;
+  return std::max(plan_for(cfg, N, B, C, false).min_total, plan_for(cfg, N, B, C, true).min_total);
 }
 
 int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
@@ -79,17 +83,17 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
                        "zo_init");
 }
 
-int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
-                        int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
-                        int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
-                        size_t ws_bytes, void* stream) {
+static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                        uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                        float* L1, float* L2, void* workspace, size_t ws_bytes, void* stream, bool fd,
+                        const char* name) {
   int st = check_config(cfg);
   if (st) return st;
   // the bf16 forward walks K in tiles of 64
   if (cfg->wdtype == ZO_WBF16 && (cfg->embed % 64 || cfg->hidden % 64))
     return fail(ZO_ESHAPE, "bf16 weights: embed (%d) and hidden (%d) must be multiples of 64",
                 cfg->embed, cfg->hidden);
-  if (!theta || !tokens || !Lplus || !Lminus || !workspace)
+  if (!theta || !tokens || !L1 || !L2 || !workspace)
     return fail(ZO_EINVAL, "a required pointer is NULL");
   if (!aligned16(theta) || !aligned16(workspace))
     return fail(ZO_EINVAL, "theta and workspace must be 16-byte aligned");
@@ -97,8 +101,8 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   if (N < 1 || B < 1 || C < 1) return fail(ZO_EINVAL, "N, B and C must be >= 1");
   if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
     return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
-  const zo::Rows rows = zo::make_rows(N, B, zo::row_granule(*cfg));
-  if (rows.M > (int64_t)1 << 30) return fail(ZO_ESHAPE, "2N*B rows too large");
+  const zo::Rows rows = zo::make_rows(N, B, zo::row_granule(*cfg, fd), fd);
+  if (rows.M > (int64_t)1 << 30) return fail(ZO_ESHAPE, "rows of all passes too many");
   const zo::WsPlan plan = zo::plan_workspace(*cfg, rows, C);
   if (ws_bytes < plan.min_total)
     return fail(ZO_ENOMEM, "workspace of %zu bytes < %zu required", ws_bytes, plan.min_total);
@@ -114,15 +118,29 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
   a.tokens = tokens;
   a.mask = mask;
   a.C = C;
-  a.Lplus = Lplus;
-  a.Lminus = Lminus;
+  a.Lplus = L1;
+  a.Lminus = L2;
   a.work = (char*)workspace;
   const char* split = std::getenv("ZO_FP32_SPLIT");
-  a.fp32_split = split && split[0] == '1';
+  a.fp32_split = !fd && split && split[0] == '1';
   // the probe cache is used when the workspace has room for it
   a.zc = (zo::probe_cache_kind(*cfg) && ws_bytes >= plan.total) ? (char*)workspace + plan.zcache : nullptr;
   a.zmap = zo::make_zcache_map(*cfg);
-  return device_status(zo::launch_forward(a, (hipStream_t)stream), "zo_perturbed_losses");
+  return device_status(zo::launch_forward(a, (hipStream_t)stream), name);
+}
+
+int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                        uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                        float* Lplus, float* Lminus, void* workspace, size_t ws_bytes, void* stream) {
+  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, Lplus, Lminus, workspace, ws_bytes,
+                      stream, false, "zo_perturbed_losses");
+}
+
+int zo_fd_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N, uint32_t i0,
+                 const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C, float* L, float* L0,
+                 void* workspace, size_t ws_bytes, void* stream) {
+  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, L, L0, workspace, ws_bytes, stream,
+                      true, "zo_fd_losses");
 }
 
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
@@ -141,6 +159,24 @@ int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float
   return device_status(zo::launch_update(cfg->wdtype, cfg->probe, theta, P, seed, eps, lr, N, i0,
                                          Lplus, Lminus, skipped_out, (hipStream_t)stream),
                        "zo_update");
+}
+
+int zo_fd_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                 uint32_t i0, const float* L, const float* L0, int32_t* skipped_out, void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (!theta || !L || !L0) return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (!aligned16(theta)) return fail(ZO_EINVAL, "theta must be 16-byte aligned");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
+  if (!std::isfinite(lr)) return fail(ZO_EINVAL, "lr must be finite");
+  if (N < 1) return fail(ZO_EINVAL, "N must be >= 1");
+  if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
+    return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
+  const uint64_t P = zo::make_layout(*cfg).total;
+  // the update kernels divide by 2 eps; eps / 2 (exact in fp32) gives (L_n - L0) / eps
+  return device_status(zo::launch_update(cfg->wdtype, cfg->probe, theta, P, seed, 0.5f * eps, lr, N, i0, L,
+                                         L0, skipped_out, (hipStream_t)stream, 0),
+                       "zo_fd_update");
 }
 
 int zo_debug_probe(int32_t probe, uint64_t seed, uint32_t i, uint64_t j0, uint64_t n, float* out,

@@ -52,39 +52,65 @@ inline Layout make_layout(const zo_config& c) {
   return L;
 }
 
-// Rows of the batched forward. The 2N passes (probe n, sign s) each run the
-// B sequences; every matrix product of a timestep covers all of them at once.
-// Row r = (2 n + sidx) * Bp + b with sidx 0 for +eps and 1 for -eps; B is
-// padded to Bp (a multiple of the path's row granule) so that every row tile
-// of a kernel lies inside one probe's rows (and, for the fp32 path, every
-// 32-row wave tile inside one sign). Padded rows (b >= B) carry zeros in, are
-// computed like the others and never scored.
+// Rows of the batched forward. The passes each run the B sequences; every
+// matrix product of a timestep covers all of them at once. B is padded to Bp
+// (a multiple of the path's row granule) so that every row tile of a kernel
+// lies inside one pass (and, for central differences, one probe). Padded
+// rows (b >= B) carry zeros in, are computed like the others and never
+// scored.
+//   central differences (2N passes): row r = (2 n + sidx) Bp + b with sidx 0
+//     for theta + eps z_n and 1 for theta - eps z_n;
+//   forward differences (N + 1 passes): row r = p Bp + b, pass p < N at
+//     theta + eps z_p, pass N at theta itself (the clean pass).
 constexpr int kRowGranuleF32 = 32;   // fp32 path: 64-row tiles, 32-row wave tiles
 constexpr int kRowGranuleBF16 = 128; // bf16 path: 256-row tiles
 
-inline int row_granule(const zo_config& c) {
+inline int row_granule(const zo_config& c, bool fd = false) {
+  // forward differences: a whole row tile (64 or 256 rows) inside one pass
+  if (fd) return c.wdtype == ZO_WBF16 ? 2 * kRowGranuleBF16 : 2 * kRowGranuleF32;
   return c.wdtype == ZO_WBF16 ? kRowGranuleBF16 : kRowGranuleF32;
 }
 
 struct Rows {
   int32_t B, Bp, N;
-  int64_t pair_rows;  // 2 Bp
-  int64_t M;          // N * 2 Bp
+  int64_t pair_rows;  // rows of one probe: 2 Bp (central) or Bp (forward)
+  int64_t M;          // all rows: 2 N Bp (central) or (N + 1) Bp (forward)
+  int fd;
 };
 
 struct RowMap {
   int Bp;
   int64_t pair_rows;
+  int fd;  // forward differences
+  int N;
 };
 
-inline Rows make_rows(int32_t N, int32_t B, int granule) {
+inline Rows make_rows(int32_t N, int32_t B, int granule, bool fd = false) {
   Rows r;
   r.B = B;
   r.N = N;
+  r.fd = fd ? 1 : 0;
   r.Bp = (B + granule - 1) / granule * granule;
-  r.pair_rows = 2 * (int64_t)r.Bp;
-  r.M = (int64_t)N * r.pair_rows;
+  r.pair_rows = fd ? (int64_t)r.Bp : 2 * (int64_t)r.Bp;
+  r.M = fd ? (int64_t)(N + 1) * r.Bp : (int64_t)N * r.pair_rows;
   return r;
+}
+
+inline RowMap row_map(const Rows& r) { return RowMap{r.Bp, r.pair_rows, r.fd, r.N}; }
+
+// The pass of row r: its probe (relative index; the clean pass reports
+// probe N - 1, whose values it multiplies by 0), the sign of eps (+1, -1, or
+// 0 for the clean pass) and its sequence b.
+struct PassOf {
+  int probe;
+  int sign;
+  int b;
+};
+__host__ __device__ inline PassOf pass_of(const RowMap& m, int64_t r) {
+  const int64_t p = r / m.pair_rows;
+  const int loc = (int)(r - p * m.pair_rows);
+  if (m.fd) return PassOf{p < m.N ? (int)p : m.N - 1, p < m.N ? 1 : 0, loc};
+  return loc >= m.Bp ? PassOf{(int)p, -1, loc - m.Bp} : PassOf{(int)p, 1, loc};
 }
 
 // Time steps whose top-layer states are kept for one batched output-head pass.

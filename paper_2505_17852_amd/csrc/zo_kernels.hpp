@@ -15,9 +15,12 @@ hipError_t launch_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, flo
                                     hipStream_t s);
 hipError_t launch_init(int wdtype, void* theta, uint64_t P, uint64_t seed, float scale,
                        hipStream_t s);
+// lm_stride 1: Lm holds one loss per probe (central differences); 0: one
+// loss for all probes (forward differences: the clean pass, with eps halved
+// by the caller so that the coefficient divides by eps).
 hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t seed, float eps,
                          float lr, int32_t N, uint32_t i0, const float* Lp, const float* Lm,
-                         int32_t* skipped, hipStream_t s);
+                         int32_t* skipped, hipStream_t s, int lm_stride = 1);
 
 // k_forward.hip: one call of the perturbed forward passes.
 struct ForwardArgs {

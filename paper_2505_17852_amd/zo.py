@@ -7,7 +7,7 @@ built (paper_2505_17852_amd/build.py); there is no fallback of any kind.
 
 Function names follow the C ABI in include/zo.h:
     param_count, workspace_bytes, workspace_bytes_min, init, perturbed_losses,
-    update, debug_probe, debug_gauss_pairs
+    update, fd_losses, fd_update, debug_probe, debug_gauss_pairs
 A model configuration is a dict with the keys n_layers, vocab, embed,
 hidden, wdtype (0 fp32, 1 bf16) and probe (0 Rademacher, 1 normal).
 """
@@ -60,12 +60,17 @@ def lib():
                                           vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, vp]
         L.zo_update.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
                                 vp, vp, vp, vp]
+        L.zo_fd_losses.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
+                                   vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, vp]
+        L.zo_fd_update.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
+                                   vp, vp, vp, vp]
         L.zo_debug_probe.argtypes = [C.c_int32, C.c_uint64, C.c_uint32, C.c_uint64, C.c_uint64, vp, vp]
         L.zo_debug_gauss_pairs.argtypes = [vp, C.c_uint64, vp, vp]
         L.zo_profile_enable.argtypes = [C.c_int32]
         L.zo_profile_read.argtypes = [C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         L.zo_last_error.restype = C.c_char_p
-        for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_debug_probe",
+        for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_fd_losses", "zo_fd_update",
+                  "zo_debug_probe",
                   "zo_debug_gauss_pairs", "zo_profile_enable", "zo_profile_read"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -187,6 +192,56 @@ def update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, Lplus: to
                          _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
                          None if skipped is None else _dev(skipped, torch.int32, "skipped"),
                          _stream(stream))
+    _check(st)
+
+
+def fd_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int, tokens: torch.Tensor,
+              mask: torch.Tensor | None = None, i0: int = 0, L: torch.Tensor | None = None,
+              L0: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None,
+              check_tokens: bool = True):
+    """Forward differences: returns (L [N], L0 [1]) as device fp32 tensors
+    (asynchronous): the losses at theta + eps z_n and at theta."""
+    c = _cfg(cfg)
+    if tokens.dim() != 2:
+        raise ValueError("tokens must be [B][C+1]")
+    if check_tokens and tokens.numel():
+        lo, hi = int(tokens.min()), int(tokens.max())
+        if lo < 0 or hi >= int(cfg["vocab"]):
+            raise ValueError(f"token ids must lie in [0, {cfg['vocab']}), got [{lo}, {hi}]")
+    B, C1 = tokens.shape
+    Cn = C1 - 1
+    if mask is not None and tuple(mask.shape) != (B, Cn):
+        raise ValueError("mask must be [B][C]")
+    dev = theta.device
+    if L is None:
+        L = torch.empty(N, dtype=torch.float32, device=dev)
+    if L0 is None:
+        L0 = torch.empty(1, dtype=torch.float32, device=dev)
+    if L.numel() < N or L0.numel() < 1:
+        raise ValueError("loss buffers too small")
+    if workspace is None:
+        workspace = new_workspace(cfg, N, B, Cn, device=dev)
+    st = lib().zo_fd_losses(
+        C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, N, i0,
+        _dev(tokens, torch.int32, "tokens"),
+        None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
+        _dev(L, torch.float32, "L"), _dev(L0, torch.float32, "L0"),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st)
+    return L, L0
+
+
+def fd_update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, L: torch.Tensor,
+              L0: torch.Tensor, i0: int = 0, skipped: torch.Tensor | None = None, stream=None):
+    """In-place forward-difference update of theta (asynchronous)."""
+    c = _cfg(cfg)
+    N = L.numel()
+    if L0.numel() < 1:
+        raise ValueError("L0 must hold one loss")
+    st = lib().zo_fd_update(C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, lr, N, i0,
+                            _dev(L, torch.float32, "L"), _dev(L0, torch.float32, "L0"),
+                            None if skipped is None else _dev(skipped, torch.int32, "skipped"),
+                            _stream(stream))
     _check(st)
 
 

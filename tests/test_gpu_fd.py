@@ -1,0 +1,221 @@
+"""Forward differences (Eq. 1, the paper's FD-RGE) on the GPU, through the C
+ABI: N perturbed passes plus one clean pass batched in one forward
+(zo_fd_losses) and the update with coefficients (L_n - L0) / eps
+(zo_fd_update).
+
+Bars: the perturbed losses are bit-identical to the central difference's
+L+ of the same probes (the same rows of the same kernels); the clean loss
+and the perturbed losses within 1e-5 relative of the oracle (fp32 weights)
+or 2e-2 (bf16 weights); the updated theta to the update's own bar; and the
+appendix's identity (forward differences of z and -z against one clean loss
+give the central difference) on the GPU's own losses and updates.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from paper_2505_17852_amd import workloads as wl  # noqa: E402
+
+RTOL = {wl.FP32: 1e-5, wl.BF16: 2e-2}
+
+
+@pytest.fixture(scope="module")
+def zo():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2505_17852_amd import zo as z
+    z.lib()
+    return z
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def theta_bits(theta, cfg, dtype):
+    return theta.view(torch.int16 if cfg["wdtype"] == wl.BF16 else torch.int32).cpu().numpy().view(dtype)
+
+
+def theta_close(got, ref, cfg):
+    if cfg["wdtype"] == wl.BF16:
+        g = (got.astype(np.uint32) << 16).view(np.float32)
+        r = (ref.astype(np.uint32) << 16).view(np.float32)
+        return np.all(np.abs(g - r) <= np.abs(r) * 2.0 ** -7 + 1e-30)
+    tol = 1e-5 * np.abs(ref) + 1e-5 * np.abs(ref).mean()
+    return np.all(np.abs(got.astype(np.float64) - ref) <= tol)
+
+
+# name, model cfg, N, B, C, eps, masked
+CASES = [
+    ("c1-rad", wl.model_cfg("c1"), 8, 4, 32, 1e-2, False),
+    # 3 unit tiles (H=96), vocabulary 300 (2 full tiles + 44), padded rows (B=5),
+    # a full and a partial time chunk (C=20)
+    ("ragged-rad", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wl.FP32, probe=wl.RADEMACHER),
+     3, 5, 20, 1e-2, True),
+    ("ragged-gauss", dict(n_layers=2, vocab=300, embed=32, hidden=128, wdtype=wl.FP32, probe=wl.GAUSSIAN),
+     2, 3, 18, 1e-2, True),
+    ("bf16-rad", dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.RADEMACHER),
+     2, 5, 20, 1e-2, True),
+    ("bf16-gauss", dict(n_layers=2, vocab=200, embed=128, hidden=64, wdtype=wl.BF16, probe=wl.GAUSSIAN),
+     3, 3, 9, 1e-2, False),
+]
+
+
+@pytest.mark.parametrize("probe_cache", [True, False], ids=["cached", "min-ws"])
+@pytest.mark.parametrize("name,cfg,N,B,C,eps,masked", CASES, ids=[c[0] for c in CASES])
+def test_fd_losses(zo, oracle, name, cfg, N, B, C, eps, masked, probe_cache):
+    say(f"fd losses {name} cfg={cfg} N={N} B={B} C={C} probe_cache={probe_cache}")
+    rng = np.random.default_rng(29)
+    tok = wl.uniform_tokens(rng, B, C, cfg["vocab"])
+    mask = (rng.random((B, C)) < 0.6).astype(np.uint8) if masked else None
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 61)
+    td = torch.from_numpy(tok).cuda()
+    md = None if mask is None else torch.from_numpy(mask).cuda()
+    ws = zo.new_workspace(cfg, N, B, C, probe_cache=probe_cache)
+    L, L0 = zo.fd_losses(cfg, theta, 808, eps, N, td, md, i0=3, workspace=ws)
+    Lp, _ = zo.perturbed_losses(cfg, theta, 808, eps, N, td, md, i0=3, workspace=ws)
+    assert torch.equal(L.view(torch.int32), Lp.view(torch.int32)), (L, Lp)
+    g, g0 = L.cpu().numpy(), float(L0.item())
+    ref_theta = oracle.init(cfg, 61)
+    r, r0 = oracle.fd_losses(cfg, ref_theta, 808, eps, N, tok, mask, i0=3)
+    say(f"gpu L {g} L0 {g0}\noracle L {r} L0 {r0}")
+    tol = RTOL[cfg["wdtype"]]
+    assert abs(g0 - r0) <= tol * abs(r0)
+    assert np.all(np.abs(g - r) <= tol * np.abs(r))
+    # the clean pass carries no probe: it does not depend on the seed or eps
+    L_b, L0_b = zo.fd_losses(cfg, theta, 9, 2 * eps, N, td, md, workspace=ws)
+    assert torch.equal(L0.view(torch.int32), L0_b.view(torch.int32))
+    assert not torch.equal(L, L_b)
+
+
+UPDATE_CASES = [
+    ("c1-rad", dict(wl.model_cfg("c1")), 8, 1e-2, 1e-3),
+    ("ragged-rad-bf16", dict(n_layers=1, vocab=77, embed=32, hidden=32, wdtype=wl.BF16, probe=0), 37, 1e-3, 1e-3),
+    ("gauss-fp32", dict(n_layers=1, vocab=50, embed=32, hidden=64, wdtype=wl.FP32, probe=1), 19, 1e-2, 1e-2),
+    ("gauss-bf16", dict(n_layers=2, vocab=50, embed=32, hidden=32, wdtype=wl.BF16, probe=1), 300, 1e-3, 1e-3),
+]
+
+
+@pytest.mark.parametrize("name,cfg,N,eps,lr", UPDATE_CASES, ids=[c[0] for c in UPDATE_CASES])
+def test_fd_update_parity(zo, oracle, name, cfg, N, eps, lr):
+    say(f"fd update {name} P={zo.param_count(cfg)} N={N}")
+    rng = np.random.default_rng(13)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 5)
+    ref = oracle.init(cfg, 5)
+    L = (5.0 + rng.standard_normal(N) * 0.01).astype(np.float32)
+    L0 = np.float32(5.0)
+    zo.fd_update(cfg, theta, 99, eps, lr, torch.from_numpy(L).cuda(),
+                 torch.tensor([L0], dtype=torch.float32, device="cuda"), i0=3)
+    got = theta_bits(theta, cfg, ref.dtype)
+    assert oracle.fd_update(cfg, ref, 99, eps, lr, L, L0, i0=3) == 0
+    assert theta_close(got, ref, cfg)
+
+
+def test_fd_update_nonfinite_skips(zo):
+    cfg = dict(wl.model_cfg("c1"))
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 3)
+    before = theta.clone()
+    L = torch.full((6,), 3.0, dtype=torch.float32, device="cuda")
+    L0 = torch.tensor([float("nan")], dtype=torch.float32, device="cuda")
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    zo.fd_update(cfg, theta, 1, 1e-2, 1e-3, L, L0, skipped=flag)
+    assert flag.item() == 1
+    assert torch.equal(theta.view(torch.int32), before.view(torch.int32))
+    L0[0] = 2.5
+    L[4] = float("inf")
+    zo.fd_update(cfg, theta, 1, 1e-2, 1e-3, L, L0, skipped=flag)
+    assert flag.item() == 1
+    assert torch.equal(theta.view(torch.int32), before.view(torch.int32))
+    L[4] = 3.0
+    zo.fd_update(cfg, theta, 1, 1e-2, 1e-3, L, L0, skipped=flag)
+    assert flag.item() == 0
+    assert not torch.equal(theta.view(torch.int32), before.view(torch.int32))
+
+
+@pytest.mark.parametrize("probe", [wl.RADEMACHER, wl.GAUSSIAN], ids=["rademacher", "gaussian"])
+def test_antithetic_forward_equals_central(zo, probe):
+    """The appendix's identity on the GPU's own numbers: the forward
+    differences of z and -z against one clean loss average to the central
+    difference. The -z losses are those of the central pass (L-); the update
+    the antithetic estimator implies is two half-rate forward-difference
+    updates, the second with losses 2 L0 - L- (so that its coefficient is
+    (L0 - L-) / eps = -(L- - L0) / eps, the probe -z's term), and it matches
+    the central update up to the two extra roundings of theta."""
+    cfg = dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wl.FP32, probe=probe)
+    N, B, C, eps, lr = 4, 5, 12, 1e-2, 0.5
+    rng = np.random.default_rng(31)
+    td = torch.from_numpy(wl.uniform_tokens(rng, B, C, cfg["vocab"])).cuda()
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 8)
+    L, L0 = zo.fd_losses(cfg, theta, 4040, eps, N, td)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 4040, eps, N, td)
+    assert torch.equal(L, Lp)
+    mirrored = (2.0 * L0.double() - Lm.double()).float()
+    t_fd = theta.clone()
+    zo.fd_update(cfg, t_fd, 4040, eps, lr / 2, L, L0)
+    zo.fd_update(cfg, t_fd, 4040, eps, lr / 2, mirrored, L0)
+    t_cd = theta.clone()
+    zo.update(cfg, t_cd, 4040, eps, lr, Lp, Lm)
+    th = theta.double().cpu().numpy()
+    a, b = t_fd.double().cpu().numpy(), t_cd.double().cpu().numpy()
+    step = np.abs(b - th)
+    say(f"largest step {step.max():.3e}, largest fd-as/cd gap {np.abs(a - b).max():.3e}")
+    assert step.max() > 0
+    zmax = 1.0 if probe == wl.RADEMACHER else 6.0
+    e = float(np.float32(eps))
+    tol = 4 * np.spacing(np.float32(np.abs(th).max())) + step * 1e-5 + \
+        lr / 2 * float(np.spacing(np.float32(2 * float(L0.item())))) / e * zmax
+    assert np.all(np.abs(a - b) <= tol)
+
+
+def test_fd_training_steps_match_oracle(zo, oracle):
+    """Four forward-difference steps of the c1 shape (fp32): per-step clean
+    losses within 1e-5 relative of the oracle's and theta after the four
+    steps within the update's bar (the oracle runs its own trajectory)."""
+    from paper_2505_17852_amd import train
+    cfg = wl.model_cfg("c1")
+    w = wl.CONFIGS["c1"]
+    tok, _ = wl.batch("c1")
+    steps, seed0 = 4, 900
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 23)
+    hist = train.train(cfg, theta, torch.from_numpy(tok).cuda(), None, N=w["N"], eps=w["eps"], lr=w["lr"],
+                       steps=steps, seed0=seed0, estimator="fd").numpy()
+    ref = oracle.init(cfg, 23)
+    ref_hist = []
+    for k in range(steps):
+        L, L0 = oracle.fd_losses(cfg, ref, seed0 + k, w["eps"], w["N"], tok)
+        ref_hist.append(L0)
+        assert oracle.fd_update(cfg, ref, seed0 + k, w["eps"], w["lr"], L.astype(np.float32), np.float32(L0)) == 0
+    ref_hist = np.array(ref_hist)
+    say(f"gpu {hist}\noracle {ref_hist}")
+    assert np.all(np.abs(hist - ref_hist) <= 1e-5 * np.abs(ref_hist))
+    got = theta.cpu().numpy()
+    tol = 1e-5 * np.abs(ref) + 1e-5 * np.abs(ref).mean()
+    assert np.all(np.abs(got.astype(np.float64) - ref) <= tol)
+
+
+def test_fd_training_lowers_the_loss(zo):
+    """300 forward-difference steps on one fixed batch (the setting of the
+    central-difference convergence test: 1 layer, V=64, E=32, H=64, fp32;
+    B=8, C=32; N=64, eps=1e-2, lr=0.3, Rademacher probes): the clean loss
+    falls by more than 0.05 nats and the last 50-step window lies below the
+    first."""
+    from paper_2505_17852_amd import train
+    cfg = dict(n_layers=1, vocab=64, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.RADEMACHER)
+    tok = wl.uniform_tokens(np.random.default_rng(5), 8, 32, 64)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 11)
+    hist = train.train(cfg, theta, torch.from_numpy(tok).cuda(), None, N=64, eps=1e-2, lr=0.3,
+                       steps=300, seed0=100, estimator="fd").numpy()
+    say(f"loss: first {hist[:3]}, last {hist[-3:]}")
+    assert np.all(np.isfinite(hist))
+    assert hist[-20:].mean() < hist[:20].mean() - 0.05
+    win = hist.reshape(6, 50).mean(axis=1)
+    assert win[-1] < win[0]

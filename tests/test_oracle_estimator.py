@@ -172,3 +172,110 @@ def test_one_step_descends_on_tiny_lstm(oracle):
     assert oracle.update(cfg, t, 55, 1e-3, 0.2, lp, lm) == 0
     L1 = oracle.lstm_loss(cfg, t.astype(np.float64), tokens)
     assert L1 < L0
+
+
+# ---------------------------------------------------------------------------
+# Forward differences (Eq. 1) and the antithetic forward estimator of the
+# appendix that proves it equal to the central difference.
+
+def test_fd_losses_are_the_clean_and_the_plus_losses(oracle):
+    """L_n is the loss at theta + eps z_n, the same number the central
+    difference's L+ is; L0 is the plain loss of theta (no probe)."""
+    cfg = wl.model_cfg("c1")
+    th = oracle.init(cfg, 2003)
+    tokens, mask = wl.batch("c1", B=2, C=6)
+    L, L0 = oracle.fd_losses(cfg, th, 3003, 1e-2, 3, tokens, mask, i0=2)
+    lp, _ = oracle.perturbed_losses(cfg, th, 3003, 1e-2, 3, tokens, mask, i0=2, as_double=True)
+    assert np.array_equal(L, lp)
+    assert L0 == oracle.lstm_loss(cfg, th.astype(np.float64), tokens, mask)
+
+
+def test_fd_bias_is_first_order(oracle):
+    """Eq. 3: the forward difference errs at O(eps), by eps/2 z^T H z to
+    leading order, while the central difference (Eq. 5) errs at O(eps^2).
+    On the tiny LSTM the curvature term (L+ + L- - 2 L0) / (2 eps) is the
+    forward difference's error against the central one; it shrinks tenfold
+    when eps does."""
+    cfg = dict(TINY)
+    th = oracle.init(cfg, 41)
+    tokens = np.random.default_rng(6).integers(0, 8, size=(2, 5)).astype(np.int32)
+    curv = {}
+    for eps in (1e-2, 1e-3):
+        L, L0 = oracle.fd_losses(cfg, th, 8, eps, 4, tokens)
+        lp, lm = oracle.perturbed_losses(cfg, th, 8, eps, 4, tokens, as_double=True)
+        e = float(np.float32(eps))
+        fd = (L - L0) / e
+        cd = (lp - lm) / (2 * e)
+        curv[eps] = fd - cd
+        np.testing.assert_allclose(curv[eps], (lp + lm - 2 * L0) / (2 * e), rtol=1e-9, atol=1e-12)
+    assert np.all(np.abs(curv[1e-2]) > 1e-6)
+    ratio = curv[1e-2] / curv[1e-3]
+    assert np.all((ratio > 9.0) & (ratio < 11.0)), ratio
+
+
+def test_fd_update_closed_forms(oracle):
+    cfg = dict(TINY)
+    th = oracle.init(cfg, 43)
+    P = th.size
+    # L_n == L0: theta bit-identical
+    t = th.copy()
+    assert oracle.fd_update(cfg, t, 5, 1e-3, 1e-3, np.full(3, 2.5, np.float32), 2.5) == 0
+    assert np.array_equal(t, th)
+    # N = 1: theta_j - c z_j with c = lr (L - L0) / eps, one rounding
+    L, L0 = np.float32(3.25), np.float32(3.0)
+    c = oracle.fd_update_coeff(0.01, 1, L, L0, 1e-3)
+    assert c == np.float32(float(np.float32(0.01)) * ((float(L) - float(L0)) / float(np.float32(1e-3))))
+    t = th.copy()
+    assert oracle.fd_update(cfg, t, 5, 1e-3, 0.01, np.array([L]), L0) == 0
+    z = oracle.probe(0, 5, 0, 0, P).astype(np.float64)
+    assert np.array_equal(t, (th.astype(np.float64) - float(c) * z).astype(np.float32))
+    # one-sided: with L0 = L- the coefficient is twice the central one
+    for N in (1, 5):
+        cf = oracle.fd_update_coeff(1e-3, N, np.float32(5.0), np.float32(4.5), 1e-3)
+        cc = oracle.update_coeff(1e-3, N, np.float32(5.0), np.float32(4.5), 1e-3)
+        assert abs(cf - 2 * cc) <= 2 * np.spacing(np.float32(cf))
+    # a non-finite clean or perturbed loss skips the step
+    t = th.copy()
+    assert oracle.fd_update(cfg, t, 1, 1e-3, 1e-3, np.array([1.0], np.float32), np.nan) == -5
+    assert oracle.fd_update(cfg, t, 1, 1e-3, 1e-3, np.array([1.0, np.inf], np.float32), 1.0) == -5
+    assert np.array_equal(t, th)
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_antithetic_forward_equals_central(oracle, kind):
+    """The appendix's identity: averaging the forward differences of z and
+    -z against the same clean loss gives the central difference. The
+    antithetic estimate is assembled from the oracle's forward-difference
+    pieces (its L_n at +z, its clean L0, and the loss at -z), and the update
+    it implies is two half-rate forward-difference updates, the second with
+    losses 2 L0 - L- standing for the losses at -z (L(-z) - L0 = L0 - (2 L0 - L(-z))
+    flips the sign the way the probe -z does). Both match the central
+    difference's estimate and update."""
+    cfg = dict(TINY, probe=kind)
+    th = oracle.init(cfg, 47)
+    P = th.size
+    tokens = np.random.default_rng(9).integers(0, 8, size=(2, 5)).astype(np.int32)
+    N, eps, lr, seed = 6, 1e-2, 0.5, 71
+    L, L0 = oracle.fd_losses(cfg, th, seed, eps, N, tokens)
+    lp, lm = oracle.perturbed_losses(cfg, th, seed, eps, N, tokens, as_double=True)
+    e = float(np.float32(eps))
+    zs = np.stack([oracle.probe(kind, seed, i, 0, P).astype(np.float64) for i in range(N)])
+    g_fdas = (0.5 * ((L - L0) / e - (lm - L0) / e)) @ zs / N
+    g_cd = oracle.cd_gradient(P, kind, seed, e, lp, lm)
+    np.testing.assert_allclose(g_fdas, g_cd, rtol=1e-9, atol=1e-12 * np.abs(g_cd).max())
+    # the update
+    Lf = L.astype(np.float32)
+    Lm32 = lm.astype(np.float32)
+    L032 = np.float32(L0)
+    mirrored = (2.0 * L032.astype(np.float64) - Lm32.astype(np.float64)).astype(np.float32)
+    t_fd = th.copy()
+    assert oracle.fd_update(cfg, t_fd, seed, eps, lr / 2, Lf, L032) == 0
+    assert oracle.fd_update(cfg, t_fd, seed, eps, lr / 2, mirrored, L032) == 0
+    t_cd = th.copy()
+    assert oracle.update(cfg, t_cd, seed, eps, lr, Lf, Lm32) == 0
+    step = np.abs(t_cd.astype(np.float64) - th)
+    assert step.max() > 0
+    # roundings: the mirrored losses (one fp32 ulp of 2 L0) and two theta stores
+    tol = 4 * np.spacing(np.float32(np.abs(th).max())) + step * 1e-5 + \
+        lr / 2 * np.spacing(np.float32(2 * L0)) / e * np.abs(zs).max()
+    assert np.all(np.abs(t_fd.astype(np.float64) - t_cd) <= tol)
