@@ -150,6 +150,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="c4", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seq-len", type=int, default=None,
+                    help="profiling runs only: score the first C positions of each sequence "
+                         "(every gate launch keeps the workload's full shape; the JSON line "
+                         "then names the shortened C)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one 1 GiB device-to-device copy and exit (the reference kernel "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     ap.add_argument("--estimator", default="cd", choices=["cd", "fd"],
                     help="cd: central differences, 2N passes (default); fd: forward "
                          "differences, N perturbed passes and one clean pass")
@@ -170,6 +177,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     zo.lib()  # fails loudly if the HIP library is not built
+    if args.calibrate_copy:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print("[bench] copied 1 GiB device to device", file=sys.stderr, flush=True)
+        return
     name = args.workload
     W_def, K_def = DEFAULTS[name]
     W = W_def if args.warmup is None else args.warmup
@@ -179,6 +193,11 @@ def main():
     sd = wl.seeds(name)
     N, eps, lr = w["N"], w["eps"], w["lr"]
     tokens, mask = wl.batch(name)
+    if args.seq_len is not None:
+        if not 1 <= args.seq_len <= tokens.shape[1] - 1:
+            raise SystemExit(f"--seq-len must lie in [1, {tokens.shape[1] - 1}]")
+        tokens = np.ascontiguousarray(tokens[:, :args.seq_len + 1])
+        mask = None if mask is None else np.ascontiguousarray(mask[:, :args.seq_len])
     B, C = tokens.shape[0], tokens.shape[1] - 1
     dev = torch.device("cuda:0")
     theta = zo.new_theta(cfg, dev)
