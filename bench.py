@@ -104,6 +104,33 @@ def embed_hbm(cfg, passes, B, w, emb, fd=False):
     return {"bytes_per_launch": byt, "ms_per_launch": ms / n, "GBps": gbps, "frac": gbps / HBM_PEAK_GBPS}
 
 
+def stream_limit(name, reps=10):
+    """The streaming rate of the update's access pattern without its
+    arithmetic: torch's in-place bitwise xor with 0 over the workload's
+    theta bytes (read and written once per launch), HIP events over `reps`
+    launches after two warm-up launches."""
+    import torch
+    from paper_2505_17852_amd import workloads as wl
+    from paper_2505_17852_amd import zo
+    cfg = wl.model_cfg(name)
+    w = 2 if cfg["wdtype"] == wl.BF16 else 4
+    nbytes = zo.param_count(cfg) * w
+    buf = torch.zeros(nbytes // 16, 4, dtype=torch.int32, device="cuda:0")
+    for _ in range(2):
+        buf.bitwise_xor_(0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        buf.bitwise_xor_(0)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    byt = 2 * buf.numel() * 4
+    return {"stream_limit": name, "bytes_per_launch": byt, "ms_per_launch": ms,
+            "GBps": byt / (ms * 1e-3) / 1e9, "frac_of_hbm_peak": byt / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+
+
 def cpu_baseline(name, budget_s=20.0, fd=False):
     """The oracle on the host cores, on a bounded sample of the workload:
     the full batch with the first N' probes (N' doubling until the budget is
@@ -157,6 +184,9 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 1 GiB device-to-device copy and exit (the reference kernel "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes)")
+    ap.add_argument("--calibrate-stream", action="store_true",
+                    help="time an in-place read-modify-write of the workload's theta bytes "
+                         "(the update's access pattern without its arithmetic) and exit")
     ap.add_argument("--estimator", default="cd", choices=["cd", "fd"],
                     help="cd: central differences, 2N passes (default); fd: forward "
                          "differences, N perturbed passes and one clean pass")
@@ -183,6 +213,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print("[bench] copied 1 GiB device to device", file=sys.stderr, flush=True)
+        return
+    if args.calibrate_stream:
+        print(json.dumps(stream_limit(args.workload)), flush=True)
         return
     name = args.workload
     W_def, K_def = DEFAULTS[name]
