@@ -28,7 +28,7 @@ METRIC = "perturbed-forward tokens/sec per CD-RGE step (2N·B·C/s); % MFMA peak
 METRIC_FD = "forward tokens/sec per FD-RGE step ((N+1)·B·C/s); % MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
 HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
-DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 1), "c4": (1, 1), "c5": (1, 3)}
+DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 3), "c4": (1, 3), "c5": (1, 3)}
 DESCRIPTION = {
     "c1": "1-layer LSTM V=256 E=32 H=64 fp32; B=4 C=32 uniform tokens; N=8 Rademacher",
     "c2": "2-layer LSTM V=256 E=128 H=256 fp32; B=64 C=256 REVERSE transduction (loss on "
