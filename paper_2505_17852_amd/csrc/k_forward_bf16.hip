@@ -11,21 +11,23 @@
 // The probe term is formed exactly apart from the bf16 rounding of eps z
 // (relative 2^-9), and accumulates in fp32 next to A . W.
 //
-// Tiles: a workgroup of 8 waves computes TM = 256 rows x TN columns with K
-// tiles of 64: TN = 256 with sign probes (waves 2 x 4, wave tiles 128 x 64),
-// TN = 128 with normal probes (waves 4 x 2, wave tiles 64 x 64; the probe
-// tile then needs LDS of its own). A wave tile is MT x 2 tiles of
-// v_mfma_f32_32x32x16_bf16 (MT = 4 or 2); two waves share each SIMD, so one
-// wave's LDS reads, probe expansion and address work run under the other's
-// matrix instructions. Lane l feeds row/column l % 32 and k block l / 32.
+// Tiles: a workgroup of 8 waves computes TM = 256 rows x TN = 256 columns
+// (waves 2 x 4, wave tiles 128 x 64 = 4 x 2 tiles of
+// v_mfma_f32_32x32x16_bf16); two waves share each SIMD, so one wave's LDS
+// reads, probe expansion and address work run under the other's matrix
+// instructions. Lane l feeds row/column l % 32 and k block l / 32.
 //
-// LDS (static, two stages, one barrier per K tile): per stage the
-// activation tile [TM][64] and the weight tile [TN][64] (bf16, 128-byte rows,
-// 16-byte chunks XOR-swizzled by row), copied from global memory straight
-// into LDS without passing through registers, and the probe tile: sign bits
-// [TN][2] words, expanded to bf16 +-eps by each wave, or bf16(eps z) [TN][64]
-// (swizzled like the weights), generated in registers. The next K tile's
-// copies and probe tile are issued before the current tile's MFMAs.
+// LDS (static, one barrier per K tile): per stage the activation tile
+// [TM][TK] and the weight tile [TN][TK] (bf16 rows of 2 TK bytes whose
+// 16-byte chunks are XOR-swizzled by row), copied from global memory straight
+// into LDS without passing through registers, and the probe tile. Sign
+// probes: K tiles of 64 in two stages, the probe tile as sign bits [TN][2]
+// words expanded to bf16 +-eps by each wave. Normal probes: the probe tile is
+// bf16(eps z) [TN][TK], copied from the probe cache like the weights or
+// generated in registers, which takes a third of the stage; K tiles of 32 in
+// three stages (3 x 48 KB) keep the 256 x 256 tile and so copy 48 KB per 16.8
+// MFLOP of matrix work instead of 64 KB with 256 x 128 tiles of 64. K tile
+// it + STAGES - 1 (copies and probe tile) is issued during the MFMAs of tile it.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -41,60 +43,77 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int TK = 64;          // K per tile
 constexpr int TM = 256;         // rows per workgroup
 constexpr int NWAVES = 8;
 constexpr int NT = 64 * NWAVES;  // threads per workgroup
-constexpr int kRowBytes = TK * 2;
-constexpr int kABytes = TM * kRowBytes;
 // Global->LDS copies: each copy instruction moves 1 KB (64 lanes x 16 B).
 // kCopyWaves of the 8 waves issue them, spread over the first kCopySteps k
 // steps of the previous K tile.
 constexpr int kCopyWaves = 4;
 constexpr int kCopySteps = 1;
-constexpr int kACopies = kABytes / 1024 / kCopyWaves;  // activation copies per copying wave
 
-// Per probe kind: workgroup columns, wave grid, MFMA tiles per wave, LDS.
+// Per probe kind: K tile, stages, LDS layout, copy split, probe roles.
 template <int kind>
 struct Tiles {
-  static constexpr int TN = kind == ZO_RADEMACHER ? kVocabTileWide : kVocabTile;
+  static constexpr bool kSigns = kind == ZO_RADEMACHER;
+  static constexpr int TK = kSigns ? 64 : 32;       // K per tile
+  static constexpr int STAGES = kSigns ? 2 : 3;     // LDS stages
+  static constexpr int RowBytes = TK * 2;           // one LDS row: TK bf16
+  static constexpr int CPR = RowBytes / 16;         // 16-byte chunks per row
+  static constexpr int RPB = 256 / RowBytes;        // rows per 256 bytes (every LDS bank once)
+  static constexpr int RPC = 1024 / RowBytes;       // rows per 1 KB copy
+  static constexpr int ABytes = TM * RowBytes;
+  static constexpr int TN = kVocabTileWide;
   static constexpr int WAVES_N = TN / 64;  // wave tiles are 64 columns wide
   static constexpr int WAVES_M = NWAVES / WAVES_N;
   static constexpr int WROWS = TM / WAVES_M;  // rows per wave tile
   static constexpr int MT = WROWS / 32;
-  static constexpr int WBytes = TN * kRowBytes;
-  static constexpr int ZBytes = kind == ZO_RADEMACHER ? TN * 8 : TN * kRowBytes;
+  static constexpr int WBytes = TN * RowBytes;
+  static constexpr int ZBytes = kSigns ? TN * 8 : TN * RowBytes;
+  static constexpr int StageBytes = ABytes + WBytes + (kSigns ? 0 : ZBytes);  // sign bits: own arrays
+  static constexpr int ACopies = ABytes / 1024 / kCopyWaves;  // activation copies per copying wave
   static constexpr int WCopies = WBytes / 1024 / kCopyWaves;  // weight copies per copying wave
   // cached normal probes: the probe tile is copied like the weight tile
   static constexpr int ZCopies = kind == kGaussCached ? WCopies : 0;
-  static constexpr int Copies = kACopies + WCopies + ZCopies;
+  static constexpr int Copies = ACopies + WCopies + ZCopies;
   static constexpr int ZROW_T = NT / TN;     // threads per probe-tile row (normal probes)
   static constexpr int ZVALS = TK / ZROW_T;  // probe values per thread and K tile (normal probes)
+  // 16-byte slot of chunk c in LDS row r: c ^ swz(r). Any RPB consecutive rows
+  // cover the 64 banks once per chunk, and swz gives the CPR groups of RPB rows
+  // among 16 consecutive rows distinct chunks, so the 16 rows of one 128-bit
+  // fragment read (same chunk) hit every bank exactly once.
+  __device__ static __forceinline__ int swz(int r) { return (r / RPB) & (CPR - 1); }
+  static_assert(RPB * CPR == 16, "swizzle period of 16 rows");
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
-  static_assert(WCopies * kCopyWaves * 1024 == WBytes && kACopies * kCopyWaves * 1024 == kABytes,
+  static_assert(WCopies * kCopyWaves * 1024 == WBytes && ACopies * kCopyWaves * 1024 == ABytes,
                 "copy split");
-  static_assert(kind != ZO_RADEMACHER || TN * 2 == NT, "one sign word per thread");
-  static_assert(kind == ZO_RADEMACHER || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
+  static_assert(Copies < 64, "outstanding copies fit the vmcnt counter");
+  static_assert(!kSigns || TN * 2 == NT, "one sign word per thread");
+  static_assert(kSigns || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
+  static_assert(TK % 16 == 0 && (TK / 16 == 4 || TK / 16 == 2), "k steps per tile");
 };
 static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole number of row tiles");
+static_assert(Tiles<kGaussCached>::StageBytes == Tiles<ZO_GAUSSIAN>::StageBytes, "normal-probe stages");
 
-// Two LDS stages per probe kind (static, so that every offset is a constant).
-__shared__ __align__(16) uint8_t lds_r0[kABytes + Tiles<ZO_RADEMACHER>::WBytes];
-__shared__ __align__(16) uint8_t lds_r1[kABytes + Tiles<ZO_RADEMACHER>::WBytes];
+// LDS stages per probe kind (static, so that every offset is a constant).
+__shared__ __align__(16) uint8_t lds_r0[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_r1[Tiles<ZO_RADEMACHER>::StageBytes];
 __shared__ __align__(16) uint32_t lds_b0[Tiles<ZO_RADEMACHER>::ZBytes / 4];
 __shared__ __align__(16) uint32_t lds_b1[Tiles<ZO_RADEMACHER>::ZBytes / 4];
-__shared__ __align__(16) uint8_t lds_g0[kABytes + Tiles<ZO_GAUSSIAN>::WBytes + Tiles<ZO_GAUSSIAN>::ZBytes];
-__shared__ __align__(16) uint8_t lds_g1[kABytes + Tiles<ZO_GAUSSIAN>::WBytes + Tiles<ZO_GAUSSIAN>::ZBytes];
-static_assert(2 * (sizeof(lds_r0) + sizeof(lds_b0)) <= 160 * 1024, "LDS");
-static_assert(2 * sizeof(lds_g0) <= 160 * 1024, "LDS");
+__shared__ __align__(16) uint8_t lds_g0[Tiles<ZO_GAUSSIAN>::StageBytes];
+__shared__ __align__(16) uint8_t lds_g1[Tiles<ZO_GAUSSIAN>::StageBytes];
+__shared__ __align__(16) uint8_t lds_g2[Tiles<ZO_GAUSSIAN>::StageBytes];
+static_assert(Tiles<ZO_RADEMACHER>::STAGES * (sizeof(lds_r0) + sizeof(lds_b0)) <= 160 * 1024, "LDS");
+static_assert(Tiles<ZO_GAUSSIAN>::STAGES * sizeof(lds_g0) <= 160 * 1024, "LDS");
 
 template <int kind, int S>
 __device__ __forceinline__ uint8_t* stage() {
+  static_assert(S >= 0 && S < Tiles<kind>::STAGES, "stage index");
   if constexpr (kind == ZO_RADEMACHER)
     return S == 0 ? lds_r0 : lds_r1;
   else
-    return S == 0 ? lds_g0 : lds_g1;
+    return S == 0 ? lds_g0 : S == 1 ? lds_g1 : lds_g2;
 }
 template <int S>
 __device__ __forceinline__ uint32_t* sign_bits() {
@@ -136,13 +155,16 @@ __device__ __forceinline__ void copy_to_lds(const void* src, uint8_t* lds) {
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
 }
 
-// Wait until this thread's global->LDS copies and LDS writes are complete
-// (s_waitcnt vmcnt(0) lgkmcnt(0)), then a workgroup barrier without a memory
-// fence. The empty asm statements keep the compiler from moving memory
-// accesses across either.
+// Wait until at most VM of this thread's global->LDS copies are outstanding
+// and its LDS accesses are complete (s_waitcnt vmcnt(VM) lgkmcnt(0); the gfx9
+// encoding splits vmcnt into bits 3:0 and 15:14, expcnt 7 = no wait), then a
+// workgroup barrier without a memory fence. The empty asm statements keep the
+// compiler from moving memory accesses across either.
+template <int VM>
 __device__ __forceinline__ void wait_and_barrier() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt");
   asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0x70);
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | 0x70);
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
@@ -178,25 +200,26 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
+  constexpr int TK = T::TK;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
 
-  // copy roles: copy q of copying wave w fills rows 8 (q kCopyWaves + w) .. +7 of the
-  // activation (q < kACopies) or weight tile, 1 KB lane-linear in LDS: lane
-  // L writes row + L / 8, slot L % 8, which holds chunk (L % 8) ^ ((row >> 1) & 7)
-  const int crow = lane >> 3;
-  int arow[kACopies], wrow[T::WCopies];
-  uint32_t aoff[kACopies], woff[T::WCopies];  // element offsets of the chunk inside the row
+  // copy roles: copy q of copying wave w fills rows RPC (q kCopyWaves + w) .. +RPC-1
+  // of the activation (q < ACopies) or weight tile, 1 KB lane-linear in LDS:
+  // lane L writes row + L / CPR, slot L % CPR, which holds chunk (L % CPR) ^ swz(row)
+  const int crow = lane / T::CPR;
+  int arow[T::ACopies], wrow[T::WCopies];
+  uint32_t aoff[T::ACopies], woff[T::WCopies];  // element offsets of the chunk inside the row
 #pragma unroll
-  for (int q = 0; q < kACopies; ++q) {
-    const int r = 8 * (q * kCopyWaves + wave % kCopyWaves) + crow;
+  for (int q = 0; q < T::ACopies; ++q) {
+    const int r = T::RPC * (q * kCopyWaves + wave % kCopyWaves) + crow;
     arow[q] = r;
-    aoff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+    aoff[q] = 8u * (uint32_t)((lane % T::CPR) ^ T::swz(r));
   }
 #pragma unroll
   for (int q = 0; q < T::WCopies; ++q) {
-    const int r = 8 * (q * kCopyWaves + wave % kCopyWaves) + crow;
+    const int r = T::RPC * (q * kCopyWaves + wave % kCopyWaves) + crow;
     colmap(r, wrow[q]);
-    woff[q] = 8u * (uint32_t)((lane & 7) ^ ((r >> 1) & 7));
+    woff[q] = 8u * (uint32_t)((lane % T::CPR) ^ T::swz(r));
   }
   // probe roles: signs, every thread: row t >> 1, one 32-k word at 32 (t & 1);
   //              normal, every thread: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
@@ -221,16 +244,16 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     if (wave < kCopyWaves) {
 #pragma unroll
       for (int c = P * T::Copies / kCopySteps; c < (P < kCopySteps ? (P + 1) * T::Copies / kCopySteps : 0); ++c) {
-        if (c < kACopies) {
+        if (c < T::ACopies) {
           copy_to_lds(sg.A + (int64_t)arow[c] * sg.lda + k0 + aoff[c], base + (c * kCopyWaves + wave) * 1024);
-        } else if (c < kACopies + T::WCopies) {
-          const int q = c - kACopies;
+        } else if (c < T::ACopies + T::WCopies) {
+          const int q = c - T::ACopies;
           copy_to_lds(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
-                      base + kABytes + (q * kCopyWaves + wave) * 1024);
+                      base + T::ABytes + (q * kCopyWaves + wave) * 1024);
         } else {  // cached probe rows: the same rows and chunk order as the weight copy q
-          const int q = c - kACopies - T::WCopies;
+          const int q = c - T::ACopies - T::WCopies;
           copy_to_lds(sg.Z + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
-                      base + kABytes + T::WBytes + (q * kCopyWaves + wave) * 1024);
+                      base + T::ABytes + T::WBytes + (q * kCopyWaves + wave) * 1024);
         }
       }
     }
@@ -249,14 +272,14 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       sign_bits<S>()[zr * 2 + zpart] = unshuffle_bits(~word);
     } else if constexpr (P == 2 && kind == ZO_GAUSSIAN) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
-      uint8_t* zrow = base + kABytes + T::WBytes + zr * kRowBytes;
+      uint8_t* zrow = base + T::ABytes + T::WBytes + zr * T::RowBytes;
 #pragma unroll
       for (int q = 0; q < T::ZVALS / 8; ++q) {
         float za[4], zb[4];
         gauss_block(key, probe, (j0 >> 2) + 2 * q, za);
         gauss_block(key, probe, (j0 >> 2) + 2 * q + 1, zb);
         const int chunk = (T::ZVALS / 8) * zpart + q;
-        *(u4*)(zrow + 16 * (chunk ^ ((zr >> 1) & 7))) =
+        *(u4*)(zrow + 16 * (chunk ^ T::swz(zr))) =
             u4{pack_bf16x2(eps * za[0], eps * za[1]), pack_bf16x2(eps * za[2], eps * za[3]),
                pack_bf16x2(eps * zb[0], eps * zb[1]), pack_bf16x2(eps * zb[2], eps * zb[3])};
       }
@@ -280,11 +303,11 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // probe values (2 column tiles). The next step's LDS reads and sign
   // expansion are issued between the current step's MFMAs (software
   // pipelining within the K tile). Lane (lr, lg) reads chunk 2 s + lg of its
-  // rows, in slot (2 s) ^ y with y = lg ^ ((lr >> 1) & 7) (every row offset
-  // below is a multiple of 16).
-  const uint32_t y = (uint32_t)(lg ^ ((lr >> 1) & 7));
-  const uint32_t a_lane = (uint32_t)(T::WROWS * wm + lr) * kRowBytes;
-  const uint32_t w_lane = (uint32_t)(64 * wn + lr) * kRowBytes;
+  // rows, in slot (2 s) ^ y with y = lg ^ swz(lr) (every row offset below is
+  // a multiple of 16, the swizzle period).
+  const uint32_t y = (uint32_t)(lg ^ T::swz(lr));
+  const uint32_t a_lane = (uint32_t)(T::WROWS * wm + lr) * T::RowBytes;
+  const uint32_t w_lane = (uint32_t)(64 * wn + lr) * T::RowBytes;
   // the pair (s eps, s eps) in bf16 (signs), or the sign flip of -eps rows (normal)
   const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
   const bool neg = sgn < 0;
@@ -298,7 +321,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     constexpr int S = decltype(stage_tag)::value;
     const uint8_t* base = stage<kind, S>();
     const uint8_t* pa = base + a_lane;
-    const uint8_t* pw = base + kABytes + w_lane;
+    const uint8_t* pw = base + T::ABytes + w_lane;
     // per lane, the flags of its k block pre-shifted so that a constant shift
     // per (k step, pair) brings them to bits 15 / 31 (see unshuffle_bits)
     uint32_t bits[2][2];
@@ -314,10 +337,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     auto load = [&](int s, Frag& f) {
       const uint32_t so = 16u * ((uint32_t)(2 * s) ^ y);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * kRowBytes + so));
+      for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * T::RowBytes + so));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * kRowBytes + so));
+        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * T::RowBytes + so));
         u4 v;
         if constexpr (kind == ZO_RADEMACHER) {
           const uint32_t x = bits[nt][s >> 1];
@@ -327,7 +350,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
             if constexpr (kFD) v[d] &= zmask;
           }
         } else {
-          v = *(const u4*)(pw + T::WBytes + 32 * nt * kRowBytes + so);
+          v = *(const u4*)(pw + T::WBytes + 32 * nt * T::RowBytes + so);
 #pragma unroll
           for (int d = 0; d < 4; ++d) {
             v[d] ^= zc;
@@ -358,11 +381,23 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
           acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.z[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
                                : __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
       if (more) {
-        constexpr std::integral_constant<int, 1 - S> next{};
-        if (s == 0) issue(next, std::integral_constant<int, 0>{});
-        if (s == 1) issue(next, std::integral_constant<int, 1>{});
-        if (s == 2) issue(next, std::integral_constant<int, 2>{});
-        if (s == 3) issue(next, std::integral_constant<int, 3>{});
+        // tile it + STAGES - 1 goes to the stage tile it - 1 used
+        constexpr std::integral_constant<int, (S + T::STAGES - 1) % T::STAGES> next{};
+        if constexpr (TK / 16 == 4) {
+          if (s == 0) issue(next, std::integral_constant<int, 0>{});
+          if (s == 1) issue(next, std::integral_constant<int, 1>{});
+          if (s == 2) issue(next, std::integral_constant<int, 2>{});
+          if (s == 3) issue(next, std::integral_constant<int, 3>{});
+        } else {
+          if (s == 0) {
+            issue(next, std::integral_constant<int, 0>{});
+            issue(next, std::integral_constant<int, 1>{});
+          }
+          if (s == 1) {
+            issue(next, std::integral_constant<int, 2>{});
+            issue(next, std::integral_constant<int, 3>{});
+          }
+        }
       }
       if (s + 1 < TK / 16) {
         // per step: the next step's LDS reads first, then each MFMA followed by
@@ -377,18 +412,30 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     }
   };
 
-  // K tile it lives in stage it % 2. Per tile: wait for this thread's copies
-  // and LDS writes of tile it; barrier (tile it complete for every wave, and
-  // the other stage, computed at it - 1, free); compute it while issuing
-  // tile it + 1.
+  // K tile it lives in stage it % STAGES. Per tile: wait for this thread's
+  // copies of tile it (with three stages those of tile it + 1, issued later,
+  // may stay in flight) and its LDS writes; barrier (tile it complete for
+  // every wave, and the stage computed at it - 1 free); compute it while
+  // issuing tile it + STAGES - 1 into that stage.
   auto step = [&](auto stage_tag, int it) {
-    wait_and_barrier();
-    compute(stage_tag, it + 1 < ntiles);
+    if constexpr (T::STAGES == 2) {
+      wait_and_barrier<0>();
+    } else {
+      if (it + 1 < ntiles) wait_and_barrier<T::Copies>();
+      else wait_and_barrier<0>();
+    }
+    compute(stage_tag, it + T::STAGES - 1 < ntiles);
   };
   issue_all(std::integral_constant<int, 0>{});
-  for (int it = 0; it < ntiles; it += 2) {
+  if constexpr (T::STAGES == 3) {
+    if (ntiles > 1) issue_all(std::integral_constant<int, 1>{});
+  }
+  for (int it = 0; it < ntiles; it += T::STAGES) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
+    if constexpr (T::STAGES == 3) {
+      if (it + 2 < ntiles) step(std::integral_constant<int, 2>{}, it + 2);
+    }
   }
   __syncthreads();  // every wave done with the stages before they are reused
 }

@@ -116,13 +116,11 @@ __host__ __device__ inline PassOf pass_of(const RowMap& m, int64_t r) {
 // Time steps whose top-layer states are kept for one batched output-head pass.
 constexpr int kTimeChunk = 16;
 
-// Output-head vocabulary tile (columns per workgroup): 256 on the bf16 path
-// with sign probes, 128 otherwise.
+// Output-head vocabulary tile (columns per workgroup): 256 on the bf16 path,
+// 128 on the fp32 path.
 constexpr int kVocabTile = 128;
 constexpr int kVocabTileWide = 256;
-inline int vocab_tile(const zo_config& c) {
-  return c.wdtype == ZO_WBF16 && c.probe == ZO_RADEMACHER ? kVocabTileWide : kVocabTile;
-}
+inline int vocab_tile(const zo_config& c) { return c.wdtype == ZO_WBF16 ? kVocabTileWide : kVocabTile; }
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
