@@ -562,6 +562,24 @@ __global__ __launch_bounds__(256) void reduce_kernel(const double* row_loss, int
   }
 }
 
+// Zero n16 16-byte words. A kernel rather than a memset, so that a caller can
+// capture the forward into a graph and replay it.
+__global__ __launch_bounds__(256) void zero_kernel(uint4* p, uint64_t n16) {
+  const uint64_t stride = (uint64_t)gridDim.x * 256u;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256u + threadIdx.x; i < n16; i += stride) p[i] = uint4{0u, 0u, 0u, 0u};
+}
+
+// bytes: a multiple of 16 at a 16-byte aligned address (every workspace buffer is).
+hipError_t zero_async(void* p, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  if ((bytes & 15u) || ((uintptr_t)p & 15u)) return hipErrorInvalidValue;
+  const uint64_t n16 = bytes / 16;
+  uint64_t grid = (n16 + 255) / 256;
+  if (grid > 8192) grid = 8192;
+  zero_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>((uint4*)p, n16);
+  return hipGetLastError();
+}
+
 // Probe cache fill: eps z (fp32 weights) or bf16(eps z) (bf16 weights) of
 // every weight matrix for probes i0 .. i0+N-1 (layout: ZCacheMap). The values
 // are the ones the forward kernels compute when they regenerate the probe:
@@ -768,11 +786,13 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     if ((e = (x)) != hipSuccess) return e; \
   } while (0)
 
-  // zero initial states (every pass starts from h = c = 0) and the row sums
-  if (L > 1) ZO_TRY(hipMemsetAsync(hbuf, 0, (size_t)(L - 1) * 2 * state, st));
-  ZO_TRY(hipMemsetAsync(hist, 0, (size_t)W.T * state, st));
-  ZO_TRY(hipMemsetAsync(cbuf, 0, (size_t)L * M * H * 4, st));
-  ZO_TRY(hipMemsetAsync(row_loss, 0, (size_t)M * 8, st));
+  const int T = W.T;
+  // every pass starts from h = c = 0: zero what is read before it is written
+  // (the state slots that timestep 0 reads, the cell states) and the row sums
+  for (int l = 0; l + 1 < L; ++l) ZO_TRY(zero_async(hbuf + (size_t)(2 * l + 1) * state, state, st));
+  ZO_TRY(zero_async(hist + (size_t)(T - 1) * state, state, st));
+  ZO_TRY(zero_async(cbuf, (size_t)L * M * H * 4, st));
+  ZO_TRY(zero_async(row_loss, (size_t)M * 8, st));
 
   // probe cache (normal probes, when the workspace holds it)
   if (a.zc) ZO_TRY(launch_zcache_fill(a, st));
@@ -790,7 +810,6 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     ZO_TRY(hipGetLastError());
   }
 
-  const int T = W.T;
   for (int t = 0; t < a.C; ++t) {
     ZO_TRY(embed(a, t, x0, st));
     const char* xin = x0;
