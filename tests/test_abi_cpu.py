@@ -118,3 +118,31 @@ def test_argument_errors_before_any_device_work(zo):
     # probe indices must stay within 32 bits
     assert L.zo_update(C.byref(c), fake, 1, 1e-3, 1e-3, 4, 0xFFFFFFFE, fake, fake, None, None) == zo.ZO_EINVAL
     assert L.zo_debug_probe(5, 1, 0, 0, 4, fake, None) == zo.ZO_EINVAL
+
+
+def test_forward_difference_argument_errors(zo):
+    """zo_fd_losses and zo_fd_update validate like their central-difference
+    counterparts, before anything touches the device."""
+    cfg = wl.model_cfg("c1")
+    c = zo._cfg(cfg)
+    fake = C.c_void_p(0x10000)
+    L = zo.lib()
+
+    def fd_losses(eps=1e-3, N=2, B=2, Cn=4, i0=0, ws=1 << 40, theta=fake, cfgv=c):
+        return L.zo_fd_losses(C.byref(cfgv), theta, 1, eps, N, i0, fake, None, B, Cn, fake, fake, fake, ws, None)
+
+    assert fd_losses(eps=0.0) == zo.ZO_EINVAL
+    assert fd_losses(eps=float("inf")) == zo.ZO_EINVAL
+    assert fd_losses(N=0) == zo.ZO_EINVAL
+    assert fd_losses(B=0) == zo.ZO_EINVAL
+    assert fd_losses(Cn=0) == zo.ZO_EINVAL
+    assert fd_losses(N=3, i0=0xFFFFFFFE) == zo.ZO_EINVAL
+    assert fd_losses(theta=None) == zo.ZO_EINVAL
+    assert fd_losses(theta=C.c_void_p(0x10004)) == zo.ZO_EINVAL  # theta not 16-byte aligned
+    assert fd_losses(ws=16) == zo.ZO_ENOMEM
+    assert fd_losses(cfgv=zo._cfg(dict(cfg, hidden=40))) == zo.ZO_ESHAPE
+    assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, float("nan"), 2, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_fd_update(C.byref(c), fake, 1, 0.0, 1e-3, 2, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 0, 0, fake, fake, None, None) == zo.ZO_EINVAL
+    assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 2, 0, fake, None, None, None) == zo.ZO_EINVAL
+    assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 4, 0xFFFFFFFE, fake, fake, None, None) == zo.ZO_EINVAL
