@@ -29,6 +29,12 @@ METRIC_FD = "forward tokens/sec per FD-RGE step ((N+1)·B·C/s); % MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
 HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
 DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 3), "c4": (1, 3), "c5": (1, 3)}
+# Event timing: every launch where kernels are long (an event pair adds a few µs to the
+# stream: 0.2% of the c4 step), every 61st launch of each class where they are short (c2:
+# every launch would add ~22% to the step). 61 is prime, so the sample cycles through the
+# layers and timesteps.
+PROF_EVERY = {"c3": 1, "c4": 1}
+PROF_EVERY_SHORT = 61
 DESCRIPTION = {
     "c1": "1-layer LSTM V=256 E=32 H=64 fp32; B=4 C=32 uniform tokens; N=8 Rademacher",
     "c2": "2-layer LSTM V=256 E=128 H=256 fp32; B=64 C=256 REVERSE transduction (loss on "
@@ -187,6 +193,9 @@ def main():
     ap.add_argument("--calibrate-stream", action="store_true",
                     help="time an in-place read-modify-write of the workload's theta bytes "
                          "(the update's access pattern without its arithmetic) and exit")
+    ap.add_argument("--prof-every", type=int, default=None,
+                    help="time every n-th launch of each kernel class with HIP events "
+                         "(default: 1 for c3/c4, 61 otherwise)")
     ap.add_argument("--estimator", default="cd", choices=["cd", "fd"],
                     help="cd: central differences, 2N passes (default); fd: forward "
                          "differences, N perturbed passes and one clean pass")
@@ -259,7 +268,8 @@ def main():
         step(k)
         torch.cuda.synchronize()
         print(f"[bench] warm-up step {k + 1}/{W} done", file=sys.stderr, flush=True)
-    zo.profile_enable(True)
+    every = args.prof_every if args.prof_every is not None else PROF_EVERY.get(name, PROF_EVERY_SHORT)
+    zo.profile_enable(every)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(W, W + K):
@@ -278,13 +288,16 @@ def main():
     value = tokens_per_step / (dt / K)
     dtype = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"
     peak = PEAK_TFLOPS[dtype]
-    gate_ms, gate_n = prof["gate"]
+    gate_ms, gate_n, _ = prof["gate"]
     fl_step = gate_flops(cfg, passes, B) * C  # algorithmic gate flops per step
-    fl_launch = fl_step / (cfg["n_layers"] * C)
+    fl_launch = fl_step / (cfg["n_layers"] * C)  # average over the layers' launches
     achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
     fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
     mult = 2 if dtype == "bf16" else 1
-    kernels = {k: {"ms_per_step": v[0] / K, "launches_per_step": v[1] / K} for k, v in prof.items()}
+    # per class: the timed launches' mean duration times all launches of the class
+    kernels = {k: {"ms_per_step": (v[0] / v[1] * v[2] / K) if v[1] else 0.0, "launches_per_step": v[2] / K,
+                   "ms_per_launch": v[0] / v[1] if v[1] else None, "timed_launches": v[1]}
+               for k, v in prof.items()}
     out = {
         "metric": METRIC_FD if fd else METRIC,
         "value": value,
@@ -311,11 +324,12 @@ def main():
                      "executed_frac": None if achieved is None else achieved * mult / peak},
         "step_mfma_frac_algorithmic": fwd_flops / (dt / K) / 1e12 / peak,
         # the parameter update reads and writes theta once: 2 P w bytes
-        "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"]),
+        "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"][:2]),
         # the perturbed embedding writes 2N*B rows of E activations per timestep
         # (and gathers B rows of EMB): algorithmic bytes over its event time
-        "embed_hbm": embed_hbm(cfg, passes, B, 2 if dtype == "bf16" else 4, prof["embed"], fd),
+        "embed_hbm": embed_hbm(cfg, passes, B, 2 if dtype == "bf16" else 4, prof["embed"][:2], fd),
         "kernels": kernels,
+        "event_timing": f"every {every}-th launch of each kernel class",
         "losses_finite": losses_ok,
     }
     if not args.no_cpu_baseline:

@@ -185,15 +185,19 @@ int zo_debug_probe(int32_t probe, uint64_t seed, uint32_t i, uint64_t j0, uint64
  * input range (n_pairs <= 2^30); not part of the step. */
 int zo_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out, void* stream);
 
-/* Kernel timing (instrumentation, off by default). zo_profile_enable(1)
- * starts recording a HIP event pair around every launch of the timed kernel
- * classes, on the stream of the launch, and discards earlier records;
- * zo_profile_enable(0) stops recording. zo_profile_read() waits for the
- * recorded events and returns, for one class, the summed kernel time in
- * milliseconds and the number of launches since the last enable. */
+/* Kernel timing (instrumentation, off by default). zo_profile_enable(every),
+ * every >= 1, discards earlier records, counts every launch of the kernel
+ * classes below and brackets every every-th launch of each class (the 1st,
+ * (every+1)-th, ...) with a HIP event pair recorded on the stream of the
+ * launch; each pair adds a few microseconds to the stream, so workloads of
+ * short kernels sample (a prime stride cycles through layers and timesteps).
+ * zo_profile_enable(0) stops recording; every < 0 is ZO_EINVAL.
+ * zo_profile_read() waits for the recorded events and returns, for one class,
+ * the summed time of the timed launches in milliseconds, their number, and
+ * the number of all launches of the class since the last enable. */
 enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4, ZO_K_PROBE_CACHE = 5 };
-int zo_profile_enable(int32_t on);
-int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches);
+int zo_profile_enable(int32_t every);
+int zo_profile_read(int32_t kernel_class, double* timed_ms, int64_t* timed_launches, int64_t* all_launches);
 
 /* Thread-local text of the last error (empty string if none). */
 const char* zo_last_error(void);

@@ -18,10 +18,14 @@ struct Slot {
 std::mutex g_mu;
 std::vector<Slot> g_slots;  // event pairs, reused across enable/read cycles
 size_t g_used = 0;
+int64_t g_all[kKClasses] = {};  // launches per class since the last enable
 }  // namespace
 
 int prof_begin(KernelClass k, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_mu);
+  const int every = g_profile_on.load(std::memory_order_relaxed);
+  if (every <= 0) return -1;
+  if (g_all[k]++ % every != 0) return -1;
   if (g_used == g_slots.size()) {
     Slot sl{};
     if (hipEventCreate(&sl.a) != hipSuccess || hipEventCreate(&sl.b) != hipSuccess) return -1;
@@ -42,15 +46,18 @@ void prof_end(int slot, hipStream_t s) {
 
 extern "C" {
 
-int zo_profile_enable(int32_t on) {
+int zo_profile_enable(int32_t every) {
+  if (every < 0) return ZO_EINVAL;
   std::lock_guard<std::mutex> lk(zo::g_mu);
   zo::g_used = 0;
-  zo::g_profile_on.store(on ? 1 : 0);
+  for (auto& n : zo::g_all) n = 0;
+  zo::g_profile_on.store(every);
   return ZO_OK;
 }
 
-int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches) {
-  if (!total_ms || !launches || kernel_class < 0 || kernel_class >= zo::kKClasses) return ZO_EINVAL;
+int zo_profile_read(int32_t kernel_class, double* timed_ms, int64_t* timed_launches, int64_t* all_launches) {
+  if (!timed_ms || !timed_launches || !all_launches || kernel_class < 0 || kernel_class >= zo::kKClasses)
+    return ZO_EINVAL;
   std::lock_guard<std::mutex> lk(zo::g_mu);
   double ms = 0.0;
   int64_t n = 0;
@@ -63,8 +70,9 @@ int zo_profile_read(int32_t kernel_class, double* total_ms, int64_t* launches) {
     ms += e;
     ++n;
   }
-  *total_ms = ms;
-  *launches = n;
+  *timed_ms = ms;
+  *timed_launches = n;
+  *all_launches = zo::g_all[kernel_class];
   return ZO_OK;
 }
 

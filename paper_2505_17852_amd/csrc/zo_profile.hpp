@@ -1,7 +1,7 @@
-// Optional kernel timing: while enabled, launchers bracket selected kernel
-// launches with HIP events recorded on the launch stream, and
-// zo_profile_read() turns them into per-class totals. Disabled by default;
-// when disabled the hooks cost one relaxed atomic load.
+// Optional kernel timing: while enabled, launchers count their launches per
+// kernel class and bracket every n-th one with HIP events recorded on the
+// launch stream; zo_profile_read() turns them into per-class totals. Disabled
+// by default; when disabled the hooks cost one relaxed atomic load.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -12,9 +12,10 @@ namespace zo {
 enum KernelClass { kKGate = 0, kKHead = 1, kKEmbed = 2, kKCombine = 3, kKUpdate = 4, kKProbeCache = 5,
                    kKClasses = 6 };
 
-extern std::atomic<int> g_profile_on;
+extern std::atomic<int> g_profile_on;  // 0: off; n >= 1: time every n-th launch of a class
 
-// Returns a slot index to pass to prof_end, or -1 when profiling is off.
+// Counts the launch; returns a slot index to pass to prof_end when this launch
+// is timed, else -1.
 int prof_begin(KernelClass k, hipStream_t s);
 void prof_end(int slot, hipStream_t s);
 

@@ -67,7 +67,8 @@ def lib():
         L.zo_debug_probe.argtypes = [C.c_int32, C.c_uint64, C.c_uint32, C.c_uint64, C.c_uint64, vp, vp]
         L.zo_debug_gauss_pairs.argtypes = [vp, C.c_uint64, vp, vp]
         L.zo_profile_enable.argtypes = [C.c_int32]
-        L.zo_profile_read.argtypes = [C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+        L.zo_profile_read.argtypes = [C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64),
+                                      C.POINTER(C.c_int64)]
         L.zo_last_error.restype = C.c_char_p
         for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_fd_losses", "zo_fd_update",
                   "zo_debug_probe",
@@ -267,16 +268,18 @@ KERNEL_CLASSES = {"gate": K_GATE, "head": K_HEAD, "embed": K_EMBED, "combine": K
                   "update": K_UPDATE, "probe_cache": K_PROBE_CACHE}
 
 
-def profile_enable(on: bool = True):
-    """Start (and reset) or stop event timing of the library's kernel launches."""
-    _check(lib().zo_profile_enable(1 if on else 0))
+def profile_enable(every: int = 1):
+    """Start (and reset) event timing of every `every`-th launch of each
+    kernel class (all launches are counted), or stop it with 0 / False."""
+    _check(lib().zo_profile_enable(int(every)))
 
 
 def profile_read() -> dict:
-    """{class: (total_ms, launches)} since the last profile_enable(True)."""
+    """{class: (timed_ms, timed_launches, all_launches)} since the last
+    profile_enable."""
     out = {}
     for name, k in KERNEL_CLASSES.items():
-        ms, n = C.c_double(0.0), C.c_int64(0)
-        _check(lib().zo_profile_read(k, C.byref(ms), C.byref(n)))
-        out[name] = (ms.value, n.value)
+        ms, n, a = C.c_double(0.0), C.c_int64(0), C.c_int64(0)
+        _check(lib().zo_profile_read(k, C.byref(ms), C.byref(n), C.byref(a)))
+        out[name] = (ms.value, n.value, a.value)
     return out
