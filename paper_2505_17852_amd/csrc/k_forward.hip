@@ -18,6 +18,8 @@
 // At the end a reduction turns row sums into the 2N losses.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "zo_kernels.hpp"
 #include "zo_profile.hpp"
 #include "zo_rng.hpp"
@@ -104,8 +106,10 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
 // ---------------------------------------------------------------------------
 // fp32 MFMA main loop shared by the gate and head kernels.
 //
-// Workgroup tile: BM=64 rows x BNC=128 columns, 4 waves in 2 (rows) x 2
-// (columns); each wave owns 2 row tiles x 4 column tiles of 16x16 and runs
+// Workgroup tile: 32 RM rows x BNC=128 columns (RM = 2: 64 rows, 4 waves;
+// RM = 4: 128 rows, 8 waves, where a probe's rows come in blocks of 128, which
+// loads a third fewer bytes per flop), waves in RM (rows) x 2 (columns); each
+// wave owns 2 row tiles x 4 column tiles of 16x16 and runs
 // v_mfma_f32_16x16x4_f32. Within a K tile of 32, lane group g (lane/16) feeds
 // k = 8g + s at MFMA step s, so each lane reads 8 consecutive k with two
 // 128-bit LDS loads (the order in which k is summed is free).
@@ -120,7 +124,7 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
 //
 // Software pipeline: the next K tile's global loads and probe generation are
 // issued before the current tile's MFMAs, so their latency overlaps the
-// matrix work; LDS holds one tile (A [64][36], two weight tiles [128][36]).
+// matrix work; LDS holds one tile (A [32 RM][36], two weight tiles [128][36]).
 struct Seg {
   const float* A;  // row r of this tile at A + r * lda
   int64_t lda;
@@ -131,32 +135,39 @@ struct Seg {
   const float* Z;  // kGaussCached: eps z of this probe and matrix, laid out like W
 };
 
-struct Smem {
-  float a[BM * LDK];
+template <int RM>
+struct SmemT {
+  float a[32 * RM * LDK];
   float p[BNC * LDK];  // W + eps z (split: W)
   float m[BNC * LDK];  // W - eps z (split: eps z)
 };
+using Smem = SmemT<BM / 32>;
 
 // colmap(rho, &n) -> true if LDS column rho maps to a real weight row n.
 // fd: forward differences: the second tile holds W itself (the clean pass)
 // instead of W - eps z.
-template <int kind, bool kSplit, typename ColMap>
+template <int kind, bool kSplit, int RM = 2, typename ColMap>
 __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, const Seg s1,
                                              int nseg, ColMap colmap, const int (&wrow)[4], int arow0,
                                              bool wave_neg, Key key, uint32_t probe, float eps,
-                                             bool fd, Smem& sm) {
+                                             bool fd, SmemT<RM>& sm) {
+  constexpr int NT = 128 * RM;     // threads
+  constexpr int PPR = NT / BNC;    // loader threads per weight row
+  constexpr int KPT = BK / PPR;    // consecutive k per loader thread
+  constexpr int NW4 = KPT / 4;     // float4 weight loads per thread
+  static_assert(PPR * KPT == BK && KPT % 4 == 0 && 32 * RM * 8 == 2 * NT, "loader roles");
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int g4 = lane >> 4;
-  // loader roles: A rows (t + 256 q) >> 3, float4 column t & 7; weight row
-  // rho = t >> 1, 16 consecutive k starting at 16 * (t & 1)
-  const int rho = t >> 1, half = t & 1;
+  // loader roles: A rows (t + NT q) >> 3, float4 column t & 7; weight row
+  // rho = t / PPR, KPT consecutive k starting at KPT * (t % PPR)
+  const int rho = t / PPR, part = t % PPR;
   int wn;
   const bool wok = colmap(rho, wn);
   const int ntiles = s0.K / BK + (nseg > 1 ? s1.K / BK : 0);
 
-  f4 ra[2], rw[4];
-  float zv[16];
+  f4 ra[2], rw[NW4];
+  float zv[KPT];
   Words zcache{{0u, 0u, 0u, 0u}};
   int seg = 0, k0 = 0;  // position of the tile being fetched
 
@@ -164,12 +175,12 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
     const Seg sg = seg == 0 ? s0 : s1;
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int idx = t + 256 * q;
+      const int idx = t + NT * q;
       ra[q] = *(const f4*)(sg.A + (int64_t)(idx >> 3) * sg.lda + k0 + 4 * (idx & 7));
     }
-    const float* wp = sg.W + (int64_t)wn * sg.ldw + k0 + 16 * half;
+    const float* wp = sg.W + (int64_t)wn * sg.ldw + k0 + KPT * part;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) rw[q] = wok ? *(const f4*)(wp + 4 * q) : f4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < NW4; ++q) rw[q] = wok ? *(const f4*)(wp + 4 * q) : f4{0.f, 0.f, 0.f, 0.f};
     const uint64_t jrow = sg.zoff + (uint64_t)wn * (uint64_t)sg.ldw + (uint64_t)k0;
     if constexpr (kind == ZO_RADEMACHER) {
       uint32_t word;
@@ -181,21 +192,21 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
       } else {
         word = rademacher_word(key, probe, jrow >> 5);
       }
-      word >>= 16 * half;
+      word >>= KPT * part;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
+      for (int e = 0; e < KPT; ++e) zv[e] = ((word >> e) & 1u) ? eps : -eps;
     } else if constexpr (kind == kGaussCached) {
-      const float* zp = sg.Z + (int64_t)wn * sg.ldw + k0 + 16 * half;
+      const float* zp = sg.Z + (int64_t)wn * sg.ldw + k0 + KPT * part;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < NW4; ++q) {
         const f4 v = wok ? *(const f4*)(zp + 4 * q) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int e = 0; e < 4; ++e) zv[4 * q + e] = v[e];
       }
     } else {
-      const uint64_t j0 = jrow + 16 * half;
+      const uint64_t j0 = jrow + KPT * part;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int b = 0; b < NW4; ++b) {
         float z4[4];
         gauss_block(key, probe, (j0 >> 2) + b, z4);
 #pragma unroll
@@ -214,11 +225,11 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
     __syncthreads();  // the previous tile's fragments have been read
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
-      const int idx = t + 256 * q;
+      const int idx = t + NT * q;
       *(f4*)(&sm.a[(idx >> 3) * LDK + 4 * (idx & 7)]) = ra[q];
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < NW4; ++q) {
       f4 vp, vm;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -231,8 +242,8 @@ __device__ __forceinline__ void mainloop_f32(f4 (&acc)[2][4], const Seg s0, cons
           vm[e] = fadd(w, fd ? 0.0f : -z);
         }
       }
-      *(f4*)(&sm.p[rho * LDK + 16 * half + 4 * q]) = vp;
-      *(f4*)(&sm.m[rho * LDK + 16 * half + 4 * q]) = vm;
+      *(f4*)(&sm.p[rho * LDK + KPT * part + 4 * q]) = vp;
+      *(f4*)(&sm.m[rho * LDK + KPT * part + 4 * q]) = vm;
     }
     __syncthreads();
     if (it + 1 < ntiles) fetch();  // next tile's loads and probe overlap this tile's MFMAs
@@ -281,7 +292,7 @@ __device__ __forceinline__ float tanhf_(float x) { return 1.0f - 2.0f / (__expf(
 // One LSTM layer at one timestep for all rows:
 //   a = W_ih x + W_hh h + b  (+ s eps (Z_ih x + Z_hh h + z_b))
 //   i, f, o = sigmoid, g = tanh; c <- f c + i g; h <- o tanh(c)
-// Workgroup: 64 rows x 32 hidden units (4 gates x 32 = 128 columns); LDS
+// Workgroup: 32 RM rows x 32 hidden units (4 gates x 32 = 128 columns); LDS
 // column rho = gate * 32 + unit.
 struct GateArgs {
   const float* x;      // [M][El]
@@ -301,13 +312,13 @@ struct GateArgs {
   uint64_t zc_stride;
 };
 
-template <int kind, bool kSplit>
-__global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
-  __shared__ Smem sm;
+template <int kind, bool kSplit, int RM>
+__global__ __launch_bounds__(128 * RM) void gate_f32_kernel(GateArgs g) {
+  __shared__ SmemT<RM> sm;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % RM, wn = wave / RM;
   const int u0 = blockIdx.x * 32;
-  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const int64_t m0 = (int64_t)blockIdx.y * (32 * RM);
   const int pair = pass_of(g.rm, m0).probe;
   const int H = g.H;
   auto colmap = [&](int rho, int& n) {
@@ -332,8 +343,8 @@ __global__ __launch_bounds__(256) void gate_f32_kernel(GateArgs g) {
                kind == kGaussCached ? g.zc_ih + zpos : nullptr};
   const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
                kind == kGaussCached ? g.zc_hh + zpos : nullptr};
-  mainloop_f32<kind, kSplit>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps,
-                             g.rm.fd != 0, sm);
+  mainloop_f32<kind, kSplit, RM>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps,
+                                 g.rm.fd != 0, sm);
 
   // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
   const int u = u0 + 16 * wn + (lane & 15);
@@ -692,19 +703,26 @@ hipError_t launch_gate_f32(const ForwardArgs& a, int l, const void* x, const voi
   g.zc_ih = a.zc ? (const float*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const float*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
-  const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / BM));
   const bool split = a.fp32_split;
-  ProfScope ps(kKGate, st);
-  if (a.cfg.probe == ZO_RADEMACHER) {
-    if (split) gate_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(g);
-    else gate_f32_kernel<ZO_RADEMACHER, false><<<grid, 256, 0, st>>>(g);
-  } else if (a.zc) {
-    if (split) gate_f32_kernel<kGaussCached, true><<<grid, 256, 0, st>>>(g);
-    else gate_f32_kernel<kGaussCached, false><<<grid, 256, 0, st>>>(g);
-  } else {
-    if (split) gate_f32_kernel<ZO_GAUSSIAN, true><<<grid, 256, 0, st>>>(g);
-    else gate_f32_kernel<ZO_GAUSSIAN, false><<<grid, 256, 0, st>>>(g);
-  }
+  // 128-row workgroups where every block of 128 rows lies inside one probe's rows
+  const bool wide = R.pair_rows % 128 == 0;
+  auto go = [&](auto rm_tag) {
+    constexpr int RM = decltype(rm_tag)::value;
+    const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / (32 * RM)));
+    ProfScope ps(kKGate, st);
+    if (a.cfg.probe == ZO_RADEMACHER) {
+      if (split) gate_f32_kernel<ZO_RADEMACHER, true, RM><<<grid, 128 * RM, 0, st>>>(g);
+      else gate_f32_kernel<ZO_RADEMACHER, false, RM><<<grid, 128 * RM, 0, st>>>(g);
+    } else if (a.zc) {
+      if (split) gate_f32_kernel<kGaussCached, true, RM><<<grid, 128 * RM, 0, st>>>(g);
+      else gate_f32_kernel<kGaussCached, false, RM><<<grid, 128 * RM, 0, st>>>(g);
+    } else {
+      if (split) gate_f32_kernel<ZO_GAUSSIAN, true, RM><<<grid, 128 * RM, 0, st>>>(g);
+      else gate_f32_kernel<ZO_GAUSSIAN, false, RM><<<grid, 128 * RM, 0, st>>>(g);
+    }
+  };
+  if (wide) go(std::integral_constant<int, 4>{});
+  else go(std::integral_constant<int, 2>{});
   return hipGetLastError();
 }
 

@@ -162,6 +162,9 @@ LOSS_CASES = [
     ("deep3-gauss", dict(n_layers=3, vocab=130, embed=128, hidden=64, wdtype=0, probe=1), 2, 2, 9, 1e-3, False),
     ("c2-widths", wl.model_cfg("c2"), 2, 3, 12, 1e-3, True),
     ("c5-widths", wl.model_cfg("c5"), 2, 2, 10, 1e-2, False),
+    # B = 64 fills 128 rows per probe: the 128-row workgroups of the fp32 gate
+    ("wide-rad", dict(n_layers=2, vocab=100, embed=32, hidden=64, wdtype=0, probe=0), 2, 64, 5, 1e-2, True),
+    ("wide-gauss", dict(n_layers=2, vocab=100, embed=64, hidden=96, wdtype=0, probe=1), 2, 50, 4, 1e-2, True),
 ]
 
 
@@ -280,15 +283,16 @@ def test_delta_loss_matches_oracle(zo, oracle, name, B, C):
     assert np.all(np.abs(dg - dr) <= tol)
 
 
-@pytest.mark.parametrize("cfg", [
-    dict(n_layers=2, vocab=200, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.GAUSSIAN),
-    dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.GAUSSIAN),
-], ids=["fp32", "bf16"])
-def test_probe_cache_is_bit_identical(zo, cfg):
+@pytest.mark.parametrize("cfg,B", [
+    (dict(n_layers=2, vocab=200, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.GAUSSIAN), 5),
+    (dict(n_layers=2, vocab=200, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.GAUSSIAN), 64),
+    (dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.GAUSSIAN), 5),
+], ids=["fp32", "fp32-wide", "bf16"])
+def test_probe_cache_is_bit_identical(zo, cfg, B):
     """Normal probes: the losses with the probe cache (default workspace) and
     without it (the smallest workspace: probes regenerated in every tile) are
     bit-identical, for a slice i0 > 0 and a ragged batch."""
-    N, B, C = 3, 5, 13
+    N, C = 3, 13
     say(f"probe cache {cfg} N={N} B={B} C={C}")
     rng = np.random.default_rng(23)
     tok = torch.from_numpy(wl.uniform_tokens(rng, B, C, cfg["vocab"])).cuda()
