@@ -288,9 +288,11 @@ def main():
     value = tokens_per_step / (dt / K)
     dtype = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"
     peak = PEAK_TFLOPS[dtype]
-    gate_ms, gate_n, _ = prof["gate"]
+    gate_ms, gate_n, gate_all = prof["gate"]
     fl_step = gate_flops(cfg, passes, B) * C  # algorithmic gate flops per step
-    fl_launch = fl_step / (cfg["n_layers"] * C)  # average over the layers' launches
+    # average per launch: C L layer-steps per step, one per launch (bf16) or several
+    # layers' steps of one wavefront per launch (fp32)
+    fl_launch = fl_step * K / gate_all if gate_all else fl_step / (cfg["n_layers"] * C)
     achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
     fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
     mult = 2 if dtype == "bf16" else 1

@@ -293,28 +293,37 @@ __device__ __forceinline__ float tanhf_(float x) { return 1.0f - 2.0f / (__expf(
 //   a = W_ih x + W_hh h + b  (+ s eps (Z_ih x + Z_hh h + z_b))
 //   i, f, o = sigmoid, g = tanh; c <- f c + i g; h <- o tanh(c)
 // Workgroup: 32 RM rows x 32 hidden units (4 gates x 32 = 128 columns); LDS
-// column rho = gate * 32 + unit.
-struct GateArgs {
+// column rho = gate * 32 + unit. One launch runs up to kLaunchLayers layers,
+// each at its own timestep (blockIdx.z picks the layer): the step is a
+// wavefront over (layer, timestep) in which layer l at time t and layer l + 1
+// at time t - 1 are independent.
+constexpr int kLaunchLayers = 8;
+struct GateLayer {
   const float* x;      // [M][El]
   const float* hprev;  // [M][H]
   float* hout;         // [M][H]
   float* cst;          // [M][H]
-  const float* theta;
   uint64_t off_ih, off_hh, off_b;
-  int El, H;
+  int El;
   const float* zb;     // [N][4H] eps z of this layer's bias
+  const float* zc_ih;  // probe cache: W_ih's and W_hh's values of probe 0; probe n at + n * zc_stride
+  const float* zc_hh;
+};
+struct GateArgs {
+  GateLayer layer[kLaunchLayers];
+  const float* theta;
+  int H;
   Key key;
   uint32_t i0;
   float eps;
   RowMap rm;
-  const float* zc_ih;  // probe cache: W_ih's and W_hh's values of probe 0; probe n at + n * zc_stride
-  const float* zc_hh;
   uint64_t zc_stride;
 };
 
 template <int kind, bool kSplit, int RM>
 __global__ __launch_bounds__(128 * RM) void gate_f32_kernel(GateArgs g) {
   __shared__ SmemT<RM> sm;
+  const GateLayer& gl = g.layer[blockIdx.z];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave % RM, wn = wave / RM;
   const int u0 = blockIdx.x * 32;
@@ -339,17 +348,17 @@ __global__ __launch_bounds__(128 * RM) void gate_f32_kernel(GateArgs g) {
 
   const uint32_t probe = g.i0 + (uint32_t)pair;
   const uint64_t zpos = (uint64_t)pair * g.zc_stride;
-  const Seg s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El,
-               kind == kGaussCached ? g.zc_ih + zpos : nullptr};
-  const Seg s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
-               kind == kGaussCached ? g.zc_hh + zpos : nullptr};
+  const Seg s0{gl.x + m0 * gl.El, gl.El, g.theta + gl.off_ih, gl.El, gl.off_ih, gl.El,
+               kind == kGaussCached ? gl.zc_ih + zpos : nullptr};
+  const Seg s1{gl.hprev + m0 * H, H, g.theta + gl.off_hh, H, gl.off_hh, H,
+               kind == kGaussCached ? gl.zc_hh + zpos : nullptr};
   mainloop_f32<kind, kSplit, RM>(acc, s0, s1, 2, colmap, wrow, 32 * wm, wave_neg, g.key, probe, g.eps,
                                  g.rm.fd != 0, sm);
 
   // epilogue: lane holds rows 4*(lane/16)+v of each row tile, unit u
   const int u = u0 + 16 * wn + (lane & 15);
-  const float* bias = g.theta + g.off_b;
-  const float* zb = g.zb + (int64_t)pair * 4 * H;
+  const float* bias = g.theta + gl.off_b;
+  const float* zb = gl.zb + (int64_t)pair * 4 * H;
   float bs[4];  // bias + eps z_b, bias - eps z_b, or the bias (clean pass)
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -367,9 +376,9 @@ __global__ __launch_bounds__(128 * RM) void gate_f32_kernel(GateArgs g) {
       const float ao = acc[mt][3][v] + bs[3];
       const float ig = sigmoidf_(ai), fg = sigmoidf_(af), gg = tanhf_(ag), og = sigmoidf_(ao);
       const int64_t o = r * H + u;
-      const float c = fg * g.cst[o] + ig * gg;
-      g.cst[o] = c;
-      g.hout[o] = og * tanhf_(c);
+      const float c = fg * gl.cst[o] + ig * gg;
+      gl.cst[o] = c;
+      gl.hout[o] = og * tanhf_(c);
     }
   }
 }
@@ -681,34 +690,25 @@ hipError_t launch_embed_f32(const ForwardArgs& a, int t, void* x0, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_gate_f32(const ForwardArgs& a, int l, const void* x, const void* hprev, void* hout,
-                           float* cst, const float* zb, hipStream_t st) {
+// One fp32 gate launch over n (<= kLaunchLayers) layer-timesteps.
+hipError_t launch_gates_f32(const ForwardArgs& a, const GateLayer* ls, int n, hipStream_t st) {
+  if (n < 1 || n > kLaunchLayers) return hipErrorInvalidValue;
   const Rows& R = a.rows;
-  GateArgs g;
-  g.x = (const float*)x;
-  g.hprev = (const float*)hprev;
-  g.hout = (float*)hout;
-  g.cst = cst;
+  GateArgs g{};
+  for (int i = 0; i < n; ++i) g.layer[i] = ls[i];
   g.theta = (const float*)a.theta;
-  g.off_ih = a.lay.w_ih[l];
-  g.off_hh = a.lay.w_hh[l];
-  g.off_b = a.lay.bias[l];
-  g.El = l == 0 ? a.cfg.embed : a.cfg.hidden;
   g.H = a.cfg.hidden;
-  g.zb = zb;
   g.key = make_key(a.seed);
   g.i0 = a.i0;
   g.eps = a.eps;
   g.rm = row_map(R);
-  g.zc_ih = a.zc ? (const float*)a.zc + a.zmap.ih[l] : nullptr;
-  g.zc_hh = a.zc ? (const float*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
   const bool split = a.fp32_split;
   // 128-row workgroups where every block of 128 rows lies inside one probe's rows
   const bool wide = R.pair_rows % 128 == 0;
   auto go = [&](auto rm_tag) {
     constexpr int RM = decltype(rm_tag)::value;
-    const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / (32 * RM)));
+    const dim3 grid((unsigned)(g.H / 32), (unsigned)(R.M / (32 * RM)), (unsigned)n);
     ProfScope ps(kKGate, st);
     if (a.cfg.probe == ZO_RADEMACHER) {
       if (split) gate_f32_kernel<ZO_RADEMACHER, true, RM><<<grid, 128 * RM, 0, st>>>(g);
@@ -796,7 +796,6 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   float* ptgt = (float*)(ws + W.ptgt);
   double* row_loss = (double*)(ws + W.row_loss);
   auto embed = bf16 ? launch_embed_bf16 : launch_embed_f32;
-  auto gate = bf16 ? launch_gate_bf16 : launch_gate_f32;
   auto head = bf16 ? launch_head_bf16 : launch_head_f32;
   hipError_t e;
 #define ZO_TRY(x)                          \
@@ -828,24 +827,59 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     ZO_TRY(hipGetLastError());
   }
 
-  for (int t = 0; t < a.C; ++t) {
-    ZO_TRY(embed(a, t, x0, st));
-    const char* xin = x0;
-    for (int l = 0; l < L; ++l) {
-      char* hprev;
-      char* hout;
-      if (l < L - 1) {
-        char* base = hbuf + (size_t)l * 2 * state;
-        hprev = base + (size_t)((t + 1) & 1) * state;
-        hout = base + (size_t)(t & 1) * state;
-      } else {
-        hprev = hist + (size_t)((t + T - 1) % T) * state;
-        hout = hist + (size_t)(t % T) * state;
+  // states of layer l at time t: lower layers alternate between two slots
+  // (time t in slot t & 1), the top layer writes the time-chunk ring
+  auto state_in = [&](int l, int t) -> char* {  // h of layer l at time t - 1
+    if (l < L - 1) return hbuf + (size_t)l * 2 * state + (size_t)((t + 1) & 1) * state;
+    return hist + (size_t)((t + T - 1) % T) * state;
+  };
+  auto state_out = [&](int l, int t) -> char* {  // h of layer l at time t
+    if (l < L - 1) return hbuf + (size_t)l * 2 * state + (size_t)(t & 1) * state;
+    return hist + (size_t)(t % T) * state;
+  };
+  // Launch order. bf16: per timestep the embedding and one gate launch per
+  // layer. fp32: a wavefront, launch d running layer l at time d - l for every
+  // layer with 0 <= d - l < C, in one launch (layer l reads layer l - 1's state
+  // of time d - l, written by launch d - 1, while layer l - 1 writes its other
+  // slot); the embedding of time d is written after launch d - 1 has read the
+  // one of time d - 1.
+  const int ndiag = bf16 ? a.C : a.C + L - 1;
+  for (int d = 0; d < ndiag; ++d) {
+    if (d < a.C) ZO_TRY(embed(a, d, x0, st));
+    if (bf16) {
+      for (int l = 0; l < L; ++l) {
+        const char* xin = l == 0 ? x0 : state_out(l - 1, d);
+        ZO_TRY(launch_gate_bf16(a, l, xin, state_in(l, d), state_out(l, d), cbuf + (size_t)l * M * H,
+                                zb + (size_t)l * R.N * 4 * H, st));
       }
-      ZO_TRY(gate(a, l, xin, hprev, hout, cbuf + (size_t)l * M * H, zb + (size_t)l * R.N * 4 * H, st));
-      xin = hout;
+    } else {
+      GateLayer ls[kLaunchLayers];
+      int n = 0;
+      for (int l = 0; l < L; ++l) {
+        const int t = d - l;
+        if (t < 0 || t >= a.C) continue;
+        GateLayer& g = ls[n++];
+        g.x = (const float*)(l == 0 ? x0 : state_out(l - 1, t));
+        g.hprev = (const float*)state_in(l, t);
+        g.hout = (float*)state_out(l, t);
+        g.cst = cbuf + (size_t)l * M * H;
+        g.off_ih = a.lay.w_ih[l];
+        g.off_hh = a.lay.w_hh[l];
+        g.off_b = a.lay.bias[l];
+        g.El = l == 0 ? c.embed : c.hidden;
+        g.zb = zb + (size_t)l * R.N * 4 * H;
+        g.zc_ih = a.zc ? (const float*)a.zc + a.zmap.ih[l] : nullptr;
+        g.zc_hh = a.zc ? (const float*)a.zc + a.zmap.hh[l] : nullptr;
+        if (n == kLaunchLayers) {
+          ZO_TRY(launch_gates_f32(a, ls, n, st));
+          n = 0;
+        }
+      }
+      if (n) ZO_TRY(launch_gates_f32(a, ls, n, st));
     }
-    if (t % T == T - 1 || t == a.C - 1) {
+    // the top layer has finished time t: the head runs over each completed time chunk
+    const int t = bf16 ? d : d - (L - 1);
+    if (t >= 0 && (t % T == T - 1 || t == a.C - 1)) {
       const int t0 = t - t % T;
       const int Tc = t - t0 + 1;
       ZO_TRY(head(a, hist, t0, Tc, zbo, pmax, psum, ptgt, st));
