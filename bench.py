@@ -95,17 +95,18 @@ def update_hbm(P, w, upd):
             "frac": gbps / HBM_PEAK_GBPS}
 
 
-def embed_hbm(cfg, passes, B, w, emb, fd=False):
-    """Algorithmic HBM rate of the perturbed-embedding kernel: per launch it
+def embed_hbm(cfg, passes, B, C, w, emb, launches_per_step, fd=False):
+    """Algorithmic HBM rate of the perturbed-embedding kernel: per timestep it
     writes the passes*B rows of E activations (w bytes each; padding rows
-    included, as written) and reads B rows of EMB."""
+    included, as written) and reads B rows of EMB; a launch covers one
+    timestep (bf16) or a time chunk (fp32)."""
     ms, n = emb
-    if n == 0 or ms <= 0:
+    if n == 0 or ms <= 0 or not launches_per_step:
         return None
     gran = (128 if w == 2 else 32) * (2 if fd else 1)
     Bp = (B + gran - 1) // gran * gran
     E = cfg["embed"]
-    byt = passes * Bp * E * w + B * E * w
+    byt = C * (passes * Bp * E * w + B * E * w) / launches_per_step
     gbps = byt / (ms / n * 1e-3) / 1e9
     return {"bytes_per_launch": byt, "ms_per_launch": ms / n, "GBps": gbps, "frac": gbps / HBM_PEAK_GBPS}
 
@@ -329,7 +330,8 @@ def main():
         "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"][:2]),
         # the perturbed embedding writes 2N*B rows of E activations per timestep
         # (and gathers B rows of EMB): algorithmic bytes over its event time
-        "embed_hbm": embed_hbm(cfg, passes, B, 2 if dtype == "bf16" else 4, prof["embed"][:2], fd),
+        "embed_hbm": embed_hbm(cfg, passes, B, C, 2 if dtype == "bf16" else 4, prof["embed"][:2],
+                               prof["embed"][2] / K, fd),
         "kernels": kernels,
         "event_timing": f"every {every}-th launch of each kernel class",
         "losses_finite": losses_ok,

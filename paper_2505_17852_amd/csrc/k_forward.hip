@@ -18,6 +18,7 @@
 // At the end a reduction turns row sums into the 2N losses.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "zo_kernels.hpp"
@@ -69,38 +70,44 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(int kind, Key key, uint3
 }
 
 // ---------------------------------------------------------------------------
-// x0[r][e] = EMB[tok][e] + s eps z_n[emb + tok E + e] for the input token of
-// row r at time t; zeros for padding rows. One thread per 4 elements.
+// x0[tt][r][e] = EMB[tok][e] + s eps z_n[emb + tok E + e] for the input token
+// of row r at time t0 + tt, tt < Tc; zeros for padding rows. One thread per 4
+// elements; one launch per time chunk.
 template <int kind>
 __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint64_t emb_off, int E,
-                                                        const int32_t* tokens, int C, int t, int B,
+                                                        const int32_t* tokens, int C, int t0, int Tc, int B,
                                                         RowMap rm, int64_t M, Key key, uint32_t i0,
                                                         float eps, float* x0) {
   const int E4 = E >> 2;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= M * E4) return;
-  const int64_t r = idx / E4;
-  const int e = (int)(idx - r * E4) * 4;
-  const PassOf ps = pass_of(rm, r);
-  const int pair = ps.probe, b = ps.b;
-  f4 out = {0.f, 0.f, 0.f, 0.f};
-  if (b < B) {
-    const int tok = tokens[(int64_t)b * (C + 1) + t];
-    const uint64_t j = emb_off + (uint64_t)tok * E + e;
-    const f4 w = *(const f4*)(theta + j);
-    float z[4];
-    if constexpr (kind == ZO_RADEMACHER) {
-      const uint32_t word = rademacher_word(key, i0 + pair, j >> 5) >> (uint32_t)(j & 31u);
+  const int64_t total = (int64_t)Tc * M * E4;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t rr = idx / E4;  // row of the chunk: tt M + r
+    const int e = (int)(idx - rr * E4) * 4;
+    const int tt = (int)(rr / M);
+    const int64_t r = rr - (int64_t)tt * M;
+    const int t = t0 + tt;
+    const PassOf ps = pass_of(rm, r);
+    const int pair = ps.probe, b = ps.b;
+    f4 out = {0.f, 0.f, 0.f, 0.f};
+    if (b < B) {
+      const int tok = tokens[(int64_t)b * (C + 1) + t];
+      const uint64_t j = emb_off + (uint64_t)tok * E + e;
+      const f4 w = *(const f4*)(theta + j);
+      float z[4];
+      if constexpr (kind == ZO_RADEMACHER) {
+        const uint32_t word = rademacher_word(key, i0 + pair, j >> 5) >> (uint32_t)(j & 31u);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) z[q] = ((word >> q) & 1u) ? 1.0f : -1.0f;
-    } else {
-      gauss_block(key, i0 + pair, j >> 2, z);
+        for (int q = 0; q < 4; ++q) z[q] = ((word >> q) & 1u) ? 1.0f : -1.0f;
+      } else {
+        gauss_block(key, i0 + pair, j >> 2, z);
+      }
+      const float se = (float)ps.sign * eps;  // 0 for the clean pass: out = w
+#pragma unroll
+      for (int q = 0; q < 4; ++q) out[q] = w[q] + fmul(se, z[q]);
     }
-    const float se = (float)ps.sign * eps;  // 0 for the clean pass: out = w
-#pragma unroll
-    for (int q = 0; q < 4; ++q) out[q] = w[q] + fmul(se, z[q]);
+    *(f4*)(x0 + rr * E + e) = out;
   }
-  *(f4*)(x0 + r * E + e) = out;
 }
 
 // ---------------------------------------------------------------------------
@@ -671,21 +678,22 @@ hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_embed_f32(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
+// Perturbed embeddings of timesteps t0 .. t0 + Tc - 1 into x0 [Tc][M][E].
+hipError_t launch_embed_f32(const ForwardArgs& a, int t0, int Tc, void* x0, hipStream_t st) {
   const Rows& R = a.rows;
   const int E = a.cfg.embed;
   const RowMap rm = row_map(R);
-  const int64_t n = R.M * (E / 4);
-  const unsigned grid = (unsigned)((n + 255) / 256);
+  const int64_t n = (int64_t)Tc * R.M * (E / 4);
+  const unsigned grid = (unsigned)std::min<int64_t>((n + 255) / 256, (int64_t)1 << 20);
   const Key key = make_key(a.seed);
   ProfScope ps(kKEmbed, st);
   if (a.cfg.probe == ZO_RADEMACHER)
     embed_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
-                                                          a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
+                                                          a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
                                                           a.eps, (float*)x0);
   else
     embed_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
-                                                        a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
+                                                        a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
                                                         a.eps, (float*)x0);
   return hipGetLastError();
 }
@@ -795,7 +803,6 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   float* psum = (float*)(ws + W.psum);
   float* ptgt = (float*)(ws + W.ptgt);
   double* row_loss = (double*)(ws + W.row_loss);
-  auto embed = bf16 ? launch_embed_bf16 : launch_embed_f32;
   auto head = bf16 ? launch_head_bf16 : launch_head_f32;
   hipError_t e;
 #define ZO_TRY(x)                          \
@@ -841,11 +848,14 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   // layer. fp32: a wavefront, launch d running layer l at time d - l for every
   // layer with 0 <= d - l < C, in one launch (layer l reads layer l - 1's state
   // of time d - l, written by launch d - 1, while layer l - 1 writes its other
-  // slot); the embedding of time d is written after launch d - 1 has read the
-  // one of time d - 1.
+  // slot); the embeddings of a whole time chunk [d, d + T) are written in one
+  // launch before launch d, after launch d - 1 read the last of the previous
+  // chunk's.
   const int ndiag = bf16 ? a.C : a.C + L - 1;
+  const size_t x0_step = (size_t)M * c.embed * el;  // one timestep of embeddings
   for (int d = 0; d < ndiag; ++d) {
-    if (d < a.C) ZO_TRY(embed(a, d, x0, st));
+    if (bf16) ZO_TRY(launch_embed_bf16(a, d, x0, st));
+    else if (d < a.C && d % T == 0) ZO_TRY(launch_embed_f32(a, d, std::min(T, a.C - d), x0, st));
     if (bf16) {
       for (int l = 0; l < L; ++l) {
         const char* xin = l == 0 ? x0 : state_out(l - 1, d);
@@ -859,7 +869,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
         const int t = d - l;
         if (t < 0 || t >= a.C) continue;
         GateLayer& g = ls[n++];
-        g.x = (const float*)(l == 0 ? x0 : state_out(l - 1, t));
+        g.x = (const float*)(l == 0 ? x0 + (size_t)(t % T) * x0_step : state_out(l - 1, t));
         g.hprev = (const float*)state_in(l, t);
         g.hout = (float*)state_out(l, t);
         g.cst = cbuf + (size_t)l * M * H;

@@ -195,7 +195,8 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
     p = align_up(p + bytes, 256);
     return o;
   };
-  w.x0 = take(M * E * el);
+  // perturbed embeddings: one timestep (bf16 path), a time chunk (fp32 path)
+  w.x0 = take((c.wdtype == ZO_WBF16 ? 1 : (size_t)w.T) * M * E * el);
   w.hbuf = take((L - 1) * 2 * M * H * el);
   w.hist = take((size_t)w.T * M * H * el);
   w.cbuf = take(L * M * H * 4);
