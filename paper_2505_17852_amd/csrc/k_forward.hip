@@ -327,8 +327,10 @@ struct GateArgs {
   uint64_t zc_stride;
 };
 
+// 128-row workgroups are held to 128 VGPRs (four waves per SIMD), so that two
+// of them share a CU and each hides the other's tile loads.
 template <int kind, bool kSplit, int RM>
-__global__ __launch_bounds__(128 * RM) void gate_f32_kernel(GateArgs g) {
+__global__ __launch_bounds__(128 * RM, RM == 4 ? 4 : 2) void gate_f32_kernel(GateArgs g) {
   __shared__ SmemT<RM> sm;
   const GateLayer& gl = g.layer[blockIdx.z];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
