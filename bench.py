@@ -30,10 +30,10 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
 HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
 DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 3), "c4": (1, 3), "c5": (1, 3)}
 # Event timing: every launch where kernels are long (an event pair adds a few µs to the
-# stream: 0.2% of the c4 step), every 61st launch of each class where they are short (c2:
+# stream: 0.2% of the c4 step, less for c5's 5 ms launches), every 61st launch of each class where they are short (c2:
 # every launch would add ~22% to the step). 61 is prime, so the sample cycles through the
 # layers and timesteps.
-PROF_EVERY = {"c3": 1, "c4": 1}
+PROF_EVERY = {"c3": 1, "c4": 1, "c5": 1}
 PROF_EVERY_SHORT = 61
 DESCRIPTION = {
     "c1": "1-layer LSTM V=256 E=32 H=64 fp32; B=4 C=32 uniform tokens; N=8 Rademacher",
@@ -68,9 +68,9 @@ def kernel_source_hash(dtype):
 
 
 def measured_traffic(name, dtype):
-    """HBM bytes (read + write) per gate launch from the committed rocprofv3
-    FETCH_SIZE / WRITE_SIZE runs, if they were taken on the current kernel
-    sources; None otherwise."""
+    """HBM bytes (read + write) per gate layer-step from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE runs, if they were taken on the current
+    kernel sources; None otherwise."""
     path = os.path.join(ROOT, "profiles", "gate_traffic_c4_c2.md")
     if not os.path.exists(path):
         return None
@@ -196,7 +196,7 @@ def main():
                          "(the update's access pattern without its arithmetic) and exit")
     ap.add_argument("--prof-every", type=int, default=None,
                     help="time every n-th launch of each kernel class with HIP events "
-                         "(default: 1 for c3/c4, 61 otherwise)")
+                         "(default: 1 for c3/c4/c5, 61 otherwise)")
     ap.add_argument("--estimator", default="cd", choices=["cd", "fd"],
                     help="cd: central differences, 2N passes (default); fd: forward "
                          "differences, N perturbed passes and one clean pass")
@@ -294,6 +294,8 @@ def main():
     # average per launch: C L layer-steps per step, one per launch (bf16) or several
     # layers' steps of one wavefront per launch (fp32)
     fl_launch = fl_step * K / gate_all if gate_all else fl_step / (cfg["n_layers"] * C)
+    steps_per_launch = cfg["n_layers"] * C * K / gate_all if gate_all else 1.0  # layer-steps per gate launch
+    traffic_step = measured_traffic(name, dtype)
     achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
     fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
     mult = 2 if dtype == "bf16" else 1
@@ -320,7 +322,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "gate (fused LSTM layer step)",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": None if achieved is None else achieved / peak,
-                     "traffic": None if fd else measured_traffic(name, dtype),
+                     "traffic": None if fd or traffic_step is None else traffic_step * steps_per_launch,
                      "flops_per_launch": fl_launch,
                      # the bf16 kernels run the weight and probe products as two MFMA
                      # streams: executed matrix work is twice the algorithmic work
