@@ -49,7 +49,7 @@ def test_param_count_matches_oracle_layout(zo, oracle, name):
     assert zo.param_count(cfg) == oracle.param_count(cfg) == wl.param_count(cfg)
 
 
-def test_param_count_survey_values(zo):
+def test_param_count_closed_form_values(zo):
     # closed-form counts of the five workloads
     expect = {"c1": 49_664, "c2": 1_018_112, "c3": 127_628_112, "c4": 1_215_054_672,
               "c5": 3_354_880}
