@@ -222,3 +222,39 @@ def test_fd_training_lowers_the_loss(zo):
     assert hist[-20:].mean() < hist[:20].mean() - 0.05
     win = hist.reshape(6, 50).mean(axis=1)
     assert win[-1] < win[0]
+
+
+def test_fd_full_size_sampled_c4(zo, oracle):
+    """Forward differences at the 1.2B shape's full launch configuration
+    (N=16 perturbed passes and the clean pass, B=256, C=1024; the launch the
+    benchmark's forward-difference step times), with a mask that scores only
+    the first positions of two sequences, so that the oracle can compute the
+    losses on the 2-sequence, 3-position prefix: the first and last probes'
+    losses and the clean loss at the bf16 bar."""
+    name = "c4"
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+    tok, _ = wl.batch(name)
+    B, C = tok.shape[0], tok.shape[1] - 1
+    mask = np.zeros((B, C), np.uint8)
+    mask[0, :3] = 1
+    mask[1, :2] = 1
+    say(f"{name} forward differences, full size N={w['N']} B={B} C={C}, sampled positions")
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    L, L0 = zo.fd_losses(cfg, theta, sd["step"], w["eps"], w["N"], torch.from_numpy(tok).cuda(),
+                         torch.from_numpy(mask).cuda())
+    g, g0 = L.cpu().numpy(), float(L0.item())
+    del theta
+    torch.cuda.empty_cache()
+    assert np.all(np.isfinite(g)) and np.isfinite(g0)
+    ref_theta = oracle.init(cfg, sd["init"])
+    ref_tok = np.ascontiguousarray(tok[:2, :4])
+    ref_mask = np.ascontiguousarray(mask[:2, :3])
+    tol = RTOL[wl.BF16]
+    for i in (0, w["N"] - 1):
+        r, r0 = oracle.fd_losses(cfg, ref_theta, sd["step"], w["eps"], 1, ref_tok, ref_mask, i0=i)
+        say(f"probe {i}: gpu L {g[i]} L0 {g0}; oracle L {r[0]} L0 {r0}")
+        assert abs(g[i] - r[0]) <= tol * abs(r[0])
+        assert abs(g0 - r0) <= tol * abs(r0)

@@ -334,3 +334,26 @@ def test_c5_full_size_sampled(zo, oracle):
         say(f"probe {i}: gpu {gp[i]} {gm[i]} oracle {rp[0]} {rm[0]}")
         assert abs(gp[i] - rp[0]) <= LOSS_RTOL * abs(rp[0])
         assert abs(gm[i] - rm[0]) <= LOSS_RTOL * abs(rm[0])
+
+
+@pytest.mark.parametrize("name,cfg,N,B,C", [
+    ("ragged", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=0, probe=0), 3, 5, 12),
+    ("wide-gauss", dict(n_layers=2, vocab=100, embed=64, hidden=96, wdtype=0, probe=1), 2, 64, 6),
+], ids=["ragged", "wide-gauss"])
+def test_fp32_split_form_matches_oracle(zo, oracle, monkeypatch, name, cfg, N, B, C):
+    """The split form of the fp32 products (ZO_FP32_SPLIT=1: W.h and
+    (s h).(eps z) as two MFMA streams into one accumulator, kept for
+    measurement) against the oracle at the fp32 bar, on 64- and 128-row
+    workgroups."""
+    say(f"fp32 split form {name}")
+    monkeypatch.setenv("ZO_FP32_SPLIT", "1")
+    tok, mask = _tokens_for(name, cfg, B, C, True)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 19)
+    td, md = dev_tokens(tok, mask)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 4545, 1e-2, N, td, md)
+    gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
+    rp, rm = oracle.perturbed_losses(cfg, oracle.init(cfg, 19), 4545, 1e-2, N, tok, mask, as_double=True)
+    say("gpu", gp, gm, "oracle", rp, rm)
+    assert np.all(np.abs(gp - rp) <= LOSS_RTOL * np.abs(rp))
+    assert np.all(np.abs(gm - rm) <= LOSS_RTOL * np.abs(rm))
