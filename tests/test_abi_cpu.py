@@ -146,3 +146,41 @@ def test_forward_difference_argument_errors(zo):
     assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 0, 0, fake, fake, None, None) == zo.ZO_EINVAL
     assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 2, 0, fake, None, None, None) == zo.ZO_EINVAL
     assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 4, 0xFFFFFFFE, fake, fake, None, None) == zo.ZO_EINVAL
+
+
+def test_header_is_c_and_the_library_links_from_c(zo, tmp_path):
+    """include/zo.h compiles as C11, and a C program linked against the
+    library calls its host-only entry points (sizes and argument checks; no
+    device work) and reads the same numbers as the binding."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.dirname(zo.LIB_PATH)
+    src = tmp_path / "abi.c"
+    src.write_text(r'''
+#include <stdio.h>
+#include "zo.h"
+int main(void) {
+    zo_config c = {1, 256, 32, 64, ZO_WFP32, ZO_RADEMACHER};
+    zo_config bad = {0, 256, 32, 64, ZO_WFP32, ZO_RADEMACHER};
+    printf("%zu %zu %zu %zu\n", zo_param_count(&c), zo_workspace_bytes(&c, 8, 4, 32),
+           zo_workspace_bytes_min(&c, 8, 4, 32), zo_param_count(&bad));
+    int st = zo_update(&c, NULL, 1, 1e-3f, 1e-3f, 8, 0, NULL, NULL, NULL, NULL);
+    printf("%d %s\n", st, zo_last_error());
+    return 0;
+}
+''')
+    exe = tmp_path / "abi"
+    subprocess.run([gcc, "-std=c11", "-Wall", "-Werror", "-I", os.path.join(root, "include"), str(src),
+                    "-L", libdir, "-l:" + os.path.basename(zo.LIB_PATH), "-Wl,-rpath," + libdir, "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    cfg = wl.model_cfg("c1")
+    p, ws, wsmin, zero = (int(x) for x in out[0].split())
+    assert p == zo.param_count(cfg) and zero == 0
+    assert ws == zo.workspace_bytes(cfg, 8, 4, 32) and wsmin == zo.workspace_bytes_min(cfg, 8, 4, 32)
+    st, msg = out[1].split(" ", 1)
+    assert int(st) == zo.ZO_EINVAL and "NULL" in msg
