@@ -2,7 +2,7 @@
 against the oracle: the smallest shapes (one probe, one sequence, one
 position), a one-word vocabulary, a zero learning rate, probe indices at the
 top of the 32-bit range, batches exactly at and one past the row granule,
-and a large perturbation."""
+a large perturbation and a nine-layer stack."""
 import numpy as np
 import pytest
 
@@ -133,3 +133,15 @@ def test_large_perturbation(zo, oracle):
     rng = np.random.default_rng(12)
     tok = wl.uniform_tokens(rng, 3, 7, cfg["vocab"])
     check(*run_both(zo, oracle, cfg, 2, tok, None, 0.5), 1e-5)
+
+
+@pytest.mark.parametrize("wdtype", [wl.FP32, wl.BF16], ids=["fp32", "bf16"])
+def test_deep_stack(zo, oracle, wdtype):
+    """Nine layers and more timesteps than layers: on the fp32 path the
+    middle wavefront steps have all nine layers active, more than one launch
+    holds (eight), so they are split over two launches."""
+    E = 32 if wdtype == wl.FP32 else 64
+    cfg = dict(n_layers=9, vocab=20, embed=E, hidden=E, wdtype=wdtype, probe=wl.RADEMACHER)
+    rng = np.random.default_rng(19)
+    tok = wl.uniform_tokens(rng, 2, 12, cfg["vocab"])
+    check(*run_both(zo, oracle, cfg, 1, tok, None, 1e-2), RTOL[wdtype])
