@@ -138,6 +138,26 @@ def stream_limit(name, reps=10):
             "GBps": byt / (ms * 1e-3) / 1e9, "frac_of_hbm_peak": byt / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
 
 
+def head_hbm(cfg, passes, B, C, w, head, launches_per_step, fd=False):
+    """Algorithmic HBM rate of the output head: per step it reads W_out once
+    per time chunk, the top layer's states of every timestep once, and writes
+    each row's (max, sum of exp) partial of every vocabulary tile (8 bytes)
+    and its target logit (4 bytes)."""
+    ms, n = head
+    if n == 0 or ms <= 0 or not launches_per_step:
+        return None
+    gran = (128 if w == 2 else 32) * (2 if fd else 1)
+    Bp = (B + gran - 1) // gran * gran
+    V, H = cfg["vocab"], cfg["hidden"]
+    M = passes * Bp
+    vt = 256 if w == 2 else 128
+    nvt = (V + vt - 1) // vt
+    per_step = launches_per_step * V * H * w + C * M * H * w + C * M * (8 * nvt + 4)
+    byt = per_step / launches_per_step
+    gbps = byt / (ms / n * 1e-3) / 1e9
+    return {"bytes_per_launch": byt, "ms_per_launch": ms / n, "GBps": gbps, "frac": gbps / HBM_PEAK_GBPS}
+
+
 def cpu_baseline(name, budget_s=20.0, fd=False):
     """The oracle on the host cores, on a bounded sample of the workload:
     the full batch with the first N' probes (N' doubling until the budget is
@@ -334,6 +354,9 @@ def main():
         # (and gathers B rows of EMB): algorithmic bytes over its event time
         "embed_hbm": embed_hbm(cfg, passes, B, C, 2 if dtype == "bf16" else 4, prof["embed"][:2],
                                prof["embed"][2] / K, fd),
+        # the head reads W_out once per time chunk and every timestep's top-layer states once
+        "head_hbm": head_hbm(cfg, passes, B, C, 2 if dtype == "bf16" else 4, prof["head"][:2],
+                             prof["head"][2] / K, fd),
         "kernels": kernels,
         "event_timing": f"every {every}-th launch of each kernel class",
         "losses_finite": losses_ok,
