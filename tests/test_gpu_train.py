@@ -73,3 +73,36 @@ def test_training_lowers_the_loss(zo, probe):
     # mostly downhill: the mean of each successive 50-step window decreases
     win = hist.reshape(6, 50).mean(axis=1)
     assert np.all(np.diff(win) < 0)
+
+
+@pytest.mark.parametrize("wdtype,probe", [(wl.FP32, wl.RADEMACHER), (wl.BF16, wl.GAUSSIAN)],
+                         ids=["fp32-rademacher", "bf16-gaussian"])
+def test_log_replay_reconstructs_theta(zo, wdtype, probe):
+    """Only 2N scalars per step leave the forward, so the per-step log (seed,
+    L+, L-) reconstructs theta from the initial weights through the update
+    alone, bit for bit; a checkpoint taken midway resumes to the same theta."""
+    E = 32 if wdtype == wl.FP32 else 64
+    cfg = dict(n_layers=2, vocab=64, embed=E, hidden=E, wdtype=wdtype, probe=probe)
+    tok = torch.from_numpy(wl.uniform_tokens(np.random.default_rng(6), 4, 8, 64)).cuda()
+    N, eps, lr, steps, base = 8, 1e-2, 1e-2, 6, 500
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 3)
+    theta0 = theta.clone()
+    log, ckpt = [], None
+    for k in range(steps):
+        Lp, Lm = zo.perturbed_losses(cfg, theta, base + k, eps, N, tok)
+        log.append((base + k, Lp.clone(), Lm.clone()))
+        zo.update(cfg, theta, base + k, eps, lr, Lp, Lm)
+        if k == 2:
+            ckpt = theta.clone()
+    bits = torch.int16 if wdtype == wl.BF16 else torch.int32
+    replay = theta0.clone()
+    for seed, Lp, Lm in log:
+        zo.update(cfg, replay, seed, eps, lr, Lp, Lm)
+    assert torch.equal(replay.view(bits), theta.view(bits))
+    resumed = ckpt.clone()
+    for k in range(3, steps):
+        Lp, Lm = zo.perturbed_losses(cfg, resumed, base + k, eps, N, tok)
+        zo.update(cfg, resumed, base + k, eps, lr, Lp, Lm)
+    assert torch.equal(resumed.view(bits), theta.view(bits))
+    assert not torch.equal(theta.view(bits), theta0.view(bits))
