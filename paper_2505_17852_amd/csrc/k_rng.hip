@@ -83,7 +83,8 @@ __device__ __forceinline__ void store4(T* theta, uint64_t j, uint64_t P, const f
   }
 }
 
-// Rademacher update. sum_n c_n z_n[j] with z = +-1 is, for each group of 8
+// Rademacher update for any N (the kernel below takes N <= 16, the common
+// case, faster). sum_n c_n z_n[j] with z = +-1 is, for each group of 8
 // probes, a table lookup: T_g[m] = sum over the group of (bit n of m ? +c_n :
 // -c_n) for the 256 sign patterns m. Persistent workgroups (as many as fit
 // at once) walk chunks of 8192 consecutive parameters (256 Philox words per
@@ -95,8 +96,7 @@ __device__ __forceinline__ void store4(T* theta, uint64_t j, uint64_t P, const f
 // thread takes, for each set of 8 parameters, one byte of sign bits from
 // each of 8 probes, transposes that 8x8 bit block (three swap stages) so that
 // byte e holds parameter e's signs, and adds one table entry per parameter
-// and group of 8. theta is read and written once. The kernel is bound by
-// these VALU instructions (about 23 per parameter at 16 probes), not by HBM.
+// and group of 8. theta is read and written once.
 constexpr int kUpdChunk = 8192;   // parameters per workgroup (32 per thread, 4 sets of 8)
 constexpr int kUpdWords = kUpdChunk / 32;
 constexpr int kUpdGroup = 16;     // probes per pass over the LDS tables
@@ -370,6 +370,216 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ 
   }
 }
 
+// Rademacher update for N <= 16 probes. Persistent workgroups of 512
+// threads (two per CU) walk tiles of 8192 parameters (64 Philox blocks),
+// tile blockIdx.x + i * gridDim.x. theta moves in coalesced 16-byte pieces
+// with non-temporal loads and stores: lane t owns the 8-parameter chunks t
+// and t + 512 of a tile, so every wave instruction covers 1 KiB of
+// consecutive memory (lanes owning 32 consecutive parameters instead measured
+// 40-80% slower for this read-modify-write).
+//
+// The sign work is done in a transposed role: lane t = 2 wg + g transposes
+// word-group wg (sign word w = wg & 3 of block wg >> 2, 32 parameters) for
+// probe group g (probes 8g .. 8g+7). The 8 lanes of a block each compute two
+// of its 16 Philox blocks and swap words through LDS; three delta-swap stages
+// transpose the 8x8 bit blocks of the 8 probe words in all four bytes at once
+// (afterwards byte k of word r holds the 8 signs of parameter 8k + r), and the
+// result goes back to the lane's LDS row. After a barrier each chunk owner
+// reads the two rows of its word-group (one per probe group) and takes byte k
+// of word i as the table index of its parameter i.
+//
+// The signed-sum tables of probes 0-7 (T0) and 8-15 (T1) are built once per
+// workgroup and replicated 32 times: entry e is 256 bytes, [32 copies of
+// T0[e]][32 copies of T1[e]], copy (lane & 31) in bank (lane & 31), so the
+// lookups of 32 lanes never meet in a bank, and one v_perm builds a lookup
+// address (the entry in byte 1, the lane's copy in byte 0). The sums, and the
+// order in which they are formed, are those of the general kernel above.
+constexpr int kR16Threads = 512;
+constexpr int kR16Tile = kR16Threads * 16;  // parameters per tile
+constexpr int kR16Copies = 32;
+constexpr int kR16Row = 8;                  // LDS row: the 8 words of one (word-group, probe group)
+constexpr int kR16PerCu = 2;                // resident workgroups per CU (LDS: 80 KiB each)
+
+// Three delta swaps: transposes the 8x8 bit block in each byte lane of the 8
+// words s[0..7] (row r = word r, column c = bit c of the byte).
+__device__ __forceinline__ void transpose8_words(uint32_t s[8]) {
+#pragma unroll
+  for (int d = 1; d < 8; d <<= 1) {
+    // columns c with bit d clear (m) of row r + d <-> columns c + d of row r
+    const uint32_t m = d == 1 ? 0x55555555u : d == 2 ? 0x33333333u : 0x0F0F0F0Fu;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      if (r & d) continue;
+      const uint32_t a = s[r], b = s[r + d];
+      s[r + d] = ((a >> d) & m) | (b & ~m);
+      s[r] = ((b << d) & (m << d)) | (a & ~(m << d));
+    }
+  }
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Orders this wave's LDS accesses: the writes and reads before it complete
+// (lgkmcnt(0)) before any after it issue. Lanes of one wave exchange data
+// through LDS this way without a workgroup barrier; the empty asm statements
+// keep the compiler from moving memory accesses across it.
+__device__ __forceinline__ void wave_lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt, expcnt at their maxima; lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <typename T>
+__global__ __launch_bounds__(kR16Threads) void update_rad16_kernel(
+    T* __restrict__ theta, uint64_t P, Key key, float eps, float lr, int N, uint32_t i0,
+    const float* __restrict__ Lp, const float* __restrict__ Lm, int32_t* __restrict__ skipped,
+    int lm_stride) {
+  // tables (64 KiB) first, so that a lookup address fits a 16-bit LDS offset;
+  // then the rows (16 KiB), which also hold the coefficients and the 4-probe
+  // partial sums while the tables are built
+  __shared__ __align__(16) uint32_t lds[256 * 2 * kR16Copies + kR16Threads * kR16Row];
+  float* tab = (float*)lds;
+  uint32_t* rows = lds + 256 * 2 * kR16Copies;
+  float* coef = (float*)rows;             // [16]
+  float* half_table = (float*)rows + 32;  // [2][32]
+  int* bad = (int*)rows + 96;
+  const int t = threadIdx.x;
+  constexpr int kVec = 8 * (int)sizeof(T) / 16;  // 16-byte vectors per chunk
+  const bool two = N > 8;
+
+  // wave 0: coefficients (lanes 0-15) and the 4-probe partial sums of both
+  // probe groups; then every thread builds one table entry's 32 copies
+  if (__builtin_amdgcn_readfirstlane(t >> 6) == 0) {
+    float c = 0.f;
+    int nonfinite = 0;
+    if (t < N && t < kUpdGroup) {
+      const float lp = Lp[t], lm = Lm[t * lm_stride];
+      c = update_coeff(lr, N, lp, lm, eps);
+      nonfinite = !(isfinite(lp) && isfinite(lm));
+    }
+    if (t < kUpdGroup) coef[t] = c;
+    const int any = __builtin_amdgcn_readfirstlane(__any(nonfinite) ? 1 : 0);
+    if (t == 0) *bad = any;
+    wave_lds_sync();
+    const int gg = t >> 5, h = (t >> 4) & 1, m = t & 15;
+    float v = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb) {
+      const float cb = coef[8 * gg + 4 * h + bb];
+      v += ((m >> bb) & 1) ? cb : -cb;
+    }
+    half_table[32 * gg + 16 * h + m] = v;
+  }
+  lds_barrier();
+  {
+    // entry e of group gt: the sums of the low and the high nibble, added
+    // (with at most 8 probes both halves of an entry hold T0)
+    const int e = t & 255, gt = t >> 8, gs = two ? gt : 0;
+    const float v = half_table[32 * gs + (e & 15)] + half_table[32 * gs + 16 + (e >> 4)];
+    float4* dst = (float4*)&tab[e * 2 * kR16Copies + gt * kR16Copies];
+#pragma unroll
+    for (int c = 0; c < kR16Copies / 4; ++c) dst[c] = float4{v, v, v, v};
+  }
+  const bool finite = *bad == 0;
+  if (blockIdx.x == 0 && t == 0 && skipped) *skipped = finite ? 0 : 1;
+  lds_barrier();  // the rows are free again
+  if (!finite) return;  // the same in every lane
+
+  const int b = t >> 3, w = (t >> 1) & 3, g = t & 1;  // transposer role
+  const bool transposer = g == 0 || two;
+  const uint32_t k = (uint32_t)(t & 3);               // owner role: byte k of each word
+  const uint32_t sel = 0x0C0C0000u | ((4u + k) << 8);  // byte 0 of the base, byte k of the word
+  const uint32_t base0 = (uint32_t)(t & 31) * 4u, base1 = 128u + base0;
+  const uint64_t ntiles = (P + kR16Tile - 1) / kR16Tile;
+  for (uint64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const uint64_t tile0 = tile * kR16Tile;
+    // chunk q of this lane holds parameters tile0 + 8 (t + 512 q) .. + 7
+    u32x4 raw[2][kVec];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const uint64_t j = tile0 + 8u * (uint64_t)(t + kR16Threads * q);
+      if (j + 8 <= P) {
+#pragma unroll
+        for (int v = 0; v < kVec; ++v)
+          raw[q][v] = __builtin_nontemporal_load((const u32x4*)(theta + j) + v);
+      } else {
+        T x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = j + e < P ? theta[j + e] : (T)0;
+        __builtin_memcpy(raw[q], x, sizeof(x));
+      }
+    }
+    if (transposer) {
+      const uint64_t blk = tile0 / 128 + (uint64_t)b;
+      Words x[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const int p = 8 * g + 2 * w + m;  // zeros past N: their coefficients are 0
+        if (p < N) x[m] = stream_block(key, blk, i0 + (uint32_t)p, kTagRademacher);
+        else x[m] = Words{{0u, 0u, 0u, 0u}};
+      }
+      // word v of these two probes goes to the row of lane (b, v, g), at 2 w
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        *(uint2*)&rows[(8 * b + 2 * v + g) * kR16Row + 2 * w] = uint2{x[0].w[v], x[1].w[v]};
+    }
+    wave_lds_sync();  // the 8 lanes of a block are in one wave
+    if (transposer) {
+      uint32_t s[8];
+      const uint4 lo = *(const uint4*)&rows[t * kR16Row], hi = *(const uint4*)&rows[t * kR16Row + 4];
+      s[0] = lo.x; s[1] = lo.y; s[2] = lo.z; s[3] = lo.w;
+      s[4] = hi.x; s[5] = hi.y; s[6] = hi.z; s[7] = hi.w;
+      transpose8_words(s);  // the row is this lane's own from here on
+      *(uint4*)&rows[t * kR16Row] = uint4{s[0], s[1], s[2], s[3]};
+      *(uint4*)&rows[t * kR16Row + 4] = uint4{s[4], s[5], s[6], s[7]};
+    }
+    lds_barrier();
+    // owner role: parameter i of chunk q is parameter 8k + i of word-group wg
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int wg = (t + kR16Threads * q) >> 2;
+      const uint4 a0 = *(const uint4*)&rows[(2 * wg) * kR16Row];
+      const uint4 a1 = *(const uint4*)&rows[(2 * wg) * kR16Row + 4];
+      const uint32_t sa[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      float acc[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        acc[i] = *(const float*)((const char*)tab + __builtin_amdgcn_perm(sa[i], base0, sel));
+      if (two) {
+        const uint4 b0 = *(const uint4*)&rows[(2 * wg + 1) * kR16Row];
+        const uint4 b1 = *(const uint4*)&rows[(2 * wg + 1) * kR16Row + 4];
+        const uint32_t sb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          acc[i] += *(const float*)((const char*)tab + __builtin_amdgcn_perm(sb[i], base1, sel));
+      }
+      const uint64_t j = tile0 + 8u * (uint64_t)(t + kR16Threads * q);
+      u32x4 out[kVec];
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          out[0][e] = pack_bf16x2_rne(bf16_to_f32((uint16_t)raw[q][0][e]) - acc[2 * e],
+                                      bf16_to_f32((uint16_t)(raw[q][0][e] >> 16)) - acc[2 * e + 1]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          out[e >> 2][e & 3] = __float_as_uint(__uint_as_float(raw[q][e >> 2][e & 3]) - acc[e]);
+      }
+      if (j + 8 <= P) {
+#pragma unroll
+        for (int v = 0; v < kVec; ++v) __builtin_nontemporal_store(out[v], (u32x4*)(theta + j) + v);
+      } else {
+        T x[8];
+        __builtin_memcpy(x, out, sizeof(x));
+        for (int e = 0; e < 8; ++e)
+          if (j + e < P) theta[j + e] = x[e];
+      }
+    }
+    lds_barrier();  // every owner has read the rows before the next tile writes them
+  }
+}
+
 // Normal-probe update: each thread owns one Philox block (4 parameters) and
 // regenerates its 4 values of every probe in ascending order.
 template <typename T>
@@ -443,7 +653,22 @@ hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t
                          int32_t* skipped, hipStream_t s, int lm_stride) {
   const Key key = make_key(seed);
   ProfScope ps(kKUpdate, s);
-  if (kind == ZO_RADEMACHER) {
+  if (kind == ZO_RADEMACHER && N <= kUpdGroup) {
+    // persistent workgroups, kR16PerCu per CU, never more than there are tiles
+    const uint64_t tiles = (P + kR16Tile - 1) / kR16Tile;
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const uint64_t slots = (uint64_t)(cus > 0 ? cus : 1) * kR16PerCu;
+    const unsigned grid = (unsigned)(tiles < slots ? tiles : slots);
+    if (wdtype == ZO_WBF16)
+      update_rad16_kernel<uint16_t><<<dim3(grid), dim3(kR16Threads), 0, s>>>(
+          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
+    else
+      update_rad16_kernel<float><<<dim3(grid), dim3(kR16Threads), 0, s>>>(
+          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
+  } else if (kind == ZO_RADEMACHER) {
     // persistent workgroups: as many as fit on the device at once, each
     // walking chunks of kUpdChunk parameters
     const uint64_t nchunks = (P + kUpdChunk - 1) / kUpdChunk;

@@ -33,10 +33,20 @@ struct Words {
   uint32_t w[4];
 };
 
+// a ^ b ^ k in one v_bitop3_b32 (truth table 0x96); the compiler would emit
+// two v_xor_b32. k must be the same in every lane (a Philox round key: the
+// seed is a launch argument), since it is read from a scalar register.
+__device__ __forceinline__ uint32_t xor3_key(uint32_t a, uint32_t b, uint32_t k) {
+  uint32_t d;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(d) : "v"(a), "v"(b), "s"(k));
+  return d;
+}
+
 // Philox4x32 with 10 rounds (Salmon, Moraes, Dror and Shaw, SC'11): each
 // round multiplies counter words 0 and 2 by two fixed odd constants, swaps
 // the halves of the 64-bit products across the lanes and mixes in the key;
-// the key advances by the two Weyl constants after every round.
+// the key advances by the two Weyl constants after every round. The key must
+// be wave-uniform (xor3_key).
 __device__ __forceinline__ Words philox(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3,
                                         Key key) {
   uint32_t k0 = key.k0, k1 = key.k1;
@@ -44,9 +54,9 @@ __device__ __forceinline__ Words philox(uint32_t x0, uint32_t x1, uint32_t x2, u
   for (int r = 0; r < 10; ++r) {
     const uint64_t pa = (uint64_t)0xD2511F53u * (uint64_t)x0;
     const uint64_t pb = (uint64_t)0xCD9E8D57u * (uint64_t)x2;
-    const uint32_t y0 = (uint32_t)(pb >> 32) ^ x1 ^ k0;
+    const uint32_t y0 = xor3_key((uint32_t)(pb >> 32), x1, k0);
     const uint32_t y1 = (uint32_t)pb;
-    const uint32_t y2 = (uint32_t)(pa >> 32) ^ x3 ^ k1;
+    const uint32_t y2 = xor3_key((uint32_t)(pa >> 32), x3, k1);
     const uint32_t y3 = (uint32_t)pa;
     x0 = y0;
     x1 = y1;
