@@ -100,6 +100,12 @@ def test_init_bit_exact(zo, oracle, cfg):
 
 UPDATE_CASES = [
     ("c1-rad", dict(wl.model_cfg("c1")), 8, 1e-2, 1e-3),
+    # sign probes, N <= 16: two 8192-parameter tiles, the second ragged (P = 13325)
+    ("tiles-rad16-bf16", dict(n_layers=1, vocab=77, embed=32, hidden=32, wdtype=wl.BF16, probe=0), 16, 1e-3, 1e-3),
+    # 23 tiles, 8 < N < 16 (probes 11..15 absent), fp32
+    ("tiles-rad11-fp32", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wl.FP32, probe=0), 11, 1e-2, 1e-2),
+    # N <= 8: one table
+    ("tiles-rad5-bf16", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wl.BF16, probe=0), 5, 1e-3, 1e-3),
     ("ragged-rad-bf16", dict(n_layers=1, vocab=77, embed=32, hidden=32, wdtype=wl.BF16, probe=0), 37, 1e-3, 1e-3),
     ("gauss-fp32", dict(n_layers=1, vocab=50, embed=32, hidden=64, wdtype=wl.FP32, probe=1), 19, 1e-2, 1e-2),
     ("gauss-bf16", dict(n_layers=2, vocab=50, embed=32, hidden=32, wdtype=wl.BF16, probe=1), 300, 1e-3, 1e-3),
@@ -119,6 +125,36 @@ def test_update_parity(zo, oracle, name, cfg, N, eps, lr):
     got = theta.view(torch.int16 if cfg["wdtype"] == wl.BF16 else torch.int32).cpu().numpy().view(ref.dtype)
     assert oracle.update(cfg, ref, 99, eps, lr, Lp, Lm, i0=3) == 0
     assert theta_close(got, ref, cfg)
+
+
+@pytest.mark.parametrize("wdtype", [wl.FP32, wl.BF16])
+@pytest.mark.parametrize("N", [5, 12, 16])
+def test_update_small_n_kernel_matches_general(zo, wdtype, N):
+    """Sign probes with N <= 16 run their own update kernel; it forms the same
+    table sums in the same order as the kernel for any N. With lr = N 2^-10 and
+    lr' = 17 2^-10 both calls use the coefficients 2^-10 (L+ - L-)/(2 eps), so
+    N probes and 17 probes whose last 17 - N have L+ = L- (coefficient 0) must
+    give the same theta (as values: only the sign of a zero may differ)."""
+    cfg = dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=wdtype, probe=wl.RADEMACHER)
+    say(f"update small-N vs general: N={N} wdtype={wdtype} P={zo.param_count(cfg)}")
+    rng = np.random.default_rng(N)
+    Lp = (5.0 + rng.standard_normal(17) * 0.01).astype(np.float32)
+    Lm = (5.0 + rng.standard_normal(17) * 0.01).astype(np.float32)
+    Lm[N:] = Lp[N:]
+    a = zo.new_theta(cfg)
+    zo.init(cfg, a, 7)
+    b = a.clone()
+    zo.update(cfg, a, 123, 1e-3, N * 2.0 ** -10, torch.from_numpy(Lp[:N]).cuda(),
+              torch.from_numpy(Lm[:N]).cuda(), i0=9)
+    zo.update(cfg, b, 123, 1e-3, 17 * 2.0 ** -10, torch.from_numpy(Lp).cuda(),
+              torch.from_numpy(Lm).cuda(), i0=9)
+    if wdtype == wl.BF16:
+        fa = (a.view(torch.int16).cpu().numpy().astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+        fb = (b.view(torch.int16).cpu().numpy().astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    else:
+        fa, fb = a.cpu().numpy(), b.cpu().numpy()
+    bad = np.nonzero(fa != fb)[0]
+    assert bad.size == 0, f"{bad.size} differ, first {bad[:5].tolist()}: {fa[bad[:5]]} vs {fb[bad[:5]]}"
 
 
 def test_update_equal_losses_leave_theta_unchanged(zo):
