@@ -26,7 +26,7 @@ if ROOT not in sys.path:
 
 METRIC = "perturbed-forward tokens/sec per CD-RGE step (2N·B·C/s); % MFMA peak"
 METRIC_FD = "forward tokens/sec per FD-RGE step ((N+1)·B·C/s); % MFMA peak"
-PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}  # dense MFMA peaks of MI355X
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0, "fp16": 2500.0}  # dense MFMA peaks of MI355X
 HBM_PEAK_GBPS = 8000.0  # HBM3E peak of MI355X
 DEFAULTS = {"c1": (3, 20), "c2": (3, 20), "c3": (1, 3), "c4": (1, 3), "c5": (1, 3)}
 # Event timing: every launch where kernels are long (an event pair adds a few µs to the
@@ -307,7 +307,11 @@ def main():
     ms_per_step = dt / K * 1e3
     tokens_per_step = passes * B * C
     value = tokens_per_step / (dt / K)
-    dtype = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"
+    wdt = "bf16" if cfg["wdtype"] == wl.BF16 else "f32"  # weight storage
+    wbytes = 2 if wdt == "bf16" else 4
+    # arithmetic of the products: bf16 weights run as fp16 MFMA operands
+    # (fp16(W + s eps z) and fp16 activations, fp32 accumulation)
+    dtype = "fp16" if wdt == "bf16" else "f32"
     peak = PEAK_TFLOPS[dtype]
     gate_ms, gate_n, gate_all = prof["gate"]
     fl_step = gate_flops(cfg, passes, B) * C  # algorithmic gate flops per step
@@ -315,10 +319,9 @@ def main():
     # layers' steps of one wavefront per launch (fp32)
     fl_launch = fl_step * K / gate_all if gate_all else fl_step / (cfg["n_layers"] * C)
     steps_per_launch = cfg["n_layers"] * C * K / gate_all if gate_all else 1.0  # layer-steps per gate launch
-    traffic_step = measured_traffic(name, dtype)
+    traffic_step = measured_traffic(name, wdt)
     achieved = (fl_launch * gate_n) / (gate_ms * 1e-3) / 1e12 if gate_ms > 0 else None
     fwd_flops = 2 * wl.gemm_params(cfg) * tokens_per_step
-    mult = 2 if dtype == "bf16" else 1
     # per class: the timed launches' mean duration times all launches of the class
     kernels = {k: {"ms_per_step": (v[0] / v[1] * v[2] / K) if v[1] else 0.0, "launches_per_step": v[2] / K,
                    "ms_per_launch": v[0] / v[1] if v[1] else None, "timed_launches": v[1]}
@@ -343,19 +346,16 @@ def main():
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": None if achieved is None else achieved / peak,
                      "traffic": None if fd or traffic_step is None else traffic_step * steps_per_launch,
-                     "flops_per_launch": fl_launch,
-                     # the bf16 kernels run the weight and probe products as two MFMA
-                     # streams: executed matrix work is twice the algorithmic work
-                     "executed_frac": None if achieved is None else achieved * mult / peak},
+                     "flops_per_launch": fl_launch},
         "step_mfma_frac_algorithmic": fwd_flops / (dt / K) / 1e12 / peak,
         # the parameter update reads and writes theta once: 2 P w bytes
-        "update_hbm": update_hbm(zo.param_count(cfg), 2 if dtype == "bf16" else 4, prof["update"][:2]),
+        "update_hbm": update_hbm(zo.param_count(cfg), wbytes, prof["update"][:2]),
         # the perturbed embedding writes 2N*B rows of E activations per timestep
         # (and gathers B rows of EMB): algorithmic bytes over its event time
-        "embed_hbm": embed_hbm(cfg, passes, B, C, 2 if dtype == "bf16" else 4, prof["embed"][:2],
+        "embed_hbm": embed_hbm(cfg, passes, B, C, wbytes, prof["embed"][:2],
                                prof["embed"][2] / K, fd),
         # the head reads W_out once per time chunk and every timestep's top-layer states once
-        "head_hbm": head_hbm(cfg, passes, B, C, 2 if dtype == "bf16" else 4, prof["head"][:2],
+        "head_hbm": head_hbm(cfg, passes, B, C, wbytes, prof["head"][:2],
                              prof["head"][2] / K, fd),
         "kernels": kernels,
         "event_timing": f"every {every}-th launch of each kernel class",

@@ -72,8 +72,10 @@ enum { ZO_RADEMACHER = 0, ZO_GAUSSIAN = 1 };
 /* Model shape. All fields > 0; embed and hidden must be multiples of 32
  * (ZO_ESHAPE otherwise), and for zo_perturbed_losses with bf16 weights
  * multiples of 64; n_layers <= 64. wdtype: ZO_WFP32 or ZO_WBF16
- * (storage type of theta; bf16 runs the matrix products in bf16 with fp32
- * accumulation and fp32 cell state). probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
+ * (storage type of theta; bf16 runs every matrix product as fp16 operands,
+ * the perturbed weight fp16(w + s eps z) formed in registers from an fp16
+ * copy of the weights, with fp32 accumulation and fp32 cell state).
+ * probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
 typedef struct {
     int32_t n_layers;
     int32_t vocab;
@@ -89,12 +91,13 @@ size_t zo_param_count(const zo_config* cfg);
 
 /* Bytes of device workspace zo_perturbed_losses (or zo_fd_losses) uses for N probes and a
  * batch of B sequences of C positions; 0 if the arguments are invalid.
- * Host only. With normal probes this includes the probe cache: N * P_g
- * values of eps z (fp32 weights) or bf16(eps z) (bf16 weights) for the
- * weight matrices (every W_ih, W_hh and W_out; P_g their total size), written
- * once per call and read by every timestep instead of regenerating the probe
- * in every tile (the results are bit-identical either way). With sign probes
- * it equals zo_workspace_bytes_min. */
+ * Host only. With bf16 weights every workspace holds an fp16 copy of the
+ * weight matrices (every W_ih, W_hh and W_out; P_g values), written once per
+ * call. With normal probes this includes the probe cache: N * P_g values of
+ * eps z (fp32 weights) or fp16(eps z) (bf16 weights) for the same matrices,
+ * written once per call and read by every timestep instead of regenerating
+ * the probe in every tile (the results are bit-identical either way). With
+ * sign probes it equals zo_workspace_bytes_min. */
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
 
 /* The smallest workspace zo_perturbed_losses accepts: without the probe
@@ -195,7 +198,8 @@ int zo_debug_gauss_pairs(const uint32_t* words, uint64_t n_pairs, float* out, vo
  * zo_profile_read() waits for the recorded events and returns, for one class,
  * the summed time of the timed launches in milliseconds, their number, and
  * the number of all launches of the class since the last enable. */
-enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4, ZO_K_PROBE_CACHE = 5 };
+enum { ZO_K_GATE = 0, ZO_K_HEAD = 1, ZO_K_EMBED = 2, ZO_K_COMBINE = 3, ZO_K_UPDATE = 4, ZO_K_PROBE_CACHE = 5,
+       ZO_K_WEIGHTS16 = 6 };
 int zo_profile_enable(int32_t every);
 int zo_profile_read(int32_t kernel_class, double* timed_ms, int64_t* timed_launches, int64_t* all_launches);
 

@@ -609,10 +609,10 @@ hipError_t zero_async(void* p, size_t bytes, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Probe cache fill: eps z (fp32 weights) or bf16(eps z) (bf16 weights) of
+// Probe cache fill: eps z (fp32 weights) or fp16(eps z) (bf16 weights) of
 // every weight matrix for probes i0 .. i0+N-1 (layout: ZCacheMap). The values
 // are the ones the forward kernels compute when they regenerate the probe:
-// fp32(eps * z) and bf16_rne(eps * z) of the same normal value z. One thread
+// fp32(eps * z) and fp16 (nearest even) of eps * z of the same normal value z. One thread
 // per Philox block (4 values); the matrices are listed by their start in a
 // probe's block and in theta.
 struct ZSegs {
@@ -637,9 +637,8 @@ __global__ __launch_bounds__(256) void zcache_fill_kernel(T* zc, ZSegs segs, Key
       float z[4];
       gauss_block(key, i0 + (uint32_t)n, j >> 2, z);
       if constexpr (sizeof(T) == 2) {
-        const uint32_t lo = (uint32_t)bf16_rne(eps * z[0]) | ((uint32_t)bf16_rne(eps * z[1]) << 16);
-        const uint32_t hi = (uint32_t)bf16_rne(eps * z[2]) | ((uint32_t)bf16_rne(eps * z[3]) << 16);
-        *(uint2*)(zp + u) = uint2{lo, hi};
+        *(uint2*)(zp + u) = uint2{pack_f16x2(fmul(eps, z[0]), fmul(eps, z[1])),
+                                  pack_f16x2(fmul(eps, z[2]), fmul(eps, z[3]))};
       } else {
         *(f4*)(zp + u) = f4{fmul(eps, z[0]), fmul(eps, z[1]), fmul(eps, z[2]), fmul(eps, z[3])};
       }
@@ -647,11 +646,35 @@ __global__ __launch_bounds__(256) void zcache_fill_kernel(T* zc, ZSegs segs, Key
   }
 }
 
+// fp16 copy of the bf16 weight matrices (layout: ZCacheMap), read by the
+// bf16 path's products in place of theta: bf16 -> fp32 is exact and fp32 ->
+// fp16 rounds to nearest even, exact for every bf16 weight in [2^-14, 65504)
+// (smaller ones keep an absolute error below 2^-25). One thread per 8 values;
+// every matrix holds a multiple of 8 values at a multiple of 8 in theta.
+__global__ __launch_bounds__(256) void w16_fill_kernel(const uint16_t* theta, uint16_t* w16, ZSegs segs) {
+  const uint64_t n8 = segs.cstart[segs.n] >> 3;
+  for (uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n8;
+       q += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t u = q << 3;
+    int m = 0;
+    while (m + 1 < segs.n && u >= segs.cstart[m + 1]) ++m;
+    const uint4 v = *(const uint4*)(theta + segs.toff[m] + (u - segs.cstart[m]));
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      o[d] = pack_f16x2(bf16_to_f32((uint16_t)w[d]), bf16_to_f32((uint16_t)(w[d] >> 16)));
+    *(uint4*)(w16 + u) = uint4{o[0], o[1], o[2], o[3]};
+  }
+}
+
 }  // namespace
 
 namespace {
 
-hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
+// The product matrices in theta order: their start in a probe-cache (and
+// fp16-copy) block and in theta.
+ZSegs matrix_segments(const ForwardArgs& a) {
   const zo_config& c = a.cfg;
   ZSegs segs{};
   int m = 0;
@@ -665,6 +688,21 @@ hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
   segs.toff[m++] = a.lay.w_out;
   segs.n = m;
   segs.cstart[m] = a.zmap.pg;
+  return segs;
+}
+
+hipError_t launch_w16_fill(const ForwardArgs& a, hipStream_t st) {
+  const ZSegs segs = matrix_segments(a);
+  uint64_t grid = (a.zmap.pg / 8 + 255) / 256;
+  if (grid > 16384) grid = 16384;
+  ProfScope ps(kKWeights16, st);
+  w16_fill_kernel<<<dim3((unsigned)grid), 256, 0, st>>>((const uint16_t*)a.theta, (uint16_t*)a.w16, segs);
+  return hipGetLastError();
+}
+
+hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
+  const zo_config& c = a.cfg;
+  const ZSegs segs = matrix_segments(a);
   const uint64_t nb = a.zmap.pg / 4;
   uint64_t gx = (nb + 255) / 256;
   if (gx > 4096) gx = 4096;
@@ -820,7 +858,9 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   ZO_TRY(zero_async(cbuf, (size_t)L * M * H * 4, st));
   ZO_TRY(zero_async(row_loss, (size_t)M * 8, st));
 
-  // probe cache (normal probes, when the workspace holds it)
+  // bf16 weights: the fp16 copy of the product matrices; probe cache (normal
+  // probes, when the workspace holds it)
+  if (bf16) ZO_TRY(launch_w16_fill(a, st));
   if (a.zc) ZO_TRY(launch_zcache_fill(a, st));
 
   // bias probes

@@ -1,29 +1,33 @@
-// bf16 kernels of the batched perturbed forward (bf16 weights, bf16 MFMA
+// Kernels of the batched perturbed forward for bf16 weights (fp16 MFMA
 // operands, fp32 accumulation and fp32 cell state).
 //
-// A bf16 weight cannot carry a perturbation of eps = 1e-3 (its spacing near
-// |w| = 1/64 is 6e-5, and a rounded w + eps z would lose several percent of
-// eps z). So every product is two MFMAs into one fp32 accumulator that share
-// the activation fragment:
-//     acc += A . W                (bf16 x bf16)
-//     acc += A . (s eps z)        (s eps z in bf16: +-bf16(eps) for signs,
-//                                  bf16(s eps z) for normal values)
-// The probe term is formed exactly apart from the bf16 rounding of eps z
-// (relative 2^-9), and accumulates in fp32 next to A . W.
+// A bf16 weight cannot carry a perturbation of eps = 1e-3: its spacing near
+// |w| = 1/64 is 1.2e-4, so a rounded w + eps z would lose about 6% of eps z
+// per element. fp16 can: its spacing there is 1.5e-5, so fp16(w + eps z) keeps
+// eps z to within 0.8% per element, and over a K-long product the rounding
+// errors average to a few tenths of a percent of the probe term. So the call
+// first writes an fp16 copy of every weight matrix (exact: bf16 values lie on
+// the fp16 grid in [2^-14, 65504)), activations are stored in fp16, and every
+// product is ONE v_mfma_f32_32x32x16_f16 stream
+//     acc += A . fp16(W + s eps z)
+// whose B fragment each wave forms in registers from the fp16 weight fragment
+// and the probe fragment with one packed fp16 add per pair (+-fp16(eps) for
+// sign probes, expanded from bits; fp16(eps z), sign-flipped for -eps rows,
+// for normal probes). theta +- eps z is never formed in memory.
 //
 // Tiles: a workgroup of 8 waves computes TM = 256 rows x TN = 256 columns
-// (waves 2 x 4, wave tiles 128 x 64 = 4 x 2 tiles of
-// v_mfma_f32_32x32x16_bf16); two waves share each SIMD, so one wave's LDS
-// reads, probe expansion and address work run under the other's matrix
-// instructions. Lane l feeds row/column l % 32 and k block l / 32.
+// (waves 2 x 4, wave tiles 128 x 64 = 4 x 2 tiles of 32x32 MFMA output); two
+// waves share each SIMD, so one wave's LDS reads, probe expansion and address
+// work run under the other's matrix instructions. Lane l feeds row/column
+// l % 32 and k block l / 32.
 //
 // LDS (static, one barrier per K tile): per stage the activation tile
-// [TM][TK] and the weight tile [TN][TK] (bf16 rows of 2 TK bytes whose
+// [TM][TK] and the weight tile [TN][TK] (fp16 rows of 2 TK bytes whose
 // 16-byte chunks are XOR-swizzled by row), copied from global memory straight
 // into LDS without passing through registers, and the probe tile. Sign
 // probes: K tiles of 64 in two stages, the probe tile as sign bits [TN][2]
-// words expanded to bf16 +-eps by each wave. Normal probes: the probe tile is
-// bf16(eps z) [TN][TK], copied from the probe cache like the weights or
+// words expanded to fp16 +-eps by each wave. Normal probes: the probe tile is
+// fp16(eps z) [TN][TK], copied from the probe cache like the weights or
 // generated in registers, which takes a third of the stage; K tiles of 32 in
 // three stages (3 x 48 KB) keep the 256 x 256 tile and so copy 48 KB per 16.8
 // MFLOP of matrix work instead of 64 KB with 256 x 128 tiles of 64. K tile
@@ -39,7 +43,7 @@
 namespace zo {
 namespace {
 
-typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
@@ -58,7 +62,7 @@ struct Tiles {
   static constexpr bool kSigns = kind == ZO_RADEMACHER;
   static constexpr int TK = kSigns ? 64 : 32;       // K per tile
   static constexpr int STAGES = kSigns ? 2 : 3;     // LDS stages
-  static constexpr int RowBytes = TK * 2;           // one LDS row: TK bf16
+  static constexpr int RowBytes = TK * 2;           // one LDS row: TK fp16
   static constexpr int CPR = RowBytes / 16;         // 16-byte chunks per row
   static constexpr int RPB = 256 / RowBytes;        // rows per 256 bytes (every LDS bank once)
   static constexpr int RPC = 1024 / RowBytes;       // rows per 1 KB copy
@@ -120,16 +124,12 @@ __device__ __forceinline__ uint32_t* sign_bits() {
   return S == 0 ? lds_b0 : lds_b1;
 }
 
-__device__ __forceinline__ bf8 as_bf8(u4 v) { return __builtin_bit_cast(bf8, v); }
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)bf16_rne(lo) | ((uint32_t)bf16_rne(hi) << 16);
-}
+__device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
 
 // Probe sign bits in LDS are kept in "unshuffled" order: the word of 32
 // consecutive k holds the negative-sign flags (1 = -1) of the even elements
 // 0, 2, .., 30 in bits 0..15 and of the odd elements 1, 3, .., 31 in bits
-// 16..31. The two elements of one packed bf16 pair then sit 16 bits apart,
+// 16..31. The two elements of one packed fp16 pair then sit 16 bits apart,
 // so one shift, one mask and one xor turn them into the pair (+-e, +-e): the
 // flag of the even element lands on bit 15 and that of the odd one on bit
 // 31, and flip the sign bits of the constant pair (e, e).
@@ -172,21 +172,21 @@ __device__ __forceinline__ void wait_and_barrier() {
 struct SegB {
   const uint16_t* A;  // first row of this workgroup's activation tile; row r at A + r * lda
   int64_t lda;
-  const uint16_t* W;  // weight row n at W + n * ldw (bf16, inside theta)
+  const uint16_t* W;  // weight row n at W + n * ldw (the fp16 copy of the matrix)
   int64_t ldw;
-  uint64_t zoff;      // offset of W inside theta (probe coordinates)
+  uint64_t zoff;      // offset of the matrix inside theta (probe coordinates)
   int K;
-  const uint16_t* Z;  // kGaussCached: bf16(eps z) of this probe and matrix, laid out like W
+  const uint16_t* Z;  // kGaussCached: fp16(eps z) of this probe and matrix, laid out like W
 };
 
 // acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave.
 // colmap(rho, &n) maps LDS column rho (0..TN-1) to a weight row n inside the
 // matrix (columns beyond the matrix map to a valid row; they are never
 // scored). sgn: the sign of eps for this wave's rows (+1, -1, or 0 for the
-// clean pass of forward differences, kFD only); eps_b: bf16 bits of eps.
+// clean pass of forward differences, kFD only); eps_b: fp16 bits of eps.
 // kTrans: accumulate the transposed product (weight columns on the rows of
 // each 32x32 tile, activation rows on its columns): both operands of
-// v_mfma_f32_32x32x16_bf16 have the same fragment layout, so only their order
+// v_mfma_f32_32x32x16_f16 have the same fragment layout, so only their order
 // changes. Lane (lr, lg) then holds, for activation row lr of a tile, the 16
 // columns 8 (v >> 2) + 4 lg + (v & 3), v < 16.
 template <int kind, bool kTrans = false, bool kFD = false, typename ColMap>
@@ -280,8 +280,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         gauss_block(key, probe, (j0 >> 2) + 2 * q + 1, zb);
         const int chunk = (T::ZVALS / 8) * zpart + q;
         *(u4*)(zrow + 16 * (chunk ^ T::swz(zr))) =
-            u4{pack_bf16x2(eps * za[0], eps * za[1]), pack_bf16x2(eps * za[2], eps * za[3]),
-               pack_bf16x2(eps * zb[0], eps * zb[1]), pack_bf16x2(eps * zb[2], eps * zb[3])};
+            u4{pack_f16x2(eps * za[0], eps * za[1]), pack_f16x2(eps * za[2], eps * za[3]),
+               pack_f16x2(eps * zb[0], eps * zb[1]), pack_f16x2(eps * zb[2], eps * zb[3])};
       }
     }
     if constexpr (P == 3) {
@@ -308,14 +308,14 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   const uint32_t y = (uint32_t)(lg ^ T::swz(lr));
   const uint32_t a_lane = (uint32_t)(T::WROWS * wm + lr) * T::RowBytes;
   const uint32_t w_lane = (uint32_t)(64 * wn + lr) * T::RowBytes;
-  // the pair (s eps, s eps) in bf16 (signs), or the sign flip of -eps rows (normal)
+  // the pair (s eps, s eps) in fp16 (signs), or the sign flip of -eps rows (normal)
   const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
   const bool neg = sgn < 0;
   const uint32_t zc = kind == ZO_RADEMACHER ? (neg ? ebits ^ 0x80008000u : ebits) : (neg ? 0x80008000u : 0u);
   // forward differences: the clean pass multiplies its probe fragments by 0
   const uint32_t zmask = sgn == 0 ? 0u : 0xFFFFFFFFu;
   struct Frag {
-    bf8 a[MT], w[2], z[2];
+    h8 a[MT], w[2], z[2];
   };
   auto compute = [&](auto stage_tag, bool more) {
     constexpr int S = decltype(stage_tag)::value;
@@ -337,10 +337,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     auto load = [&](int s, Frag& f) {
       const uint32_t so = 16u * ((uint32_t)(2 * s) ^ y);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_bf8(*(const u4*)(pa + 32 * mt * T::RowBytes + so));
+      for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_h8(*(const u4*)(pa + 32 * mt * T::RowBytes + so));
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        f.w[nt] = as_bf8(*(const u4*)(pw + 32 * nt * T::RowBytes + so));
+        f.w[nt] = as_h8(*(const u4*)(pw + 32 * nt * T::RowBytes + so));
         u4 v;
         if constexpr (kind == ZO_RADEMACHER) {
           const uint32_t x = bits[nt][s >> 1];
@@ -357,7 +357,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
             if constexpr (kFD) v[d] &= zmask;
           }
         }
-        f.z[nt] = as_bf8(v);
+        f.z[nt] = as_h8(v);
       }
     };
     Frag f[2];
@@ -366,20 +366,17 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     for (int s = 0; s < TK / 16; ++s) {
       const Frag& c = f[s & 1];
       if (s + 1 < TK / 16) load(s + 1, f[(s + 1) & 1]);
-      // weight products of every accumulator first, then the probe products,
-      // so that two MFMAs into one accumulator are 2 MT apart
+      // B = fp16(W + s eps z): one packed fp16 add per pair (round to
+      // nearest even), then one MFMA per accumulator
+      h8 wz[2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) wz[nt] = c.w[nt] + c.z[nt];
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.w[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
-                               : __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.w[nt], acc[mt][nt], 0, 0, 0);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.z[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
-                               : __builtin_amdgcn_mfma_f32_32x32x16_bf16(c.a[mt], c.z[nt], acc[mt][nt], 0, 0, 0);
+          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_f16(wz[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
+                               : __builtin_amdgcn_mfma_f32_32x32x16_f16(c.a[mt], wz[nt], acc[mt][nt], 0, 0, 0);
       if (more) {
         // tile it + STAGES - 1 goes to the stage tile it - 1 used
         constexpr std::integral_constant<int, (S + T::STAGES - 1) % T::STAGES> next{};
@@ -404,7 +401,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         // a few VALU instructions of the next step's probe fragments
         __builtin_amdgcn_sched_group_barrier(0x100, MT + 2 + (kind == ZO_RADEMACHER ? 0 : 2), 0);
 #pragma unroll
-        for (int i = 0; i < 4 * MT; ++i) {
+        for (int i = 0; i < 2 * MT; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
@@ -497,6 +494,8 @@ struct GateArgsB {
   const uint16_t* zc_ih;  // probe cache: W_ih's and W_hh's values of probe 0; probe n at + n * zc_stride
   const uint16_t* zc_hh;
   uint64_t zc_stride;
+  const uint16_t* w_ih16;  // fp16 copies of W_ih and W_hh
+  const uint16_t* w_hh16;
 };
 
 // Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
@@ -523,9 +522,9 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   f16v acc[T::MT][2];
   zero_acc(acc);
   const uint64_t zpos = (uint64_t)pair * g.zc_stride;
-  const SegB s0{g.x + m0 * g.El, g.El, g.theta + g.off_ih, g.El, g.off_ih, g.El,
+  const SegB s0{g.x + m0 * g.El, g.El, g.w_ih16, g.El, g.off_ih, g.El,
                 kind == kGaussCached ? g.zc_ih + zpos : nullptr};
-  const SegB s1{g.hprev + m0 * H, H, g.theta + g.off_hh, H, g.off_hh, H,
+  const SegB s1{g.hprev + m0 * H, H, g.w_hh16, H, g.off_hh, H,
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   mainloop_bf16<kind, false, kFD>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
 
@@ -558,14 +557,14 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
       const int64_t o = (m0 + lrow) * H + u;
       const float c = sigm(fp) * g.cst[o] + sigm(ip) * tanh_(gp);
       g.cst[o] = c;
-      g.hout[o] = bf16_rne(sigm(op) * tanh_(c));
+      g.hout[o] = f16_bits(sigm(op) * tanh_(c));
     }
   }
 }
 
 // ---------------------------------------------------------------------------
 struct HeadArgsB {
-  const uint16_t* h;  // [rows][H] bf16
+  const uint16_t* h;  // [rows][H] fp16
   const uint16_t* theta;
   uint64_t off_w, off_b;
   int H, V;
@@ -584,6 +583,7 @@ struct HeadArgsB {
   int nvt;  // vocabulary tiles
   const uint16_t* zc_out;  // probe cache: W_out's values of probe 0; probe n at + n * zc_stride
   uint64_t zc_stride;
+  const uint16_t* w_out16;  // fp16 copy of W_out
 };
 
 template <int kind, bool kFD>
@@ -604,7 +604,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
   f16v acc[T::MT][2];
   zero_acc(acc);
-  const SegB s0{g.h + rr0 * g.H, g.H, g.theta + g.off_w, g.H, g.off_w, g.H,
+  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, g.H, g.off_w, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   mainloop_bf16<kind, true, kFD>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
 
@@ -683,7 +683,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
 }
 
 // ---------------------------------------------------------------------------
-// x0[r][e] = bf16(EMB[tok][e] + s eps z_n[emb + tok E + e]); zeros for padding rows.
+// x0[r][e] = fp16(EMB[tok][e] + s eps z_n[emb + tok E + e]); zeros for padding rows.
 template <int kind>
 __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, uint64_t emb_off, int E,
                                                          const int32_t* tokens, int C, int t, int B,
@@ -712,8 +712,8 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
       gauss_block(key, i0 + pair, j >> 2, z);
     }
     const float se = (float)ps.sign * eps;  // 0 for the clean pass
-    lo = pack_bf16x2(w[0] + se * z[0], w[1] + se * z[1]);
-    hi = pack_bf16x2(w[2] + se * z[2], w[3] + se * z[3]);
+    lo = pack_f16x2(w[0] + se * z[0], w[1] + se * z[1]);
+    hi = pack_f16x2(w[2] + se * z[2], w[3] + se * z[3]);
   }
   *(uint2*)(x0 + r * E + e) = uint2{lo, hi};
 }
@@ -746,7 +746,7 @@ __global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* the
         const int k = 8 * q + 2 * d;
         const float w0 = bf16_to_f32((uint16_t)wv[d]), w1 = bf16_to_f32((uint16_t)(wv[d] >> 16));
         const float z0 = ((word >> k) & 1u) ? 1.0f : -1.0f, z1 = ((word >> (k + 1)) & 1u) ? 1.0f : -1.0f;
-        out[q][d] = pack_bf16x2(w0 + se * z0, w1 + se * z1);
+        out[q][d] = pack_f16x2(w0 + se * z0, w1 + se * z1);
       }
     }
   }
@@ -796,9 +796,11 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.key = make_key(a.seed);
   g.i0 = a.i0;
   g.eps = a.eps;
-  g.eps_b = bf16_rne(a.eps);
+  g.eps_b = f16_rne(a.eps);
   g.rm = row_map(R);
   g.n_row_blocks = (int)(R.M / TM);
+  g.w_ih16 = (const uint16_t*)a.w16 + a.zmap.ih[l];
+  g.w_hh16 = (const uint16_t*)a.w16 + a.zmap.hh[l];
   g.zc_ih = a.zc ? (const uint16_t*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const uint16_t*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
@@ -833,7 +835,8 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.key = make_key(a.seed);
   h.i0 = a.i0;
   h.eps = a.eps;
-  h.eps_b = bf16_rne(a.eps);
+  h.eps_b = f16_rne(a.eps);
+  h.w_out16 = (const uint16_t*)a.w16 + a.zmap.out;
   h.rm = row_map(R);
   h.M = R.M;
   h.rows = (int64_t)Tc * R.M;

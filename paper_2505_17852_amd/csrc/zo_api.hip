@@ -126,6 +126,7 @@ static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, 
   // the probe cache is used when the workspace has room for it
   a.zc = (zo::probe_cache_kind(*cfg) && ws_bytes >= plan.total) ? (char*)workspace + plan.zcache : nullptr;
   a.zmap = zo::make_zcache_map(*cfg);
+  a.w16 = cfg->wdtype == ZO_WBF16 ? (char*)workspace + plan.w16 : nullptr;
   return device_status(zo::launch_forward(a, (hipStream_t)stream), name);
 }
 

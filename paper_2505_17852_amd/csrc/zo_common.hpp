@@ -174,6 +174,7 @@ struct WsPlan {
   size_t psum;       // f32 [nvt][T*M]     per vocabulary tile: sum of exp(y - max)
   size_t ptgt;       // f32 [T*M]          target logit
   size_t row_loss;   // f64 [M]            masked loss sum of each row
+  size_t w16;        // f16 [P_g]          bf16 weights: the product matrices in fp16 (ZCacheMap layout)
   size_t min_total;  // bytes without the probe cache
   size_t zcache;     // probe cache [N][P_g] (normal probes; see ZCacheMap)
   size_t total;      // bytes with the probe cache (= min_total for sign probes)
@@ -206,6 +207,8 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
   w.psum = take((size_t)w.nvt * w.T * M * 4);
   w.ptgt = take((size_t)w.T * M * 4);
   w.row_loss = take(M * 8);
+  w.w16 = p;
+  if (c.wdtype == ZO_WBF16) take((size_t)make_zcache_map(c).pg * 2);
   w.min_total = p;
   w.zcache = p;
   if (probe_cache_kind(c)) take((size_t)r.N * make_zcache_map(c).pg * (c.wdtype == ZO_WBF16 ? 2 : 4));

@@ -40,6 +40,7 @@ struct ForwardArgs {
   char* work;
   bool fp32_split;  // fp32 path: separate W.h and probe MFMA streams (measurement variant)
   void* zc;         // probe cache inside work, or nullptr (probes regenerated in every tile)
+  void* w16;        // bf16 weights: fp16 copy of the product matrices inside work (ZCacheMap layout)
   ZCacheMap zmap;
 };
 hipError_t launch_forward(const ForwardArgs& a, hipStream_t s);

@@ -10,7 +10,7 @@
 namespace zo {
 
 enum KernelClass { kKGate = 0, kKHead = 1, kKEmbed = 2, kKCombine = 3, kKUpdate = 4, kKProbeCache = 5,
-                   kKClasses = 6 };
+                   kKWeights16 = 6, kKClasses = 7 };
 
 extern std::atomic<int> g_profile_on;  // 0: off; n >= 1: time every n-th launch of a class
 

@@ -210,4 +210,40 @@ __host__ __device__ inline uint16_t bf16_rne(float f) {
 }
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// fp32 -> fp16 bits, round to nearest even (subnormals kept, overflow to
+// infinity, NaN kept quiet); the host's conversion of eps, bit-equal to the
+// device's v_cvt_f16_f32 under its default rounding.
+__host__ __device__ inline uint16_t f16_rne(float f) {
+  uint32_t x;
+  __builtin_memcpy(&x, &f, 4);
+  const uint32_t sign = (x >> 16) & 0x8000u;
+  x &= 0x7FFFFFFFu;
+  if (x >= 0x7F800000u) return (uint16_t)(sign | (x > 0x7F800000u ? 0x7E00u : 0x7C00u));
+  if (x >= 0x477FF000u) return (uint16_t)(sign | 0x7C00u);  // >= 65520 rounds to infinity
+  uint32_t h, rem, half;
+  if (x >= 0x38800000u) {  // normal: rebias the exponent (127 -> 15), round off 13 bits
+    const uint32_t r = x - 0x38000000u;
+    h = r >> 13;
+    rem = r & 0x1FFFu;
+    half = 0x1000u;
+  } else {  // subnormal or zero: round(|f| 2^24)
+    const int shift = 126 - (int)(x >> 23);
+    if (shift > 24) return (uint16_t)sign;
+    const uint32_t m = (x & 0x007FFFFFu) | 0x00800000u;
+    h = m >> shift;
+    rem = m & ((1u << shift) - 1u);
+    half = 1u << (shift - 1);
+  }
+  if (rem > half || (rem == half && (h & 1u))) ++h;
+  return (uint16_t)(sign | h);
+}
+
+// Two fp32 values to packed fp16 (round to nearest even), low half first.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){lo, hi}, h2));
+}
+__device__ __forceinline__ uint16_t f16_bits(float x) { return __builtin_bit_cast(uint16_t, (_Float16)x); }
+
 }  // namespace zo

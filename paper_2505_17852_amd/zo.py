@@ -263,9 +263,9 @@ def debug_gauss_pairs(words: torch.Tensor, stream=None) -> torch.Tensor:
     return out
 
 
-K_GATE, K_HEAD, K_EMBED, K_COMBINE, K_UPDATE, K_PROBE_CACHE = 0, 1, 2, 3, 4, 5
+K_GATE, K_HEAD, K_EMBED, K_COMBINE, K_UPDATE, K_PROBE_CACHE, K_WEIGHTS16 = 0, 1, 2, 3, 4, 5, 6
 KERNEL_CLASSES = {"gate": K_GATE, "head": K_HEAD, "embed": K_EMBED, "combine": K_COMBINE,
-                  "update": K_UPDATE, "probe_cache": K_PROBE_CACHE}
+                  "update": K_UPDATE, "probe_cache": K_PROBE_CACHE, "weights16": K_WEIGHTS16}
 
 
 def profile_enable(every: int = 1):
