@@ -56,12 +56,17 @@ constexpr int NT = 64 * NWAVES;  // threads per workgroup
 constexpr int kCopyWaves = 4;
 constexpr int kCopySteps = 1;
 
+// Sign probes: K per tile and LDS stages.
+constexpr int kSignTK = 64;
+constexpr int kSignStages = 2;
+
 // Per probe kind: K tile, stages, LDS layout, copy split, probe roles.
 template <int kind>
 struct Tiles {
   static constexpr bool kSigns = kind == ZO_RADEMACHER;
-  static constexpr int TK = kSigns ? 64 : 32;       // K per tile
-  static constexpr int STAGES = kSigns ? 2 : 3;     // LDS stages
+  static constexpr int TK = kSigns ? kSignTK : 32;           // K per tile
+  static constexpr int STAGES = kSigns ? kSignStages : 3;    // LDS stages
+  static constexpr int SW = TK / 32;                         // sign words per row and tile
   static constexpr int RowBytes = TK * 2;           // one LDS row: TK fp16
   static constexpr int CPR = RowBytes / 16;         // 16-byte chunks per row
   static constexpr int RPB = 256 / RowBytes;        // rows per 256 bytes (every LDS bank once)
@@ -73,7 +78,7 @@ struct Tiles {
   static constexpr int WROWS = TM / WAVES_M;  // rows per wave tile
   static constexpr int MT = WROWS / 32;
   static constexpr int WBytes = TN * RowBytes;
-  static constexpr int ZBytes = kSigns ? TN * 8 : TN * RowBytes;
+  static constexpr int ZBytes = kSigns ? TN * 4 * SW : TN * RowBytes;
   static constexpr int StageBytes = ABytes + WBytes + (kSigns ? 0 : ZBytes);  // sign bits: own arrays
   static constexpr int ACopies = ABytes / 1024 / kCopyWaves;  // activation copies per copying wave
   static constexpr int WCopies = WBytes / 1024 / kCopyWaves;  // weight copies per copying wave
@@ -92,7 +97,8 @@ struct Tiles {
   static_assert(WCopies * kCopyWaves * 1024 == WBytes && ACopies * kCopyWaves * 1024 == ABytes,
                 "copy split");
   static_assert(Copies < 64, "outstanding copies fit the vmcnt counter");
-  static_assert(!kSigns || TN * 2 == NT, "one sign word per thread");
+  static_assert(!kSigns || TN * SW <= NT, "at most one sign word per thread");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
   static_assert(kSigns || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
   static_assert(TK % 16 == 0 && (TK / 16 == 4 || TK / 16 == 2), "k steps per tile");
@@ -103,8 +109,12 @@ static_assert(Tiles<kGaussCached>::StageBytes == Tiles<ZO_GAUSSIAN>::StageBytes,
 // LDS stages per probe kind (static, so that every offset is a constant).
 __shared__ __align__(16) uint8_t lds_r0[Tiles<ZO_RADEMACHER>::StageBytes];
 __shared__ __align__(16) uint8_t lds_r1[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_r2[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_r3[Tiles<ZO_RADEMACHER>::StageBytes];
 __shared__ __align__(16) uint32_t lds_b0[Tiles<ZO_RADEMACHER>::ZBytes / 4];
 __shared__ __align__(16) uint32_t lds_b1[Tiles<ZO_RADEMACHER>::ZBytes / 4];
+__shared__ __align__(16) uint32_t lds_b2[Tiles<ZO_RADEMACHER>::ZBytes / 4];
+__shared__ __align__(16) uint32_t lds_b3[Tiles<ZO_RADEMACHER>::ZBytes / 4];
 __shared__ __align__(16) uint8_t lds_g0[Tiles<ZO_GAUSSIAN>::StageBytes];
 __shared__ __align__(16) uint8_t lds_g1[Tiles<ZO_GAUSSIAN>::StageBytes];
 __shared__ __align__(16) uint8_t lds_g2[Tiles<ZO_GAUSSIAN>::StageBytes];
@@ -115,13 +125,14 @@ template <int kind, int S>
 __device__ __forceinline__ uint8_t* stage() {
   static_assert(S >= 0 && S < Tiles<kind>::STAGES, "stage index");
   if constexpr (kind == ZO_RADEMACHER)
-    return S == 0 ? lds_r0 : lds_r1;
+    return S == 0 ? lds_r0 : S == 1 ? lds_r1 : S == 2 ? lds_r2 : lds_r3;
   else
     return S == 0 ? lds_g0 : S == 1 ? lds_g1 : lds_g2;
 }
 template <int S>
 __device__ __forceinline__ uint32_t* sign_bits() {
-  return S == 0 ? lds_b0 : lds_b1;
+  static_assert(S >= 0 && S < Tiles<ZO_RADEMACHER>::STAGES, "stage index");
+  return S == 0 ? lds_b0 : S == 1 ? lds_b1 : S == 2 ? lds_b2 : lds_b3;
 }
 
 __device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
@@ -221,10 +232,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     colmap(r, wrow[q]);
     woff[q] = 8u * (uint32_t)((lane % T::CPR) ^ T::swz(r));
   }
-  // probe roles: signs, every thread: row t >> 1, one 32-k word at 32 (t & 1);
+  // probe roles: signs, threads t < TN SW: row t / SW, one 32-k word at 32 (t % SW);
   //              normal, every thread: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
-  const int zr = kind == ZO_RADEMACHER ? t >> 1 : t / T::ZROW_T;
-  const int zpart = kind == ZO_RADEMACHER ? (t & 1) : (t % T::ZROW_T);
+  const int zr = kind == ZO_RADEMACHER ? t / T::SW : t / T::ZROW_T;
+  const int zpart = kind == ZO_RADEMACHER ? (t % T::SW) : (t % T::ZROW_T);
   int zn;
   colmap(zr, zn);
 
@@ -258,6 +269,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       }
     }
     if constexpr (P == 2 && kind == ZO_RADEMACHER) {
+      if (T::TN * T::SW == NT || t < T::TN * T::SW) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 32 * zpart;
       uint32_t word;
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
@@ -269,7 +281,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         word = rademacher_word(key, probe, j0 >> 5);
       }
       // negative-sign flags in unshuffled order
-      sign_bits<S>()[zr * 2 + zpart] = unshuffle_bits(~word);
+      sign_bits<S>()[zr * T::SW + zpart] = unshuffle_bits(~word);
+      }
     } else if constexpr (P == 2 && kind == ZO_GAUSSIAN) {
       const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
       uint8_t* zrow = base + T::ABytes + T::WBytes + zr * T::RowBytes;
@@ -329,9 +342,14 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       const uint32_t pre = 4u * (uint32_t)(1 - lg);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const uint2 v = *(const uint2*)(sign_bits<S>() + (64 * wn + 32 * nt + lr) * 2);
-        bits[nt][0] = v.x << pre;
-        bits[nt][1] = v.y << pre;
+        if constexpr (T::SW == 2) {
+          const uint2 v = *(const uint2*)(sign_bits<S>() + (64 * wn + 32 * nt + lr) * 2);
+          bits[nt][0] = v.x << pre;
+          bits[nt][1] = v.y << pre;
+        } else {
+          bits[nt][0] = sign_bits<S>()[64 * wn + 32 * nt + lr] << pre;
+          bits[nt][1] = 0u;
+        }
       }
     }
     auto load = [&](int s, Frag& f) {
@@ -415,23 +433,34 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // every wave, and the stage computed at it - 1 free); compute it while
   // issuing tile it + STAGES - 1 into that stage.
   auto step = [&](auto stage_tag, int it) {
-    if constexpr (T::STAGES == 2) {
-      wait_and_barrier<0>();
-    } else {
+    // the copies of tiles it + 1 .. it + STAGES - 2 (those issued) may stay in flight
+    if constexpr (T::STAGES == 4) {
+      if (it + 2 < ntiles) wait_and_barrier<2 * T::Copies>();
+      else if (it + 1 < ntiles) wait_and_barrier<T::Copies>();
+      else wait_and_barrier<0>();
+    } else if constexpr (T::STAGES == 3) {
       if (it + 1 < ntiles) wait_and_barrier<T::Copies>();
       else wait_and_barrier<0>();
+    } else {
+      wait_and_barrier<0>();
     }
     compute(stage_tag, it + T::STAGES - 1 < ntiles);
   };
   issue_all(std::integral_constant<int, 0>{});
-  if constexpr (T::STAGES == 3) {
+  if constexpr (T::STAGES >= 3) {
     if (ntiles > 1) issue_all(std::integral_constant<int, 1>{});
+  }
+  if constexpr (T::STAGES >= 4) {
+    if (ntiles > 2) issue_all(std::integral_constant<int, 2>{});
   }
   for (int it = 0; it < ntiles; it += T::STAGES) {
     step(std::integral_constant<int, 0>{}, it);
     if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
-    if constexpr (T::STAGES == 3) {
-      if (it + 2 < ntiles) step(std::integral_constant<int, 2>{}, it + 2);
+    if constexpr (T::STAGES >= 3) {
+      if (it + 2 < ntiles) step(std::integral_constant<int, 2 % T::STAGES>{}, it + 2);
+    }
+    if constexpr (T::STAGES >= 4) {
+      if (it + 3 < ntiles) step(std::integral_constant<int, 3 % T::STAGES>{}, it + 3);
     }
   }
   __syncthreads();  // every wave done with the stages before they are reused
