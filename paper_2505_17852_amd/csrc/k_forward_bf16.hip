@@ -54,7 +54,7 @@ constexpr int NT = 64 * NWAVES;  // threads per workgroup
 // kCopyWaves of the 8 waves issue them, spread over the first kCopySteps k
 // steps of the previous K tile.
 constexpr int kCopyWaves = 4;
-constexpr int kCopySteps = 1;
+constexpr int kCopySteps = 2;
 
 // Sign probes: K per tile and LDS stages.
 constexpr int kSignTK = 64;
