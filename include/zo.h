@@ -122,8 +122,13 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
  *            set gives bit-identical losses to the same probes in the full set)
  *   tokens   device int32 [B][C+1], ids in [0, V): position t reads token
  *            tokens[b][t] and is scored on the next token tokens[b][t+1]
- *            (teacher forcing). Ids outside [0, V) are not checked on the
- *            device: the caller guarantees the range.
+ *            (teacher forcing). Ids outside [0, V) are never used to address
+ *            memory: an input id outside the range makes that sequence's
+ *            states NaN from its position on, and a scored target id outside
+ *            it makes that position's loss NaN, so the losses it reaches are
+ *            not finite (zo_update then skips, see skipped_out); an id that
+ *            only serves as an unscored target changes nothing. The call
+ *            itself still returns ZO_OK: the ids are not read on the host.
  *   mask     device uint8 [B][C] or NULL (all positions scored)
  *   Lplus, Lminus  device fp32 [N]: the masked mean over (b, t) of the
  *            next-token cross-entropy in nats at theta + eps z and at

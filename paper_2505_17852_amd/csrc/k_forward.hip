@@ -71,10 +71,11 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(int kind, Key key, uint3
 
 // ---------------------------------------------------------------------------
 // x0[tt][r][e] = EMB[tok][e] + s eps z_n[emb + tok E + e] for the input token
-// of row r at time t0 + tt, tt < Tc; zeros for padding rows. One thread per 4
-// elements; one launch per time chunk.
+// of row r at time t0 + tt, tt < Tc; zeros for padding rows, NaN for a token
+// outside [0, V) (never read). One thread per 4 elements; one launch per time
+// chunk.
 template <int kind>
-__global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint64_t emb_off, int E,
+__global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint64_t emb_off, int E, int V,
                                                         const int32_t* tokens, int C, int t0, int Tc, int B,
                                                         RowMap rm, int64_t M, Key key, uint32_t i0,
                                                         float eps, float* x0) {
@@ -90,8 +91,10 @@ __global__ __launch_bounds__(256) void embed_f32_kernel(const float* theta, uint
     const PassOf ps = pass_of(rm, r);
     const int pair = ps.probe, b = ps.b;
     f4 out = {0.f, 0.f, 0.f, 0.f};
-    if (b < B) {
-      const int tok = tokens[(int64_t)b * (C + 1) + t];
+    const int tok = b < B ? tokens[(int64_t)b * (C + 1) + t] : 0;
+    if (b < B && (uint32_t)tok >= (uint32_t)V) {
+      out = f4{__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf("")};
+    } else if (b < B) {
       const uint64_t j = emb_off + (uint64_t)tok * E + e;
       const f4 w = *(const f4*)(theta + j);
       float z[4];
@@ -514,11 +517,12 @@ __global__ __launch_bounds__(256) void head_f32_kernel(HeadArgs g) {
 // Cross-entropy of every position of the chunk: logsumexp over the
 // vocabulary tiles' (max, sum of exp) partials, merged online in tile order,
 // minus the target logit. One thread per (timestep, row); the loss replaces
-// the target logit in ptgt (0 for unscored positions and padding rows).
+// the target logit in ptgt (0 for unscored positions and padding rows, NaN
+// for a scored position whose target token lies outside [0, V)).
 __global__ __launch_bounds__(256) void combine_kernel(const float* pmax, const float* psum,
                                                       float* ptgt, int nvt, int64_t rows,
                                                       int64_t M, int t0, int C, int B, RowMap rm,
-                                                      const uint8_t* mask) {
+                                                      const uint8_t* mask, const int32_t* tokens, int V) {
   const int64_t rr = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (rr >= rows) return;
   const int tt = (int)(rr / M);
@@ -526,6 +530,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* pmax, const f
   const int b = pass_of(rm, r).b;
   if (b >= B || (mask && !mask[(int64_t)b * C + t0 + tt])) {
     ptgt[rr] = 0.f;
+    return;
+  }
+  if ((uint32_t)tokens[(int64_t)b * (C + 1) + t0 + tt + 1] >= (uint32_t)V) {
+    ptgt[rr] = __builtin_nanf("");
     return;
   }
   float mx = -INFINITY, s = 0.f;
@@ -729,11 +737,11 @@ hipError_t launch_embed_f32(const ForwardArgs& a, int t0, int Tc, void* x0, hipS
   ProfScope ps(kKEmbed, st);
   if (a.cfg.probe == ZO_RADEMACHER)
     embed_f32_kernel<ZO_RADEMACHER><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
-                                                          a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
+                                                          a.cfg.vocab, a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
                                                           a.eps, (float*)x0);
   else
     embed_f32_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>((const float*)a.theta, a.lay.emb, E,
-                                                        a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
+                                                        a.cfg.vocab, a.tokens, a.C, t0, Tc, R.B, rm, R.M, key, a.i0,
                                                         a.eps, (float*)x0);
   return hipGetLastError();
 }
@@ -938,7 +946,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
       ProfScope ps(kKCombine, st);
       const int64_t rows = (int64_t)Tc * M;
       combine_kernel<<<dim3((unsigned)((rows + 255) / 256)), 256, 0, st>>>(
-          pmax, psum, ptgt, W.nvt, rows, M, t0, a.C, R.B, rm, a.mask);
+          pmax, psum, ptgt, W.nvt, rows, M, t0, a.C, R.B, rm, a.mask, a.tokens, a.cfg.vocab);
       ZO_TRY(hipGetLastError());
       accumulate_kernel<<<dim3((unsigned)((M + 255) / 256)), 256, 0, st>>>(ptgt, M, Tc, row_loss);
       ZO_TRY(hipGetLastError());

@@ -712,9 +712,11 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
 }
 
 // ---------------------------------------------------------------------------
-// x0[r][e] = fp16(EMB[tok][e] + s eps z_n[emb + tok E + e]); zeros for padding rows.
+// x0[r][e] = fp16(EMB[tok][e] + s eps z_n[emb + tok E + e]); zeros for padding
+// rows, NaN for a token outside [0, V) (never read).
+constexpr uint32_t kNaNf16x2 = 0x7E007E00u;
 template <int kind>
-__global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, uint64_t emb_off, int E,
+__global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, uint64_t emb_off, int E, int V,
                                                          const int32_t* tokens, int C, int t, int B,
                                                          RowMap rm, int64_t M, Key key, uint32_t i0,
                                                          float eps, uint16_t* x0) {
@@ -726,8 +728,10 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
   const PassOf ps = pass_of(rm, r);
   const int pair = ps.probe, b = ps.b;
   uint32_t lo = 0u, hi = 0u;
-  if (b < B) {
-    const int tok = tokens[(int64_t)b * (C + 1) + t];
+  const int tok = b < B ? tokens[(int64_t)b * (C + 1) + t] : 0;
+  if (b < B && (uint32_t)tok >= (uint32_t)V) {
+    lo = hi = kNaNf16x2;
+  } else if (b < B) {
     const uint64_t j = emb_off + (uint64_t)tok * E + e;
     const uint2 wv = *(const uint2*)(theta + j);
     float w[4] = {bf16_to_f32((uint16_t)wv.x), bf16_to_f32((uint16_t)(wv.x >> 16)),
@@ -750,7 +754,7 @@ __global__ __launch_bounds__(256) void embed_bf16_kernel(const uint16_t* theta, 
 // Sign probes: one thread per 32 consecutive elements of a row, which share
 // one Philox word (bit k of the word for element k), so a row costs E / 128
 // Philox blocks instead of E / 4.
-__global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* theta, uint64_t emb_off, int E,
+__global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* theta, uint64_t emb_off, int E, int V,
                                                              const int32_t* tokens, int C, int t, int B,
                                                              RowMap rm, int64_t M, Key key, uint32_t i0,
                                                              float eps, uint16_t* x0) {
@@ -762,8 +766,11 @@ __global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* the
   const PassOf ps = pass_of(rm, r);
   const int pair = ps.probe, b = ps.b;
   u4 out[4] = {u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}, u4{0u, 0u, 0u, 0u}};
-  if (b < B) {
-    const int tok = tokens[(int64_t)b * (C + 1) + t];
+  const int tok = b < B ? tokens[(int64_t)b * (C + 1) + t] : 0;
+  if (b < B && (uint32_t)tok >= (uint32_t)V) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) out[q] = u4{kNaNf16x2, kNaNf16x2, kNaNf16x2, kNaNf16x2};
+  } else if (b < B) {
     const uint64_t j = emb_off + (uint64_t)tok * E + e;  // a multiple of 32: one whole word
     const uint32_t word = rademacher_word(key, i0 + pair, j >> 5);
     const float se = (float)ps.sign * eps;  // 0 for the clean pass
@@ -795,13 +802,13 @@ hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t 
   if (a.cfg.probe == ZO_RADEMACHER) {
     const int64_t n = R.M * (E / 32);
     const unsigned grid = (unsigned)((n + 255) / 256);
-    embed_bf16_rad_kernel<<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E, a.tokens, a.C, t, R.B,
+    embed_bf16_rad_kernel<<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E, a.cfg.vocab, a.tokens, a.C, t, R.B,
                                                 rm, R.M, key, a.i0, a.eps, (uint16_t*)x0);
   } else {
     const int64_t n = R.M * (E / 4);
     const unsigned grid = (unsigned)((n + 255) / 256);
     embed_bf16_kernel<ZO_GAUSSIAN><<<grid, 256, 0, st>>>((const uint16_t*)a.theta, a.lay.emb, E,
-                                                         a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
+                                                         a.cfg.vocab, a.tokens, a.C, t, R.B, rm, R.M, key, a.i0,
                                                          a.eps, (uint16_t*)x0);
   }
   return hipGetLastError();

@@ -150,8 +150,10 @@ def perturbed_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int,
                      check_tokens: bool = True):
     """Returns (L+, L-) as device fp32 tensors of N elements (asynchronous).
 
-    The kernels do not range-check token ids; with check_tokens (default)
-    this wrapper verifies 0 <= id < vocab first (one device sync)."""
+    The kernels never read memory by an id outside [0, vocab): such an id
+    makes the affected losses non-finite (and zo_update then skips). With
+    check_tokens (default) this wrapper rejects them first (one device
+    sync)."""
     c = _cfg(cfg)
     if tokens.dim() != 2:
         raise ValueError("tokens must be [B][C+1]")

@@ -145,3 +145,59 @@ def test_deep_stack(zo, oracle, wdtype):
     rng = np.random.default_rng(19)
     tok = wl.uniform_tokens(rng, 2, 12, cfg["vocab"])
     check(*run_both(zo, oracle, cfg, 1, tok, None, 1e-2), RTOL[wdtype])
+
+
+BADTOK = [
+    ("fp32", dict(n_layers=1, vocab=50, embed=32, hidden=32, wdtype=wl.FP32, probe=wl.RADEMACHER)),
+    ("fp32-gauss", dict(n_layers=1, vocab=50, embed=32, hidden=32, wdtype=wl.FP32, probe=wl.GAUSSIAN)),
+    ("bf16", dict(n_layers=1, vocab=50, embed=64, hidden=64, wdtype=wl.BF16, probe=wl.RADEMACHER)),
+    ("bf16-gauss", dict(n_layers=1, vocab=50, embed=64, hidden=64, wdtype=wl.BF16, probe=wl.GAUSSIAN)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", BADTOK, ids=[g[0] for g in BADTOK])
+def test_out_of_range_tokens_poison_losses_and_skip_update(zo, oracle, name, cfg):
+    """Token ids outside [0, V) are never read: an input id makes the
+    sequence's states NaN from there on, a scored target id makes that
+    position's loss NaN, so every loss is non-finite and the update skips
+    with theta unchanged; an id used only as an unscored target changes
+    nothing; the next call on valid tokens is unaffected."""
+    V, B, Cn, N, eps, seed = cfg["vocab"], 3, 6, 2, 1e-2, 77
+    rng = np.random.default_rng(5)
+    tok = wl.uniform_tokens(rng, B, Cn, V)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 21)
+    before = theta.clone()
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for bad in (V, -1, 2 ** 31 - 1):
+        for where in ("input", "target"):
+            t = tok.copy()
+            if where == "input":
+                t[1, 2] = bad  # input at position 2, target of position 1 (scored)
+            else:
+                t[0, Cn] = bad  # target of the last position only
+            say(f"{name}: token {bad} as {where}")
+            td = torch.from_numpy(t).cuda()
+            Lp, Lm = zo.perturbed_losses(cfg, theta, seed, eps, N, td, None, check_tokens=False)
+            L, L0 = zo.fd_losses(cfg, theta, seed, eps, N, td, None, check_tokens=False)
+            for x in (Lp, Lm, L, L0):
+                assert not torch.isfinite(x).any().item(), (where, x)
+            zo.update(cfg, theta, seed, eps, 1e-3, Lp, Lm, skipped=flag)
+            assert flag.item() == 1
+            assert torch.equal(theta.view(torch.int32), before.view(torch.int32))
+    # an out-of-range id only at an unscored target position
+    t = tok.copy()
+    t[2, Cn] = V + 3
+    mask = np.ones((B, Cn), np.uint8)
+    mask[2, Cn - 1] = 0
+    ok = t.copy()
+    ok[2, Cn] = 0
+    Lp, Lm = zo.perturbed_losses(cfg, theta, seed, eps, N, torch.from_numpy(t).cuda(),
+                                 torch.from_numpy(mask).cuda(), check_tokens=False)
+    ref_theta = oracle.init(cfg, 21)
+    rp, rm = oracle.perturbed_losses(cfg, ref_theta, seed, eps, N, ok, mask, as_double=True)
+    check(dict(Lp=Lp.cpu().numpy(), Lm=Lm.cpu().numpy()), dict(Lp=rp, Lm=rm), RTOL[cfg["wdtype"]])
+    # valid tokens afterwards
+    Lp, Lm = zo.perturbed_losses(cfg, theta, seed, eps, N, torch.from_numpy(tok).cuda(), None)
+    rp, rm = oracle.perturbed_losses(cfg, ref_theta, seed, eps, N, tok, None, as_double=True)
+    check(dict(Lp=Lp.cpu().numpy(), Lm=Lm.cpu().numpy()), dict(Lp=rp, Lm=rm), RTOL[cfg["wdtype"]])
