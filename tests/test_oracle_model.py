@@ -158,3 +158,20 @@ def test_materialise_is_theta_plus_signed_eps_probe(oracle):
         np.testing.assert_array_equal(w, base + 1e-3 * z)
         wn = oracle.materialise(cfg, th, 42, 9, 1e-3, negate=True)
         np.testing.assert_array_equal(wn, base - 1e-3 * z)
+
+
+@pytest.mark.parametrize("bad", [-1, 7, 2 ** 31 - 1])
+def test_out_of_range_tokens_are_rejected(oracle, bad):
+    """The oracle checks every token id against [0, V) on the host and
+    refuses the call (EINVAL); in-range ids at the same place are fine."""
+    cfg = dict(n_layers=1, vocab=7, embed=32, hidden=32, wdtype=0, probe=0)
+    theta = oracle.init(cfg, 3)
+    tok = np.zeros((2, 5), np.int32)
+    oracle.perturbed_losses(cfg, theta, 1, 1e-2, 1, tok)
+    for pos in ((0, 0), (1, 4)):
+        t = tok.copy()
+        t[pos] = bad
+        with pytest.raises(ValueError, match="status"):
+            oracle.perturbed_losses(cfg, theta, 1, 1e-2, 1, t)
+        with pytest.raises(ValueError, match="status"):
+            oracle.fd_losses(cfg, theta, 1, 1e-2, 1, t)
