@@ -83,6 +83,39 @@ def measured_traffic(name, dtype):
     return None
 
 
+def library_gemm(name):
+    """torch's fp16 GEMM (hipBLASLt) of the bf16 gate's plain product at the
+    workload's shape: rows 2 N B (one layer-step of every pass) by K = 2 H
+    (the layers above the first; the first has E + H) against the [4H][K]
+    weight matrix, as
+    torch.nn.functional.linear computes it. Context for the fused gate, which
+    also forms fp16(W + s eps z) per fragment and runs the LSTM cell."""
+    import torch
+    from paper_2505_17852_amd import workloads as wl
+    w, cfg = wl.CONFIGS[name], wl.model_cfg(name)
+    if cfg["wdtype"] != wl.BF16:
+        raise SystemExit("--library-gemm: bf16-weight workloads only")
+    H = cfg["hidden"]
+    M, K, N = 2 * w["N"] * w["B"], 2 * H, 4 * H
+    g = torch.Generator(device="cuda:0").manual_seed(0)
+    a = torch.randn(M, K, device="cuda:0", dtype=torch.float16, generator=g)
+    wt = torch.randn(N, K, device="cuda:0", dtype=torch.float16, generator=g)
+    for _ in range(5):
+        torch.nn.functional.linear(a, wt)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 50
+    e0.record()
+    for _ in range(reps):
+        torch.nn.functional.linear(a, wt)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    tf = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+    return {"kernel": "torch fp16 GEMM (hipBLASLt)", "workload": name, "M": M, "N": N, "K": K,
+            "ms_per_launch": ms, "TFLOPs": tf, "peak": PEAK_TFLOPS["fp16"], "frac": tf / PEAK_TFLOPS["fp16"]}
+
+
 def update_hbm(P, w, upd):
     """Algorithmic HBM rate of the update kernel (theta read and written
     once) from its HIP-event time, against the 8 TB/s HBM3E peak."""
@@ -214,6 +247,10 @@ def main():
     ap.add_argument("--calibrate-stream", action="store_true",
                     help="time an in-place read-modify-write of the workload's theta bytes "
                          "(the update's access pattern without its arithmetic) and exit")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="bf16-weight workloads: time torch's fp16 GEMM (hipBLASLt) of the "
+                         "gate's plain product, the workload's rows times [x; h] against a "
+                         "[4H][E + H] weight matrix, for context, and exit")
     ap.add_argument("--prof-every", type=int, default=None,
                     help="time every n-th launch of each kernel class with HIP events "
                          "(default: 1 for c3/c4/c5, 61 otherwise)")
@@ -246,6 +283,9 @@ def main():
         return
     if args.calibrate_stream:
         print(json.dumps(stream_limit(args.workload)), flush=True)
+        return
+    if args.library_gemm:
+        print(json.dumps(library_gemm(args.workload)), flush=True)
         return
     name = args.workload
     W_def, K_def = DEFAULTS[name]
