@@ -15,7 +15,9 @@
  * Device pointers. Every buffer argument (theta, tokens, mask, losses,
  * workspace, out) is a device pointer on the current HIP device, allocated
  * and owned by the caller. The library never allocates, frees or retains
- * caller memory, and keeps no state between calls.
+ * caller memory. It keeps no state between calls apart from the optional
+ * kernel-timing records (zo_profile_enable) and, for zo_perturbed_losses_noalloc,
+ * one fixed scratch array per device.
  *
  * Streams. `stream` is a hipStream_t (NULL = the default stream). Every call
  * only enqueues work on that stream and returns; outputs are valid once the
@@ -72,10 +74,9 @@ enum { ZO_RADEMACHER = 0, ZO_GAUSSIAN = 1 };
 /* Model shape. All fields > 0; embed and hidden must be multiples of 32
  * (ZO_ESHAPE otherwise), and for zo_perturbed_losses with bf16 weights
  * multiples of 64; n_layers <= 64. wdtype: ZO_WFP32 or ZO_WBF16
- * (storage type of theta; bf16 runs every matrix product as fp16 operands,
- * the perturbed weight fp16(w + s eps z) formed in registers from an fp16
- * copy of the weights, with fp32 accumulation and fp32 cell state).
- * probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
+ * (storage type of theta; bf16 runs every matrix product on fp16 operands
+ * from an fp16 copy of the weights, with fp32 accumulation and fp32 cell
+ * state, see "Products" below). probe: ZO_RADEMACHER or ZO_GAUSSIAN. */
 typedef struct {
     int32_t n_layers;
     int32_t vocab;
@@ -84,6 +85,31 @@ typedef struct {
     int32_t wdtype;
     int32_t probe;
 } zo_config;
+
+/* Products (bf16 weights). Each perturbed product A.(W + s eps Z) runs on
+ * fp16 MFMA operands in one of two forms:
+ *   fused      acc += A . fp16(W + s eps z): the probe added to the fp16
+ *              weight fragment in registers and rounded once (one matrix
+ *              stream). The rounding costs each element up to half an fp16
+ *              ulp of w, 2^-11 |w|, so the form is used only for
+ *              eps >= ZO_BF16_FUSED_EPS_MIN (there, for |w| < 2^-5, at most
+ *              1.6% of eps z per element, zero-mean across elements);
+ *   two-stream acc += A . W, then acc += A . (s fp16(eps z)) into the same
+ *              fp32 accumulator (twice the matrix work): the probe operand
+ *              keeps eps z to 2^-11 relative, or to 2^-25 absolute where it is
+ *              subnormal in fp16, so eps >= ZO_BF16_EPS_MIN keeps it within
+ *              0.4% of eps per element.
+ * Sign probes use +-fp16(eps) in both forms (a scale error of at most 2^-11,
+ * or 0.4% at ZO_BF16_EPS_MIN, that is the same for every element). The
+ * perturbed embedding rows are formed in fp32 and rounded once to fp16 in
+ * both forms. zo_perturbed_losses chooses by eps (ZO_PRODUCTS_AUTO); the _ex
+ * entry points take the form as an argument, for measurement. A bf16 call
+ * with eps < ZO_BF16_EPS_MIN returns ZO_EINVAL. fp32 weights form
+ * w +- eps z in fp32 (fused, one fp32 rounding); their two-stream form exists
+ * for measurement only (central differences). */
+#define ZO_BF16_FUSED_EPS_MIN 0x1p-10f /* 9.765625e-4 */
+#define ZO_BF16_EPS_MIN 0x1p-17f       /* 7.62939453125e-6 */
+enum { ZO_PRODUCTS_AUTO = 0, ZO_PRODUCTS_FUSED = 1, ZO_PRODUCTS_SPLIT = 2 };
 
 /* Number of elements P of theta for this shape (layout above); 0 if the
  * configuration is invalid. Host only. */
@@ -116,7 +142,7 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
  * the worker's probes; Eq. 2's two loss queries per probe).
  *   theta    device, P elements (read only)
  *   seed     Philox key of this step's probes; probe n uses index i0 + n
- *   eps      perturbation size, > 0 and finite
+ *   eps      perturbation size, > 0 and finite (bf16 weights: >= ZO_BF16_EPS_MIN)
  *   N        number of probes (>= 1); 2N forward passes
  *   i0       global index of the first probe (a slice [i0, i0+N) of a larger
  *            set gives bit-identical losses to the same probes in the full set)
@@ -138,13 +164,21 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream);
  *            cache; same results, fewer probe regenerations)
  * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_ENOMEM or ZO_EDEVICE.
  * fp32 weights: each matrix product uses the perturbed weight tile
- * w +- eps z formed in LDS (one fp32 rounding); with the environment variable
- * ZO_FP32_SPLIT=1 it instead accumulates W.x and (+-x).(eps z) as two MFMA
- * streams (same result to rounding, twice the matrix work; for measurement). */
+ * w +- eps z formed in LDS (one fp32 rounding). bf16 weights: the fused or
+ * the two-stream products by eps (see "Products"). */
 int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
                         int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
                         int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
                         size_t ws_bytes, void* stream);
+
+/* zo_perturbed_losses with the form of the products given: ZO_PRODUCTS_AUTO
+ * (as zo_perturbed_losses), ZO_PRODUCTS_FUSED or ZO_PRODUCTS_SPLIT (any
+ * other value is ZO_EINVAL). For measuring one form against the other; the
+ * eps floor of bf16 weights applies to both. */
+int zo_perturbed_losses_ex(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
+                           int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
+                           int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
+                           size_t ws_bytes, int32_t products, void* stream);
 
 /* The update of Eq. 7 in its general form (Algorithm 1's closing loop):
  *   c_n = fp32( (lr / N) * (L+_n - L-_n) / (2 eps) )  (computed in double)
@@ -155,7 +189,7 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
  * [N]. If any of them is not finite the update is skipped on the device,
  * theta is left bit-unchanged and, when skipped_out (device int32, may be
  * NULL) is given, *skipped_out is set to 1 (0 otherwise).
- * Returns ZO_OK, ZO_EINVAL or ZO_EDEVICE. */
+ * Returns ZO_OK, ZO_EINVAL, ZO_ESHAPE or ZO_EDEVICE. */
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
               uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
               void* stream);
@@ -165,12 +199,18 @@ int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float
  *   L   device fp32 [N]: the loss at theta + eps z_{i0+n}, as zo_perturbed_losses'
  *       Lplus (bit-identical to it)
  *   L0  device fp32 [1]: the loss at theta itself (the clean pass)
- * Other arguments, the workspace (zo_workspace_bytes covers both estimators)
- * and the return codes as for zo_perturbed_losses; with fp32 weights the
- * clean pass uses the weight tile itself (ZO_FP32_SPLIT does not apply). */
+ * Other arguments, the workspace (zo_workspace_bytes covers both estimators),
+ * the products and the return codes as for zo_perturbed_losses. */
 int zo_fd_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
                  uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
                  float* L, float* L0, void* workspace, size_t ws_bytes, void* stream);
+
+/* zo_fd_losses with the form of the products given, as
+ * zo_perturbed_losses_ex (fp32 weights: ZO_PRODUCTS_SPLIT is ZO_EINVAL). */
+int zo_fd_losses_ex(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                    uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                    float* L, float* L0, void* workspace, size_t ws_bytes, int32_t products,
+                    void* stream);
 
 /* The forward-difference update:
  *   c_n = fp32( (lr / N) * (L_n - L0) / eps )  (computed in double)

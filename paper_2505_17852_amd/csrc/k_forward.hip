@@ -759,7 +759,7 @@ hipError_t launch_gates_f32(const ForwardArgs& a, const GateLayer* ls, int n, hi
   g.eps = a.eps;
   g.rm = row_map(R);
   g.zc_stride = a.zmap.pg;
-  const bool split = a.fp32_split;
+  const bool split = a.split;
   // 128-row workgroups where every block of 128 rows lies inside one probe's rows
   const bool wide = R.pair_rows % 128 == 0;
   auto go = [&](auto rm_tag) {
@@ -809,7 +809,7 @@ hipError_t launch_head_f32(const ForwardArgs& a, const void* hist, int t0, int T
   h.zc_out = a.zc ? (const float*)a.zc + a.zmap.out : nullptr;
   h.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)a.ws.nvt, (unsigned)(h.rows / BM));
-  const bool split = a.fp32_split;
+  const bool split = a.split;
   ProfScope ps(kKHead, st);
   if (a.cfg.probe == ZO_RADEMACHER) {
     if (split) head_f32_kernel<ZO_RADEMACHER, true><<<grid, 256, 0, st>>>(h);

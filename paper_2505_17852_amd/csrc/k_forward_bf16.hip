@@ -200,7 +200,12 @@ struct SegB {
 // v_mfma_f32_32x32x16_f16 have the same fragment layout, so only their order
 // changes. Lane (lr, lg) then holds, for activation row lr of a tile, the 16
 // columns 8 (v >> 2) + 4 lg + (v & 3), v < 16.
-template <int kind, bool kTrans = false, bool kFD = false, typename ColMap>
+// kSplit: the two-stream form for small eps, acc += A.W then acc += A.(s eps z)
+// (the probe fragment as an operand of its own, twice the matrix work),
+// instead of acc += A.fp16(W + s eps z): a weight fragment rounded with the
+// probe added loses up to half an fp16 ulp of w per element, which is a
+// large share of eps z once eps is small against |w|.
+template <int kind, bool kTrans = false, bool kFD = false, bool kSplit = false, typename ColMap>
 __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
                                               int nseg, ColMap colmap, Key key, uint32_t probe, int sgn,
                                               float eps, uint16_t eps_b) {
@@ -384,17 +389,27 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     for (int s = 0; s < TK / 16; ++s) {
       const Frag& c = f[s & 1];
       if (s + 1 < TK / 16) load(s + 1, f[(s + 1) & 1]);
-      // B = fp16(W + s eps z): one packed fp16 add per pair (round to
-      // nearest even), then one MFMA per accumulator
-      h8 wz[2];
+      auto mma = [&](const h8(&b)[2]) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) wz[nt] = c.w[nt] + c.z[nt];
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+          for (int nt = 0; nt < 2; ++nt)
+            acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_f16(b[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
+                                 : __builtin_amdgcn_mfma_f32_32x32x16_f16(c.a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+      };
+      if constexpr (kSplit) {
+        // A.W for every accumulator, then A.(s eps z): the two products into
+        // one accumulator are MT x 2 instructions apart
+        mma(c.w);
+        mma(c.z);
+      } else {
+        // B = fp16(W + s eps z): one packed fp16 add per pair (round to
+        // nearest even), then one MFMA per accumulator
+        h8 wz[2];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          acc[mt][nt] = kTrans ? __builtin_amdgcn_mfma_f32_32x32x16_f16(wz[nt], c.a[mt], acc[mt][nt], 0, 0, 0)
-                               : __builtin_amdgcn_mfma_f32_32x32x16_f16(c.a[mt], wz[nt], acc[mt][nt], 0, 0, 0);
+        for (int nt = 0; nt < 2; ++nt) wz[nt] = c.w[nt] + c.z[nt];
+        mma(wz);
+      }
       if (more) {
         // tile it + STAGES - 1 goes to the stage tile it - 1 used
         constexpr std::integral_constant<int, (S + T::STAGES - 1) % T::STAGES> next{};
@@ -419,7 +434,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         // a few VALU instructions of the next step's probe fragments
         __builtin_amdgcn_sched_group_barrier(0x100, MT + 2 + (kind == ZO_RADEMACHER ? 0 : 2), 0);
 #pragma unroll
-        for (int i = 0; i < 2 * MT; ++i) {
+        for (int i = 0; i < (kSplit ? 4 : 2) * MT; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
         }
@@ -531,7 +546,7 @@ struct GateArgsB {
 // is gate c / 16 of unit 16 wn + c % 16, so lane lr holds gates i, g (lr < 16)
 // or f, o (lr >= 16) of unit lr % 16 in its two column tiles, and one
 // exchange with lane lr ^ 16 brings all four gates of a (row, unit) together.
-template <int kind, bool kFD>
+template <int kind, bool kFD, bool kSplit>
 __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -555,7 +570,8 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
                 kind == kGaussCached ? g.zc_ih + zpos : nullptr};
   const SegB s1{g.hprev + m0 * H, H, g.w_hh16, H, g.off_hh, H,
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
-  mainloop_bf16<kind, false, kFD>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
+  mainloop_bf16<kind, false, kFD, kSplit>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps,
+                                          g.eps_b);
 
   const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
   const int u = u0 + 16 * wn + (lr & 15);
@@ -615,7 +631,7 @@ struct HeadArgsB {
   const uint16_t* w_out16;  // fp16 copy of W_out
 };
 
-template <int kind, bool kFD>
+template <int kind, bool kFD, bool kSplit>
 __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   using T = Tiles<kind>;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -635,7 +651,8 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   zero_acc(acc);
   const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, g.H, g.off_w, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
-  mainloop_bf16<kind, true, kFD>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b);
+  mainloop_bf16<kind, true, kFD, kSplit>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps,
+                                         g.eps_b);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
@@ -791,6 +808,25 @@ __global__ __launch_bounds__(256) void embed_bf16_rad_kernel(const uint16_t* the
   for (int q = 0; q < 4; ++q) dst[q] = out[q];
 }
 
+// Calls go(kind, fd, split) with the compile-time variant of this call: the
+// probe kind (sign probes; normal probes read from the probe cache or
+// regenerated), central or forward differences, fused or two-stream products.
+template <typename Go>
+void dispatch_bf16(const ForwardArgs& a, Go&& go) {
+  using std::integral_constant;
+  auto by_split = [&](auto kind_tag, auto fd_tag) {
+    if (a.split) go(kind_tag, fd_tag, integral_constant<bool, true>{});
+    else go(kind_tag, fd_tag, integral_constant<bool, false>{});
+  };
+  auto by_fd = [&](auto kind_tag) {
+    if (a.rows.fd) by_split(kind_tag, integral_constant<bool, true>{});
+    else by_split(kind_tag, integral_constant<bool, false>{});
+  };
+  if (a.cfg.probe == ZO_RADEMACHER) by_fd(integral_constant<int, ZO_RADEMACHER>{});
+  else if (a.zc) by_fd(integral_constant<int, kGaussCached>{});
+  else by_fd(integral_constant<int, ZO_GAUSSIAN>{});
+}
+
 }  // namespace
 
 hipError_t launch_embed_bf16(const ForwardArgs& a, int t, void* x0, hipStream_t st) {
@@ -840,20 +876,15 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.zc_ih = a.zc ? (const uint16_t*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const uint16_t*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
-  auto go = [&](auto kind_tag, auto fd_tag) {
+  auto go = [&](auto kind_tag, auto fd_tag, auto split_tag) {
     constexpr int kind = decltype(kind_tag)::value;
     constexpr bool fd = decltype(fd_tag)::value;
+    constexpr bool split = decltype(split_tag)::value;
     const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<kind>::TN / 4))));
     ProfScope ps(kKGate, st);
-    gate_bf16_kernel<kind, fd><<<grid, NT, 0, st>>>(g);
+    gate_bf16_kernel<kind, fd, split><<<grid, NT, 0, st>>>(g);
   };
-  const int kind = a.cfg.probe == ZO_RADEMACHER ? ZO_RADEMACHER : a.zc ? kGaussCached : ZO_GAUSSIAN;
-  using std::integral_constant;
-  using T_ = integral_constant<bool, true>;
-  using F_ = integral_constant<bool, false>;
-  if (kind == ZO_RADEMACHER) R.fd ? go(integral_constant<int, ZO_RADEMACHER>{}, T_{}) : go(integral_constant<int, ZO_RADEMACHER>{}, F_{});
-  else if (kind == kGaussCached) R.fd ? go(integral_constant<int, kGaussCached>{}, T_{}) : go(integral_constant<int, kGaussCached>{}, F_{});
-  else R.fd ? go(integral_constant<int, ZO_GAUSSIAN>{}, T_{}) : go(integral_constant<int, ZO_GAUSSIAN>{}, F_{});
+  dispatch_bf16(a, go);
   return hipGetLastError();
 }
 
@@ -887,19 +918,14 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.zc_out = a.zc ? (const uint16_t*)a.zc + a.zmap.out : nullptr;
   h.zc_stride = a.zmap.pg;
   const dim3 grid((unsigned)((int64_t)a.ws.nvt * (h.rows / TM)));
-  auto go = [&](auto kind_tag, auto fd_tag) {
+  auto go = [&](auto kind_tag, auto fd_tag, auto split_tag) {
     constexpr int kind = decltype(kind_tag)::value;
     constexpr bool fd = decltype(fd_tag)::value;
+    constexpr bool split = decltype(split_tag)::value;
     ProfScope ps(kKHead, st);
-    head_bf16_kernel<kind, fd><<<grid, NT, 0, st>>>(h);
+    head_bf16_kernel<kind, fd, split><<<grid, NT, 0, st>>>(h);
   };
-  const int kind = a.cfg.probe == ZO_RADEMACHER ? ZO_RADEMACHER : a.zc ? kGaussCached : ZO_GAUSSIAN;
-  using std::integral_constant;
-  using T_ = integral_constant<bool, true>;
-  using F_ = integral_constant<bool, false>;
-  if (kind == ZO_RADEMACHER) R.fd ? go(integral_constant<int, ZO_RADEMACHER>{}, T_{}) : go(integral_constant<int, ZO_RADEMACHER>{}, F_{});
-  else if (kind == kGaussCached) R.fd ? go(integral_constant<int, kGaussCached>{}, T_{}) : go(integral_constant<int, kGaussCached>{}, F_{});
-  else R.fd ? go(integral_constant<int, ZO_GAUSSIAN>{}, T_{}) : go(integral_constant<int, ZO_GAUSSIAN>{}, F_{});
+  dispatch_bf16(a, go);
   return hipGetLastError();
 }
 

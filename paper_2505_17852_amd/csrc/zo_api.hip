@@ -6,7 +6,6 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
-#include <cstdlib>
 #include <cstring>
 
 #include "../../include/zo.h"
@@ -85,8 +84,8 @@ int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
 
 static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
                         uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
-                        float* L1, float* L2, void* workspace, size_t ws_bytes, void* stream, bool fd,
-                        const char* name) {
+                        float* L1, float* L2, void* workspace, size_t ws_bytes, int32_t products,
+                        void* stream, bool fd, const char* name) {
   int st = check_config(cfg);
   if (st) return st;
   // the bf16 forward walks K in tiles of 64
@@ -98,6 +97,13 @@ static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, 
   if (!aligned16(theta) || !aligned16(workspace))
     return fail(ZO_EINVAL, "theta and workspace must be 16-byte aligned");
   if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
+  if (cfg->wdtype == ZO_WBF16 && eps < ZO_BF16_EPS_MIN)
+    return fail(ZO_EINVAL, "bf16 weights: eps (%g) must be >= %g (fp16 probe operands)", (double)eps,
+                (double)ZO_BF16_EPS_MIN);
+  if (products != ZO_PRODUCTS_AUTO && products != ZO_PRODUCTS_FUSED && products != ZO_PRODUCTS_SPLIT)
+    return fail(ZO_EINVAL, "unknown products mode %d", products);
+  if (fd && cfg->wdtype == ZO_WFP32 && products == ZO_PRODUCTS_SPLIT)
+    return fail(ZO_EINVAL, "fp32 weights: forward differences have no two-stream form");
   if (N < 1 || B < 1 || C < 1) return fail(ZO_EINVAL, "N, B and C must be >= 1");
   if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
     return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
@@ -121,8 +127,12 @@ static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, 
   a.Lplus = L1;
   a.Lminus = L2;
   a.work = (char*)workspace;
-  const char* split = std::getenv("ZO_FP32_SPLIT");
-  a.fp32_split = !fd && split && split[0] == '1';
+  // bf16 weights: the fused form fp16(W + s eps z) down to its floor, the
+  // two-stream form below it; fp32 weights: fused (w +- eps z in fp32)
+  if (products == ZO_PRODUCTS_AUTO)
+    a.split = cfg->wdtype == ZO_WBF16 && eps < ZO_BF16_FUSED_EPS_MIN;
+  else
+    a.split = products == ZO_PRODUCTS_SPLIT;
   // the probe cache is used when the workspace has room for it
   a.zc = (zo::probe_cache_kind(*cfg) && ws_bytes >= plan.total) ? (char*)workspace + plan.zcache : nullptr;
   a.zmap = zo::make_zcache_map(*cfg);
@@ -134,14 +144,29 @@ int zo_perturbed_losses(const zo_config* cfg, const void* theta, uint64_t seed, 
                         uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
                         float* Lplus, float* Lminus, void* workspace, size_t ws_bytes, void* stream) {
   return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, Lplus, Lminus, workspace, ws_bytes,
-                      stream, false, "zo_perturbed_losses");
+                      ZO_PRODUCTS_AUTO, stream, false, "zo_perturbed_losses");
+}
+
+int zo_perturbed_losses_ex(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                           uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                           float* Lplus, float* Lminus, void* workspace, size_t ws_bytes, int32_t products,
+                           void* stream) {
+  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, Lplus, Lminus, workspace, ws_bytes,
+                      products, stream, false, "zo_perturbed_losses_ex");
 }
 
 int zo_fd_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N, uint32_t i0,
                  const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C, float* L, float* L0,
                  void* workspace, size_t ws_bytes, void* stream) {
-  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, L, L0, workspace, ws_bytes, stream,
-                      true, "zo_fd_losses");
+  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, L, L0, workspace, ws_bytes,
+                      ZO_PRODUCTS_AUTO, stream, true, "zo_fd_losses");
+}
+
+int zo_fd_losses_ex(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N, uint32_t i0,
+                    const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C, float* L, float* L0,
+                    void* workspace, size_t ws_bytes, int32_t products, void* stream) {
+  return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, L, L0, workspace, ws_bytes, products,
+                      stream, true, "zo_fd_losses_ex");
 }
 
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,

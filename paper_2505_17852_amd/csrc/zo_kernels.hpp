@@ -38,7 +38,8 @@ struct ForwardArgs {
   float* Lplus;
   float* Lminus;
   char* work;
-  bool fp32_split;  // fp32 path: separate W.h and probe MFMA streams (measurement variant)
+  bool split;       // two-stream products: A.W and A.(s eps z) as separate MFMA streams into one
+                    // accumulator (bf16 weights: eps below the fused form's floor; fp32: measurement)
   void* zc;         // probe cache inside work, or nullptr (probes regenerated in every tile)
   void* w16;        // bf16 weights: fp16 copy of the product matrices inside work (ZCacheMap layout)
   ZCacheMap zmap;

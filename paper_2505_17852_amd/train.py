@@ -15,10 +15,23 @@ estimator of Section 2:
 The step's probes are drawn from the seed `seed0 + k`. Argument marshalling
 only: the forwards and the update run in the library's HIP kernels, and θ
 stays on the device for the whole run.
+
+As a program it trains one of the seeded workloads and prints its curve,
+one JSON line per evaluation:
+    python -m paper_2505_17852_amd.train --workload c2 --steps 10000 \
+        --eps 3e-2 --lr 3e-2 --fresh-batches --eval-every 1000
+Each line holds the mean per-step estimate over the last window and the
+clean loss L(θ) (the clean pass of a forward-difference call) on the
+training batch and, with --fresh-batches, on a held-out batch of the same
+shape.
 """
 from __future__ import annotations
 
+import argparse
 import contextlib
+import json
+import sys
+import time
 
 import torch
 
@@ -66,3 +79,69 @@ def train(cfg, theta: torch.Tensor, tokens: torch.Tensor, mask: torch.Tensor | N
                 hist[k] = 0.5 * (L1.mean() + L2.mean())
                 zo.update(cfg, theta, seed0 + k, eps, lr, L1, L2)
         return hist.cpu()
+
+
+def clean_loss(cfg, theta: torch.Tensor, tokens: torch.Tensor, mask: torch.Tensor | None) -> float:
+    """L(θ) on one batch: the clean pass of zo_fd_losses (with one probe,
+    whose perturbed pass is ignored)."""
+    _, L0 = zo.fd_losses(cfg, theta, 0, 1e-3, 1, tokens, mask)
+    return float(L0.item())
+
+
+def main(argv=None):
+    import numpy as np
+
+    from . import workloads as wl
+    ap = argparse.ArgumentParser(description="zeroth-order training of a seeded workload on one GPU")
+    ap.add_argument("--workload", default="c2", choices=sorted(wl.CONFIGS))
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--eps", type=float, default=None, help="perturbation size (default: the workload's)")
+    ap.add_argument("--lr", type=float, default=None, help="step size (default: the workload's)")
+    ap.add_argument("--estimator", default="cd", choices=ESTIMATORS)
+    ap.add_argument("--fresh-batches", action="store_true",
+                    help="draw a new batch of the workload's distribution every step (seed data + 1 + k) "
+                         "and evaluate on a held-out batch; default: one fixed batch")
+    ap.add_argument("--eval-every", type=int, default=500)
+    args = ap.parse_args(argv)
+    name = args.workload
+    w, cfg, sd = wl.CONFIGS[name], wl.model_cfg(name), wl.seeds(name)
+    eps = w["eps"] if args.eps is None else args.eps
+    lr = w["lr"] if args.lr is None else args.lr
+    dev = torch.device("cuda:0")
+
+    def dev_batch(seed=None):
+        tok, mask = wl.batch(name, seed=seed)
+        return (torch.from_numpy(tok).to(dev), None if mask is None else torch.from_numpy(mask).to(dev))
+
+    tokens, mask = dev_batch()
+    held = dev_batch(seed=sd["data"] + 10_000_000) if args.fresh_batches else None
+    batches = (lambda k: dev_batch(seed=sd["data"] + 1 + k)) if args.fresh_batches else None
+    theta = zo.new_theta(cfg, dev)
+    zo.init(cfg, theta, sd["init"])
+    t0 = time.time()
+
+    def report(step, window):
+        row = {"workload": name, "step": step, "eps": eps, "lr": lr, "estimator": args.estimator,
+               "N": w["N"], "fresh_batches": args.fresh_batches,
+               "window_estimate": None if window is None else float(np.mean(window)),
+               "clean_loss_train_batch": clean_loss(cfg, theta, tokens, mask),
+               "seconds": round(time.time() - t0, 1)}
+        if held is not None:
+            row["clean_loss_held_out"] = clean_loss(cfg, theta, *held)
+        print(json.dumps(row), flush=True)
+
+    report(0, None)
+    done = 0
+    while done < args.steps:
+        n = min(args.eval_every, args.steps - done)
+        first = (tokens, mask) if batches is None else batches(done)
+        shifted = None if batches is None else (lambda k, d=done: batches(d + k))
+        hist = train(cfg, theta, first[0], first[1], N=w["N"], eps=eps, lr=lr, steps=n,
+                     seed0=sd["step"] + done, batches=shifted, estimator=args.estimator)
+        done += n
+        report(done, hist.numpy())
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -6,8 +6,9 @@ kernels. PyTorch supplies device memory (torch.cuda tensors) and the stream
 built (paper_2505_17852_amd/build.py); there is no fallback of any kind.
 
 Function names follow the C ABI in include/zo.h:
-    param_count, workspace_bytes, workspace_bytes_min, init, perturbed_losses,
-    update, fd_losses, fd_update, debug_probe, debug_gauss_pairs
+    param_count, workspace_bytes, workspace_bytes_min, init, perturbed_losses
+    (zo_perturbed_losses / _ex), update, fd_losses (zo_fd_losses / _ex),
+    fd_update, debug_probe, debug_gauss_pairs
 A model configuration is a dict with the keys n_layers, vocab, embed,
 hidden, wdtype (0 fp32, 1 bf16) and probe (0 Rademacher, 1 normal).
 """
@@ -24,6 +25,11 @@ LIB_PATH = os.path.join(HERE, "libzo.so")
 ZO_OK, ZO_EINVAL, ZO_ESHAPE, ZO_EDEVICE, ZO_ENOMEM, ZO_ENONFINITE = 0, -1, -2, -3, -4, -5
 FP32, BF16 = 0, 1
 RADEMACHER, GAUSSIAN = 0, 1
+# form of the perturbed products (bf16 weights: fused fp16(W + s eps z) or the
+# two-stream A.W + A.(s eps z)); AUTO picks by eps
+PRODUCTS_AUTO, PRODUCTS_FUSED, PRODUCTS_SPLIT = 0, 1, 2
+BF16_FUSED_EPS_MIN = 2.0 ** -10  # ZO_BF16_FUSED_EPS_MIN
+BF16_EPS_MIN = 2.0 ** -17        # ZO_BF16_EPS_MIN
 
 
 class ZoError(RuntimeError):
@@ -62,6 +68,11 @@ def lib():
                                 vp, vp, vp, vp]
         L.zo_fd_losses.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
                                    vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, vp]
+        L.zo_perturbed_losses_ex.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
+                                             vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t,
+                                             C.c_int32, vp]
+        L.zo_fd_losses_ex.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
+                                      vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, C.c_int32, vp]
         L.zo_fd_update.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
                                    vp, vp, vp, vp]
         L.zo_debug_probe.argtypes = [C.c_int32, C.c_uint64, C.c_uint32, C.c_uint64, C.c_uint64, vp, vp]
@@ -71,6 +82,7 @@ def lib():
                                       C.POINTER(C.c_int64)]
         L.zo_last_error.restype = C.c_char_p
         for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_fd_losses", "zo_fd_update",
+                  "zo_perturbed_losses_ex", "zo_fd_losses_ex",
                   "zo_debug_probe",
                   "zo_debug_gauss_pairs", "zo_profile_enable", "zo_profile_read"):
             getattr(L, f).restype = C.c_int
@@ -108,6 +120,14 @@ def theta_dtype(cfg):
     return torch.bfloat16 if int(cfg["wdtype"]) == BF16 else torch.float32
 
 
+def _theta(cfg, theta: torch.Tensor):
+    """theta's device pointer after checking its type and its length, P."""
+    p = _dev(theta, theta_dtype(cfg), "theta")
+    if theta.numel() != param_count(cfg):
+        raise ValueError(f"theta has {theta.numel()} elements, the model has {param_count(cfg)}")
+    return p
+
+
 def param_count(cfg) -> int:
     c = _cfg(cfg)
     return int(lib().zo_param_count(C.byref(c)))
@@ -124,9 +144,7 @@ def new_theta(cfg, device="cuda") -> torch.Tensor:
 
 def init(cfg, theta: torch.Tensor, seed: int, stream=None):
     c = _cfg(cfg)
-    if theta.numel() != param_count(cfg):
-        raise ValueError("theta has the wrong number of elements")
-    _check(lib().zo_init(C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, _stream(stream)))
+    _check(lib().zo_init(C.byref(c), _theta(cfg, theta), seed, _stream(stream)))
 
 
 def workspace_bytes_min(cfg, N: int, B: int, C_: int) -> int:
@@ -147,13 +165,14 @@ def perturbed_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int,
                      tokens: torch.Tensor, mask: torch.Tensor | None = None, i0: int = 0,
                      Lplus: torch.Tensor | None = None, Lminus: torch.Tensor | None = None,
                      workspace: torch.Tensor | None = None, stream=None,
-                     check_tokens: bool = True):
+                     check_tokens: bool = True, products: int = PRODUCTS_AUTO):
     """Returns (L+, L-) as device fp32 tensors of N elements (asynchronous).
 
     The kernels never read memory by an id outside [0, vocab): such an id
     makes the affected losses non-finite (and zo_update then skips). With
     check_tokens (default) this wrapper rejects them first (one device
-    sync)."""
+    sync). products: PRODUCTS_AUTO (zo_perturbed_losses), or PRODUCTS_FUSED /
+    PRODUCTS_SPLIT (zo_perturbed_losses_ex, for measurement)."""
     c = _cfg(cfg)
     if tokens.dim() != 2:
         raise ValueError("tokens must be [B][C+1]")
@@ -174,12 +193,15 @@ def perturbed_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int,
         raise ValueError("loss buffers smaller than N")
     if workspace is None:
         workspace = new_workspace(cfg, N, B, Cn, device=dev)
-    st = lib().zo_perturbed_losses(
-        C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, N, i0,
-        _dev(tokens, torch.int32, "tokens"),
-        None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
-        _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
-        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    args = (C.byref(c), _theta(cfg, theta), seed, eps, N, i0,
+            _dev(tokens, torch.int32, "tokens"),
+            None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
+            _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
+            _dev(workspace, torch.uint8, "workspace"), workspace.numel())
+    if products == PRODUCTS_AUTO:
+        st = lib().zo_perturbed_losses(*args, _stream(stream))
+    else:
+        st = lib().zo_perturbed_losses_ex(*args, int(products), _stream(stream))
     _check(st)
     return Lplus, Lminus
 
@@ -191,7 +213,7 @@ def update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, Lplus: to
     N = Lplus.numel()
     if Lminus.numel() != N:
         raise ValueError("Lplus and Lminus differ in length")
-    st = lib().zo_update(C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, lr, N, i0,
+    st = lib().zo_update(C.byref(c), _theta(cfg, theta), seed, eps, lr, N, i0,
                          _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
                          None if skipped is None else _dev(skipped, torch.int32, "skipped"),
                          _stream(stream))
@@ -201,9 +223,10 @@ def update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, Lplus: to
 def fd_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int, tokens: torch.Tensor,
               mask: torch.Tensor | None = None, i0: int = 0, L: torch.Tensor | None = None,
               L0: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None,
-              check_tokens: bool = True):
+              check_tokens: bool = True, products: int = PRODUCTS_AUTO):
     """Forward differences: returns (L [N], L0 [1]) as device fp32 tensors
-    (asynchronous): the losses at theta + eps z_n and at theta."""
+    (asynchronous): the losses at theta + eps z_n and at theta. products as
+    for perturbed_losses (zo_fd_losses_ex when not PRODUCTS_AUTO)."""
     c = _cfg(cfg)
     if tokens.dim() != 2:
         raise ValueError("tokens must be [B][C+1]")
@@ -224,12 +247,15 @@ def fd_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int, tokens: t
         raise ValueError("loss buffers too small")
     if workspace is None:
         workspace = new_workspace(cfg, N, B, Cn, device=dev)
-    st = lib().zo_fd_losses(
-        C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, N, i0,
-        _dev(tokens, torch.int32, "tokens"),
-        None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
-        _dev(L, torch.float32, "L"), _dev(L0, torch.float32, "L0"),
-        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    args = (C.byref(c), _theta(cfg, theta), seed, eps, N, i0,
+            _dev(tokens, torch.int32, "tokens"),
+            None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
+            _dev(L, torch.float32, "L"), _dev(L0, torch.float32, "L0"),
+            _dev(workspace, torch.uint8, "workspace"), workspace.numel())
+    if products == PRODUCTS_AUTO:
+        st = lib().zo_fd_losses(*args, _stream(stream))
+    else:
+        st = lib().zo_fd_losses_ex(*args, int(products), _stream(stream))
     _check(st)
     return L, L0
 
@@ -241,7 +267,7 @@ def fd_update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, L: tor
     N = L.numel()
     if L0.numel() < 1:
         raise ValueError("L0 must hold one loss")
-    st = lib().zo_fd_update(C.byref(c), _dev(theta, theta_dtype(cfg), "theta"), seed, eps, lr, N, i0,
+    st = lib().zo_fd_update(C.byref(c), _theta(cfg, theta), seed, eps, lr, N, i0,
                             _dev(L, torch.float32, "L"), _dev(L0, torch.float32, "L0"),
                             None if skipped is None else _dev(skipped, torch.int32, "skipped"),
                             _stream(stream))

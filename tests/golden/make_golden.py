@@ -1,5 +1,8 @@
-"""Writes the oracle regression fixture of this directory. Calls only the
-oracle (never the HIP library): python tests/golden/make_golden.py"""
+"""Writes the oracle fixtures of this directory. Calls only the oracle (never
+the HIP library):
+    python tests/golden/make_golden.py          oracle_losses.txt (small cases)
+    python tests/golden/make_golden.py --wide   oracle_losses_wide.txt (the
+        billion-parameter and 1024-wide layer shapes at several eps; minutes)"""
 import os
 import sys
 
@@ -20,6 +23,44 @@ CASES = [
 ]
 
 
+# The estimator's signal at the real layer widths: the workload's model, init
+# and step seeds and a short batch of its token distribution, at several eps.
+# name, workload, probe override, N, B, C, eps values
+WIDE_CASES = [
+    ("c4", "c4", None, 4, 2, 4, (1e-3, 1e-4, 1e-5)),
+    ("c3", "c3", None, 8, 2, 4, (1e-3, 3e-4, 1e-4, 3e-5, 1e-5)),
+    ("c3-rad", "c3", 0, 8, 2, 4, (1e-3, 1e-4, 1e-5)),
+]
+
+
+def wide_key(name, eps):
+    return f"{name}@{eps:g}"
+
+
+def wide_inputs(name, workload, probe, B, C):
+    cfg = wl.model_cfg(workload) if probe is None else wl.model_cfg(workload, probe=probe)
+    tok, _ = wl.batch(workload, B=B, C=C)
+    return cfg, wl.seeds(workload), tok
+
+
+def main_wide():
+    ob.build()
+    from oracle import oracle
+    lines = ["# Oracle losses at the real layer widths (written by make_golden.py --wide from the oracle only).",
+             "# name@eps | L+ (N, fp64) | L- (N, fp64); repr() of each double"]
+    for name, workload, probe, N, B, C, epss in WIDE_CASES:
+        cfg, sd, tok = wide_inputs(name, workload, probe, B, C)
+        theta = oracle.init(cfg, sd["init"])
+        for eps in epss:
+            lp, lm = oracle.perturbed_losses(cfg, theta, sd["step"], eps, N, tok, as_double=True)
+            lines.append(" | ".join([wide_key(name, eps), " ".join(repr(float(x)) for x in lp),
+                                     " ".join(repr(float(x)) for x in lm)]))
+            print(lines[-1], flush=True)
+        del theta
+    with open(os.path.join(HERE, "oracle_losses_wide.txt"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ob.build()
     from oracle import oracle
@@ -37,4 +78,4 @@ def main():
 
 
 if __name__ == "__main__":
-    main()
+    main_wide() if "--wide" in sys.argv else main()

@@ -148,6 +148,38 @@ def test_forward_difference_argument_errors(zo):
     assert L.zo_fd_update(C.byref(c), fake, 1, 1e-3, 1e-3, 4, 0xFFFFFFFE, fake, fake, None, None) == zo.ZO_EINVAL
 
 
+def test_products_and_eps_floor_errors(zo):
+    """The form of the products and the bf16 eps floor are checked on the
+    host: bf16 weights reject eps below ZO_BF16_EPS_MIN (2^-17) and accept it
+    at the floor (the call then fails only on the 16-byte workspace);
+    unknown product forms and the fp32 two-stream form of forward differences
+    are argument errors."""
+    L = zo.lib()
+    fake = C.c_void_p(0x10000)
+    bf = zo._cfg(dict(n_layers=1, vocab=256, embed=64, hidden=64, wdtype=wl.BF16, probe=wl.RADEMACHER))
+    f32 = zo._cfg(wl.model_cfg("c1"))
+
+    def losses(cfgv, eps, products=zo.PRODUCTS_AUTO, ws=1 << 40, fd=False):
+        f = L.zo_fd_losses_ex if fd else L.zo_perturbed_losses_ex
+        return f(C.byref(cfgv), fake, 1, eps, 2, 0, fake, None, 2, 4, fake, fake, fake, ws, products, None)
+
+    assert losses(bf, 2.0 ** -18) == zo.ZO_EINVAL
+    assert "eps" in L.zo_last_error().decode()
+    assert losses(bf, 2.0 ** -17, ws=16) == zo.ZO_ENOMEM
+    assert losses(bf, 2.0 ** -18, products=zo.PRODUCTS_SPLIT) == zo.ZO_EINVAL
+    assert L.zo_perturbed_losses(C.byref(bf), fake, 1, 2.0 ** -18, 2, 0, fake, None, 2, 4, fake, fake, fake,
+                                 1 << 40, None) == zo.ZO_EINVAL
+    assert L.zo_fd_losses(C.byref(bf), fake, 1, 2.0 ** -18, 2, 0, fake, None, 2, 4, fake, fake, fake,
+                          1 << 40, None) == zo.ZO_EINVAL
+    assert losses(f32, 2.0 ** -20, ws=16) == zo.ZO_ENOMEM  # fp32 weights have no floor
+    assert losses(bf, 1e-3, products=3) == zo.ZO_EINVAL
+    assert losses(bf, 1e-3, products=-1) == zo.ZO_EINVAL
+    assert losses(f32, 1e-3, products=zo.PRODUCTS_SPLIT, fd=True) == zo.ZO_EINVAL
+    assert losses(f32, 1e-3, products=zo.PRODUCTS_SPLIT, ws=16) == zo.ZO_ENOMEM
+    assert losses(bf, 1e-3, products=zo.PRODUCTS_SPLIT, ws=16, fd=True) == zo.ZO_ENOMEM
+    assert zo.BF16_EPS_MIN == 2.0 ** -17 and zo.BF16_FUSED_EPS_MIN == 2.0 ** -10
+
+
 def test_header_is_c_and_the_library_links_from_c(zo, tmp_path):
     """include/zo.h compiles as C11, and a C program linked against the
     library calls its host-only entry points (sizes and argument checks; no

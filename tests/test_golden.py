@@ -72,3 +72,43 @@ def test_hip_path_matches_stored_losses(case):
     assert np.all(np.abs(Lp.cpu().numpy() - lp) <= tol * np.abs(lp))
     assert np.all(np.abs(Lm.cpu().numpy() - lm) <= tol * np.abs(lm))
     assert abs(float(L0.item()) - l0) <= tol * abs(l0)
+
+
+def _wide():
+    import sys
+    sys.path.insert(0, HERE)
+    from make_golden import WIDE_CASES, wide_key
+    stored = {}
+    with open(os.path.join(HERE, "oracle_losses_wide.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                key, lp, lm = [x.strip() for x in line.split("|")]
+                stored[key] = (np.array([float(x) for x in lp.split()]), np.array([float(x) for x in lm.split()]))
+    return WIDE_CASES, stored, wide_key
+
+
+def test_wide_fixture_is_complete():
+    cases, stored, key = _wide()
+    for name, _, _, N, _, _, epss in cases:
+        for eps in epss:
+            lp, lm = stored[key(name, eps)]
+            assert lp.size == N and lm.size == N and np.all(np.isfinite(lp)) and np.all(np.isfinite(lm))
+
+
+@pytest.mark.parametrize("name", ["c4", "c3", "c3-rad"])
+def test_oracle_reproduces_stored_wide_losses(oracle, name):
+    """The first probe of each wide case at its largest and smallest eps
+    (c4: the largest only), recomputed (a probe slice of one gives the same losses as in the full
+    set)."""
+    import sys
+    sys.path.insert(0, HERE)
+    from make_golden import wide_inputs
+    cases, stored, key = _wide()
+    (_, workload, probe, N, B, C, epss), = [c for c in cases if c[0] == name]
+    cfg, sd, tok = wide_inputs(name, workload, probe, B, C)
+    theta = oracle.init(cfg, sd["init"])
+    for eps in ((epss[0],) if name == "c4" else (epss[0], epss[-1])):  # c4: ~10 s per probe
+        gp, gm = oracle.perturbed_losses(cfg, theta, sd["step"], eps, 1, tok, as_double=True)
+        lp, lm = stored[key(name, eps)]
+        np.testing.assert_allclose(gp, lp[:1], rtol=1e-13)
+        np.testing.assert_allclose(gm, lm[:1], rtol=1e-13)

@@ -61,6 +61,11 @@ CASES = [
      2, 5, 20, 1e-2, True),
     ("bf16-gauss", dict(n_layers=2, vocab=200, embed=128, hidden=64, wdtype=wl.BF16, probe=wl.GAUSSIAN),
      3, 3, 9, 1e-2, False),
+    # eps below 2^-10: the two-stream products of the bf16 path
+    ("bf16-rad-2stream", dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.RADEMACHER),
+     2, 5, 20, 1e-4, True),
+    ("bf16-gauss-2stream", dict(n_layers=2, vocab=200, embed=128, hidden=64, wdtype=wl.BF16, probe=wl.GAUSSIAN),
+     3, 3, 9, 3e-5, False),
     # B = 128 rows per pass: the 128-row workgroups of the fp32 gate
     ("fp32-wide", dict(n_layers=2, vocab=100, embed=32, hidden=64, wdtype=wl.FP32, probe=wl.RADEMACHER),
      2, 128, 4, 1e-2, True),

@@ -376,18 +376,17 @@ def test_c5_full_size_sampled(zo, oracle):
     ("ragged", dict(n_layers=2, vocab=300, embed=64, hidden=96, wdtype=0, probe=0), 3, 5, 12),
     ("wide-gauss", dict(n_layers=2, vocab=100, embed=64, hidden=96, wdtype=0, probe=1), 2, 64, 6),
 ], ids=["ragged", "wide-gauss"])
-def test_fp32_split_form_matches_oracle(zo, oracle, monkeypatch, name, cfg, N, B, C):
-    """The split form of the fp32 products (ZO_FP32_SPLIT=1: W.h and
-    (s h).(eps z) as two MFMA streams into one accumulator, kept for
-    measurement) against the oracle at the fp32 bar, on 64- and 128-row
-    workgroups."""
+def test_fp32_split_form_matches_oracle(zo, oracle, name, cfg, N, B, C):
+    """The two-stream form of the fp32 products (zo_perturbed_losses_ex with
+    ZO_PRODUCTS_SPLIT: W.h and (s h).(eps z) as two MFMA streams into one
+    accumulator, kept for measurement) against the oracle at the fp32 bar, on
+    64- and 128-row workgroups."""
     say(f"fp32 split form {name}")
-    monkeypatch.setenv("ZO_FP32_SPLIT", "1")
     tok, mask = _tokens_for(name, cfg, B, C, True)
     theta = zo.new_theta(cfg)
     zo.init(cfg, theta, 19)
     td, md = dev_tokens(tok, mask)
-    Lp, Lm = zo.perturbed_losses(cfg, theta, 4545, 1e-2, N, td, md)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 4545, 1e-2, N, td, md, products=zo.PRODUCTS_SPLIT)
     gp, gm = Lp.cpu().numpy(), Lm.cpu().numpy()
     rp, rm = oracle.perturbed_losses(cfg, oracle.init(cfg, 19), 4545, 1e-2, N, tok, mask, as_double=True)
     say("gpu", gp, gm, "oracle", rp, rm)
