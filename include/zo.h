@@ -16,8 +16,7 @@
  * workspace, out) is a device pointer on the current HIP device, allocated
  * and owned by the caller. The library never allocates, frees or retains
  * caller memory. It keeps no state between calls apart from the optional
- * kernel-timing records (zo_profile_enable) and, for zo_perturbed_losses_noalloc,
- * one fixed scratch array per device.
+ * kernel-timing records (zo_profile_enable).
  *
  * Streams. `stream` is a hipStream_t (NULL = the default stream). Every call
  * only enqueues work on that stream and returns; outputs are valid once the

@@ -22,6 +22,7 @@
 #include <type_traits>
 
 #include "zo_kernels.hpp"
+#include "zo_pack.hpp"
 #include "zo_profile.hpp"
 #include "zo_rng.hpp"
 
@@ -617,25 +618,24 @@ hipError_t zero_async(void* p, size_t bytes, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Probe cache fill: eps z (fp32 weights) or fp16(eps z) (bf16 weights) of
-// every weight matrix for probes i0 .. i0+N-1 (layout: ZCacheMap). The values
-// are the ones the forward kernels compute when they regenerate the probe:
-// fp32(eps * z) and fp16 (nearest even) of eps * z of the same normal value z. One thread
-// per Philox block (4 values); the matrices are listed by their start in a
-// probe's block and in theta.
+// Probe cache fill of the fp32 path: eps z of every weight matrix for probes
+// i0 .. i0+N-1 (layout: ZCacheMap, row-major matrices). The values are the
+// ones the forward kernels compute when they regenerate the probe,
+// fp32(eps * z) of the same normal value z. One thread per Philox block (4
+// values); the matrices are listed by their start in a probe's block and in
+// theta.
 struct ZSegs {
   int n;
   uint64_t cstart[2 * kMaxLayers + 2];  // start of matrix m in a probe's block; cstart[n] = P_g
   uint64_t toff[2 * kMaxLayers + 1];    // offset of matrix m in theta
 };
 
-template <typename T>
-__global__ __launch_bounds__(256) void zcache_fill_kernel(T* zc, ZSegs segs, Key key, uint32_t i0, int N,
+__global__ __launch_bounds__(256) void zcache_fill_kernel(float* zc, ZSegs segs, Key key, uint32_t i0, int N,
                                                           float eps) {
   const uint64_t pg = segs.cstart[segs.n];
   const uint64_t nb = pg >> 2;
   for (int n = blockIdx.y; n < N; n += gridDim.y) {
-    T* zp = zc + (uint64_t)n * pg;
+    float* zp = zc + (uint64_t)n * pg;
     for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb;
          b += (uint64_t)gridDim.x * blockDim.x) {
       const uint64_t u = b << 2;
@@ -644,35 +644,89 @@ __global__ __launch_bounds__(256) void zcache_fill_kernel(T* zc, ZSegs segs, Key
       const uint64_t j = segs.toff[m] + (u - segs.cstart[m]);
       float z[4];
       gauss_block(key, i0 + (uint32_t)n, j >> 2, z);
-      if constexpr (sizeof(T) == 2) {
-        *(uint2*)(zp + u) = uint2{pack_f16x2(fmul(eps, z[0]), fmul(eps, z[1])),
-                                  pack_f16x2(fmul(eps, z[2]), fmul(eps, z[3]))};
-      } else {
-        *(f4*)(zp + u) = f4{fmul(eps, z[0]), fmul(eps, z[1]), fmul(eps, z[2]), fmul(eps, z[3])};
-      }
+      *(f4*)(zp + u) = f4{fmul(eps, z[0]), fmul(eps, z[1]), fmul(eps, z[2]), fmul(eps, z[3])};
     }
   }
 }
 
-// fp16 copy of the bf16 weight matrices (layout: ZCacheMap), read by the
-// bf16 path's products in place of theta: bf16 -> fp32 is exact and fp32 ->
-// fp16 rounds to nearest even, exact for every bf16 weight in [2^-14, 65504)
-// (smaller ones keep an absolute error below 2^-25). One thread per 8 values;
-// every matrix holds a multiple of 8 values at a multiple of 8 in theta.
-__global__ __launch_bounds__(256) void w16_fill_kernel(const uint16_t* theta, uint16_t* w16, ZSegs segs) {
-  const uint64_t n8 = segs.cstart[segs.n] >> 3;
-  for (uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n8;
+// The bf16 path's product matrices in fragment-packed order (zo_pack.hpp):
+// their packed start (ZCacheMap offsets, in values), their offset in theta,
+// K, and whether the matrix is the head (vocabulary rows, zero-padded) or a
+// gate matrix (4H rows in the gate column order).
+struct PackSegs {
+  int n;
+  int64_t H, V;
+  uint64_t cstart[2 * kMaxLayers + 2];  // cstart[n] = P_g (padded)
+  uint64_t toff[2 * kMaxLayers + 1];
+  int64_t K[2 * kMaxLayers + 1];
+  int head[2 * kMaxLayers + 1];
+};
+
+// Theta row of packed chunk u (16 bytes) of matrix m and its first k;
+// row < 0 for the head's padding rows.
+__device__ __forceinline__ void packed_source(const PackSegs& segs, uint64_t chunk, int& m, int64_t& row,
+                                              int64_t& k) {
+  const uint64_t u = chunk << 3;
+  m = 0;
+  while (m + 1 < segs.n && u >= segs.cstart[m + 1]) ++m;
+  const PackedChunk pc = packed_chunk((u - segs.cstart[m]) >> 3, segs.K[m]);
+  row = segs.head[m] ? (pc.col < segs.V ? pc.col : -1) : gate_row_of_column(pc.col, segs.H);
+  k = pc.k;
+}
+
+// fp16 copy of the bf16 weight matrices, fragment-packed, read by the bf16
+// path's products in place of theta: bf16 -> fp32 is exact and fp32 -> fp16
+// rounds to nearest even, exact for every bf16 weight in [2^-14, 65504)
+// (smaller ones keep an absolute error below 2^-25). One thread per packed
+// 16-byte chunk (8 consecutive k of one row, 16 bytes of theta).
+__global__ __launch_bounds__(256) void w16_pack_kernel(const uint16_t* theta, uint16_t* w16, PackSegs segs) {
+  const uint64_t nchunks = segs.cstart[segs.n] >> 3;
+  for (uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nchunks;
        q += (uint64_t)gridDim.x * blockDim.x) {
-    const uint64_t u = q << 3;
-    int m = 0;
-    while (m + 1 < segs.n && u >= segs.cstart[m + 1]) ++m;
-    const uint4 v = *(const uint4*)(theta + segs.toff[m] + (u - segs.cstart[m]));
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[4];
+    int m;
+    int64_t row, k;
+    packed_source(segs, q, m, row, k);
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+    if (row >= 0) {
+      const uint4 v = *(const uint4*)(theta + segs.toff[m] + (uint64_t)row * (uint64_t)segs.K[m] + (uint64_t)k);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-      o[d] = pack_f16x2(bf16_to_f32((uint16_t)w[d]), bf16_to_f32((uint16_t)(w[d] >> 16)));
-    *(uint4*)(w16 + u) = uint4{o[0], o[1], o[2], o[3]};
+      for (int d = 0; d < 4; ++d)
+        o[d] = pack_f16x2(bf16_to_f32((uint16_t)w[d]), bf16_to_f32((uint16_t)(w[d] >> 16)));
+    }
+    *(uint4*)(w16 + (q << 3)) = uint4{o[0], o[1], o[2], o[3]};
+  }
+}
+
+// Probe cache of the bf16 path: fp16(eps z) of every product matrix,
+// fragment-packed like the weight copy, for probes i0 .. i0 + N - 1. One
+// thread per packed chunk: 8 consecutive elements j (a multiple of 8), two
+// Philox blocks; zeros for the head's padding rows. The values are those the
+// kernels compute when they regenerate the probe.
+__global__ __launch_bounds__(256) void zcache_pack_kernel(uint16_t* zc, PackSegs segs, Key key, uint32_t i0, int N,
+                                                          float eps) {
+  const uint64_t pg = segs.cstart[segs.n];
+  const uint64_t nchunks = pg >> 3;
+  for (int n = blockIdx.y; n < N; n += gridDim.y) {
+    uint16_t* zp = zc + (uint64_t)n * pg;
+    for (uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nchunks;
+         q += (uint64_t)gridDim.x * blockDim.x) {
+      int m;
+      int64_t row, k;
+      packed_source(segs, q, m, row, k);
+      uint32_t o[4] = {0u, 0u, 0u, 0u};
+      if (row >= 0) {
+        const uint64_t j = segs.toff[m] + (uint64_t)row * (uint64_t)segs.K[m] + (uint64_t)k;
+        float za[4], zb[4];
+        gauss_block(key, i0 + (uint32_t)n, j >> 2, za);
+        gauss_block(key, i0 + (uint32_t)n, (j >> 2) + 1, zb);
+        o[0] = pack_f16x2(fmul(eps, za[0]), fmul(eps, za[1]));
+        o[1] = pack_f16x2(fmul(eps, za[2]), fmul(eps, za[3]));
+        o[2] = pack_f16x2(fmul(eps, zb[0]), fmul(eps, zb[1]));
+        o[3] = pack_f16x2(fmul(eps, zb[2]), fmul(eps, zb[3]));
+      }
+      *(uint4*)(zp + (q << 3)) = uint4{o[0], o[1], o[2], o[3]};
+    }
   }
 }
 
@@ -680,8 +734,8 @@ __global__ __launch_bounds__(256) void w16_fill_kernel(const uint16_t* theta, ui
 
 namespace {
 
-// The product matrices in theta order: their start in a probe-cache (and
-// fp16-copy) block and in theta.
+// The product matrices in theta order: their start in a probe-cache block
+// (fp32 path) and in theta.
 ZSegs matrix_segments(const ForwardArgs& a) {
   const zo_config& c = a.cfg;
   ZSegs segs{};
@@ -699,30 +753,58 @@ ZSegs matrix_segments(const ForwardArgs& a) {
   return segs;
 }
 
+// The same matrices for the bf16 path's packed fp16 weight copy and probe
+// cache.
+PackSegs packed_segments(const ForwardArgs& a) {
+  const zo_config& c = a.cfg;
+  PackSegs segs{};
+  segs.H = c.hidden;
+  segs.V = c.vocab;
+  int m = 0;
+  for (int l = 0; l < c.n_layers; ++l) {
+    segs.cstart[m] = a.zmap.ih[l];
+    segs.toff[m] = a.lay.w_ih[l];
+    segs.K[m] = l == 0 ? c.embed : c.hidden;
+    segs.head[m++] = 0;
+    segs.cstart[m] = a.zmap.hh[l];
+    segs.toff[m] = a.lay.w_hh[l];
+    segs.K[m] = c.hidden;
+    segs.head[m++] = 0;
+  }
+  segs.cstart[m] = a.zmap.out;
+  segs.toff[m] = a.lay.w_out;
+  segs.K[m] = c.hidden;
+  segs.head[m++] = 1;
+  segs.n = m;
+  segs.cstart[m] = a.zmap.pg;
+  return segs;
+}
+
 hipError_t launch_w16_fill(const ForwardArgs& a, hipStream_t st) {
-  const ZSegs segs = matrix_segments(a);
+  const PackSegs segs = packed_segments(a);
   uint64_t grid = (a.zmap.pg / 8 + 255) / 256;
   if (grid > 16384) grid = 16384;
   ProfScope ps(kKWeights16, st);
-  w16_fill_kernel<<<dim3((unsigned)grid), 256, 0, st>>>((const uint16_t*)a.theta, (uint16_t*)a.w16, segs);
+  w16_pack_kernel<<<dim3((unsigned)grid), 256, 0, st>>>((const uint16_t*)a.theta, (uint16_t*)a.w16, segs);
   return hipGetLastError();
 }
 
 hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
   const zo_config& c = a.cfg;
-  const ZSegs segs = matrix_segments(a);
-  const uint64_t nb = a.zmap.pg / 4;
-  uint64_t gx = (nb + 255) / 256;
-  if (gx > 4096) gx = 4096;
   const unsigned gy = (unsigned)(a.rows.N < 65535 ? a.rows.N : 65535);
   const Key key = make_key(a.seed);
   ProfScope ps(kKProbeCache, st);
-  if (c.wdtype == ZO_WBF16)
-    zcache_fill_kernel<uint16_t><<<dim3((unsigned)gx, gy), 256, 0, st>>>((uint16_t*)a.zc, segs, key, a.i0,
-                                                                         a.rows.N, a.eps);
-  else
-    zcache_fill_kernel<float><<<dim3((unsigned)gx, gy), 256, 0, st>>>((float*)a.zc, segs, key, a.i0,
-                                                                      a.rows.N, a.eps);
+  if (c.wdtype == ZO_WBF16) {
+    const PackSegs segs = packed_segments(a);
+    uint64_t gx = (a.zmap.pg / 8 + 255) / 256;
+    if (gx > 4096) gx = 4096;
+    zcache_pack_kernel<<<dim3((unsigned)gx, gy), 256, 0, st>>>((uint16_t*)a.zc, segs, key, a.i0, a.rows.N, a.eps);
+  } else {
+    const ZSegs segs = matrix_segments(a);
+    uint64_t gx = (a.zmap.pg / 4 + 255) / 256;
+    if (gx > 4096) gx = 4096;
+    zcache_fill_kernel<<<dim3((unsigned)gx, gy), 256, 0, st>>>((float*)a.zc, segs, key, a.i0, a.rows.N, a.eps);
+  }
   return hipGetLastError();
 }
 

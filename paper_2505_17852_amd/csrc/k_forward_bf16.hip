@@ -13,30 +13,39 @@
 // whose B fragment each wave forms in registers from the fp16 weight fragment
 // and the probe fragment with one packed fp16 add per pair (+-fp16(eps) for
 // sign probes, expanded from bits; fp16(eps z), sign-flipped for -eps rows,
-// for normal probes). theta +- eps z is never formed in memory.
+// for normal probes). theta +- eps z is never formed in memory. For small eps
+// the two-stream form acc += A . W; acc += A . (s eps z) is used instead
+// (kSplit).
 //
 // Tiles: a workgroup of 8 waves computes TM = 256 rows x TN = 256 columns
 // (waves 2 x 4, wave tiles 128 x 64 = 4 x 2 tiles of 32x32 MFMA output); two
-// waves share each SIMD, so one wave's LDS reads, probe expansion and address
+// waves share each SIMD, so one wave's loads, probe expansion and address
 // work run under the other's matrix instructions. Lane l feeds row/column
 // l % 32 and k block l / 32.
 //
-// LDS (static, one barrier per K tile): per stage the activation tile
-// [TM][TK] and the weight tile [TN][TK] (fp16 rows of 2 TK bytes whose
-// 16-byte chunks are XOR-swizzled by row), copied from global memory straight
-// into LDS without passing through registers, and the probe tile. Sign
-// probes: K tiles of 64 in two stages, the probe tile as sign bits [TN][2]
-// words expanded to fp16 +-eps by each wave. Normal probes: the probe tile is
-// fp16(eps z) [TN][TK], copied from the probe cache like the weights or
-// generated in registers, which takes a third of the stage; K tiles of 32 in
-// three stages (3 x 48 KB) keep the 256 x 256 tile and so copy 48 KB per 16.8
-// MFLOP of matrix work instead of 64 KB with 256 x 128 tiles of 64. K tile
-// it + STAGES - 1 (copies and probe tile) is issued during the MFMAs of tile it.
+// Operands. The LDS of a compute unit serves about 128 bytes per clock, shared
+// between copies into it and fragment reads, and that is what bounds a
+// 256 x 256 tile whose two operands both pass through it (256 KB per K tile of
+// 64: 64 KB copied in, 192 KB read). So only the A operand (the activations,
+// read by the 4 waves of a row half) goes through LDS: each K tile of the 256
+// rows (32 KB) is copied from global memory straight into LDS (buffer loads
+// with the LDS destination, 1 KB per wave instruction), one tile ahead, into
+// one of two stages. The B operand (the fp16 weight copy, and the cached
+// fp16(eps z) of normal probes), read by 2 waves each, is loaded by each wave
+// straight into registers, a few k steps ahead, from the fragment-packed
+// copies the call writes (zo_pack.hpp): one contiguous 1 KB per wave
+// instruction. Every global access is a buffer access against a resource
+// sized to its matrix (or to the workgroup's activation rows), so an offset
+// outside it reads zeros rather than faulting. The probe term: sign probes as
+// sign bits in LDS (one Philox word per 32 k), expanded per fragment; normal
+// probes either regenerated into an LDS tile per K tile or loaded like the
+// weights from the probe cache.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
 
 #include "zo_kernels.hpp"
+#include "zo_pack.hpp"
 #include "zo_profile.hpp"
 #include "zo_rng.hpp"
 
@@ -46,104 +55,73 @@ namespace {
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 constexpr int TM = 256;         // rows per workgroup
 constexpr int NWAVES = 8;
 constexpr int NT = 64 * NWAVES;  // threads per workgroup
-// Global->LDS copies: each copy instruction moves 1 KB (64 lanes x 16 B).
-// kCopyWaves of the 8 waves issue them, spread over the first kCopySteps k
-// steps of the previous K tile.
-constexpr int kCopyWaves = 4;
-constexpr int kCopySteps = 2;
 
-// Sign probes: K per tile and LDS stages.
-constexpr int kSignTK = 64;
-constexpr int kSignStages = 2;
-
-// Per probe kind: K tile, stages, LDS layout, copy split, probe roles.
+// Per probe kind: K tile, LDS layout, copy roles, B-operand prefetch depth.
 template <int kind>
 struct Tiles {
   static constexpr bool kSigns = kind == ZO_RADEMACHER;
-  static constexpr int TK = kSigns ? kSignTK : 32;           // K per tile
-  static constexpr int STAGES = kSigns ? kSignStages : 3;    // LDS stages
-  static constexpr int SW = TK / 32;                         // sign words per row and tile
-  static constexpr int RowBytes = TK * 2;           // one LDS row: TK fp16
-  static constexpr int CPR = RowBytes / 16;         // 16-byte chunks per row
-  static constexpr int RPB = 256 / RowBytes;        // rows per 256 bytes (every LDS bank once)
-  static constexpr int RPC = 1024 / RowBytes;       // rows per 1 KB copy
+  static constexpr bool kZDirect = kind == kGaussCached;  // probe fragments loaded like the weights
+  static constexpr bool kZTile = !kZDirect;               // probe tile formed in LDS (signs or normals)
+  static constexpr int TK = 64;                            // K per tile
+  static constexpr int KSTEPS = TK / 16;                   // MFMA k steps per tile
+  static constexpr int SW = TK / 32;                       // sign words per column and tile
+  static constexpr int RowBytes = TK * 2;                  // one LDS row: TK fp16
   static constexpr int ABytes = TM * RowBytes;
   static constexpr int TN = kVocabTileWide;
   static constexpr int WAVES_N = TN / 64;  // wave tiles are 64 columns wide
   static constexpr int WAVES_M = NWAVES / WAVES_N;
   static constexpr int WROWS = TM / WAVES_M;  // rows per wave tile
   static constexpr int MT = WROWS / 32;
-  static constexpr int WBytes = TN * RowBytes;
-  static constexpr int ZBytes = kSigns ? TN * 4 * SW : TN * RowBytes;
-  static constexpr int StageBytes = ABytes + WBytes + (kSigns ? 0 : ZBytes);  // sign bits: own arrays
-  static constexpr int ACopies = ABytes / 1024 / kCopyWaves;  // activation copies per copying wave
-  static constexpr int WCopies = WBytes / 1024 / kCopyWaves;  // weight copies per copying wave
-  // cached normal probes: the probe tile is copied like the weight tile
-  static constexpr int ZCopies = kind == kGaussCached ? WCopies : 0;
-  static constexpr int Copies = ACopies + WCopies + ZCopies;
-  static constexpr int ZROW_T = NT / TN;     // threads per probe-tile row (normal probes)
-  static constexpr int ZVALS = TK / ZROW_T;  // probe values per thread and K tile (normal probes)
-  // 16-byte slot of chunk c in LDS row r: c ^ swz(r). Any RPB consecutive rows
-  // cover the 64 banks once per chunk, and swz gives the CPR groups of RPB rows
-  // among 16 consecutive rows distinct chunks, so the 16 rows of one 128-bit
-  // fragment read (same chunk) hit every bank exactly once.
-  __device__ static __forceinline__ int swz(int r) { return (r / RPB) & (CPR - 1); }
-  static_assert(RPB * CPR == 16, "swizzle period of 16 rows");
+  static constexpr int ZTileBytes = TN * RowBytes;
+  static constexpr int StageBytes = ABytes + (kZTile ? ZTileBytes : 0);
+  static constexpr int ACopies = ABytes / 1024 / NWAVES;  // activation copies per wave and tile
+  // B fragments for k step s + DIST are loaded at step s, into SLOTS rotating
+  // register sets (the cached probe doubles the loads, so it looks less far
+  // ahead to stay within the registers of two waves per SIMD)
+  static constexpr int DIST = kZDirect ? 1 : 3;
+  static constexpr int SLOTS = DIST + 1;
+  static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
+  // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
+  static constexpr int ZROW_T = NT / TN;
+  static constexpr int ZVALS = TK / ZROW_T;
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
-  static_assert(WCopies * kCopyWaves * 1024 == WBytes && ACopies * kCopyWaves * 1024 == ABytes,
-                "copy split");
-  static_assert(Copies < 64, "outstanding copies fit the vmcnt counter");
-  static_assert(!kSigns || TN * SW <= NT, "at most one sign word per thread");
-  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
-  static_assert(kSigns || (ZVALS % 8 == 0 && ZROW_T * TN == NT), "probe roles");
+  static_assert(ACopies * NWAVES * 1024 == ABytes, "copy split");
+  static_assert(KSTEPS % SLOTS == 0, "the B slots repeat every tile");
+  static_assert(ZVALS == 32 && ZROW_T * TN == NT, "probe roles: one 32-k sign word per thread");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
-  static_assert(TK % 16 == 0 && (TK / 16 == 4 || TK / 16 == 2), "k steps per tile");
+  static_assert(RowBytes == 128, "swizzle of 128-byte rows (act_swizzle)");
 };
 static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole number of row tiles");
-static_assert(Tiles<kGaussCached>::StageBytes == Tiles<ZO_GAUSSIAN>::StageBytes, "normal-probe stages");
 
-// LDS stages per probe kind (static, so that every offset is a constant).
-__shared__ __align__(16) uint8_t lds_r0[Tiles<ZO_RADEMACHER>::StageBytes];
-__shared__ __align__(16) uint8_t lds_r1[Tiles<ZO_RADEMACHER>::StageBytes];
-__shared__ __align__(16) uint8_t lds_r2[Tiles<ZO_RADEMACHER>::StageBytes];
-__shared__ __align__(16) uint8_t lds_r3[Tiles<ZO_RADEMACHER>::StageBytes];
-__shared__ __align__(16) uint32_t lds_b0[Tiles<ZO_RADEMACHER>::ZBytes / 4];
-__shared__ __align__(16) uint32_t lds_b1[Tiles<ZO_RADEMACHER>::ZBytes / 4];
-__shared__ __align__(16) uint32_t lds_b2[Tiles<ZO_RADEMACHER>::ZBytes / 4];
-__shared__ __align__(16) uint32_t lds_b3[Tiles<ZO_RADEMACHER>::ZBytes / 4];
-__shared__ __align__(16) uint8_t lds_g0[Tiles<ZO_GAUSSIAN>::StageBytes];
-__shared__ __align__(16) uint8_t lds_g1[Tiles<ZO_GAUSSIAN>::StageBytes];
-__shared__ __align__(16) uint8_t lds_g2[Tiles<ZO_GAUSSIAN>::StageBytes];
-static_assert(Tiles<ZO_RADEMACHER>::STAGES * (sizeof(lds_r0) + sizeof(lds_b0)) <= 160 * 1024, "LDS");
-static_assert(Tiles<ZO_GAUSSIAN>::STAGES * sizeof(lds_g0) <= 160 * 1024, "LDS");
+// LDS stages (static, so that every offset is a constant): activation tile
+// and probe tile (sign and regenerated normal probes), or the activation tile
+// alone (cached normal probes).
+__shared__ __align__(16) uint8_t lds_s0[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_s1[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_c0[Tiles<kGaussCached>::StageBytes];
+__shared__ __align__(16) uint8_t lds_c1[Tiles<kGaussCached>::StageBytes];
+static_assert(Tiles<ZO_GAUSSIAN>::StageBytes == Tiles<ZO_RADEMACHER>::StageBytes, "probe-tile stages");
+static_assert(2 * sizeof(lds_s0) <= 160 * 1024, "LDS");
 
 template <int kind, int S>
 __device__ __forceinline__ uint8_t* stage() {
-  static_assert(S >= 0 && S < Tiles<kind>::STAGES, "stage index");
-  if constexpr (kind == ZO_RADEMACHER)
-    return S == 0 ? lds_r0 : S == 1 ? lds_r1 : S == 2 ? lds_r2 : lds_r3;
+  static_assert(S == 0 || S == 1, "stage index");
+  if constexpr (kind == kGaussCached)
+    return S == 0 ? lds_c0 : lds_c1;
   else
-    return S == 0 ? lds_g0 : S == 1 ? lds_g1 : lds_g2;
-}
-template <int S>
-__device__ __forceinline__ uint32_t* sign_bits() {
-  static_assert(S >= 0 && S < Tiles<ZO_RADEMACHER>::STAGES, "stage index");
-  return S == 0 ? lds_b0 : S == 1 ? lds_b1 : S == 2 ? lds_b2 : lds_b3;
+    return S == 0 ? lds_s0 : lds_s1;
 }
 
 __device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
 
-// Probe sign bits in LDS are kept in "unshuffled" order: the word of 32
-// consecutive k holds the negative-sign flags (1 = -1) of the even elements
-// 0, 2, .., 30 in bits 0..15 and of the odd elements 1, 3, .., 31 in bits
-// 16..31. The two elements of one packed fp16 pair then sit 16 bits apart,
-// so one shift, one mask and one xor turn them into the pair (+-e, +-e): the
-// flag of the even element lands on bit 15 and that of the odd one on bit
-// 31, and flip the sign bits of the constant pair (e, e).
+// The word of 32 consecutive sign flags with the even elements' flags moved
+// to bits 0..15 and the odd elements' to bits 16..31 (in order), so that the
+// two elements of one packed fp16 pair sit 16 bits apart.
 __device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
   uint32_t t;
   t = (x ^ (x >> 1)) & 0x22222222u;
@@ -157,16 +135,24 @@ __device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
   return x;
 }
 
-// 16 bytes per lane from global memory straight into LDS: the wave's 64
-// lanes fill the 1 KB at lds (wave-uniform), lane L at lds + 16 L. Written as
-// an asm statement, so the compiler inserts no waits of its own for these
-// copies; the K-tile loop waits for them explicitly (vmcnt) before each barrier.
-__device__ __forceinline__ void copy_to_lds(const void* src, uint8_t* lds) {
-  const uint32_t m0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+// A raw buffer resource over [base, base + bytes), bytes < 2^31.
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// Wait until at most VM of this thread's global->LDS copies are outstanding
+// 16 bytes per lane from global memory straight into LDS: the wave's 64
+// lanes fill the 1 KB at lds (wave-uniform), lane L at lds + 16 L; the
+// address is the resource base + voff (per lane) + soff (wave-uniform).
+__device__ __forceinline__ void copy_to_lds(Rsrc r, uint32_t voff, uint32_t soff, uint8_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0, 0);
+}
+
+// One 16-byte B fragment piece per lane, straight into registers.
+__device__ __forceinline__ h8 load_frag(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Wait until at most VM of this thread's vector memory loads are outstanding
 // and its LDS accesses are complete (s_waitcnt vmcnt(VM) lgkmcnt(0); the gfx9
 // encoding splits vmcnt into bits 3:0 and 15:14, expcnt 7 = no wait), then a
 // workgroup barrier without a memory fence. The empty asm statements keep the
@@ -180,21 +166,35 @@ __device__ __forceinline__ void wait_and_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Keeps the compiler from moving memory accesses or scheduling instructions
+// across this point (the load counts of wait_and_barrier depend on the order
+// in which the tile's loads are issued).
+__device__ __forceinline__ void issue_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// One K segment of a product: the activations (A, rows of the workgroup's
+// tile), the packed fp16 weight copy (B) and, for cached normal probes, this
+// probe's packed fp16(eps z) of the same matrix.
 struct SegB {
   const uint16_t* A;  // first row of this workgroup's activation tile; row r at A + r * lda
   int64_t lda;
-  const uint16_t* W;  // weight row n at W + n * ldw (the fp16 copy of the matrix)
-  int64_t ldw;
+  const uint16_t* W;  // packed fp16 weights of the matrix (cols x K)
+  uint32_t wbytes;    // bytes of the packed matrix
   uint64_t zoff;      // offset of the matrix inside theta (probe coordinates)
+  int64_t ldw;        // row stride of the matrix in theta (= K)
   int K;
-  const uint16_t* Z;  // kGaussCached: fp16(eps z) of this probe and matrix, laid out like W
+  const uint16_t* Z;  // kGaussCached: fp16(eps z) of this probe and matrix, packed like W
 };
 
-// acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave.
-// colmap(rho, &n) maps LDS column rho (0..TN-1) to a weight row n inside the
-// matrix (columns beyond the matrix map to a valid row; they are never
-// scored). sgn: the sign of eps for this wave's rows (+1, -1, or 0 for the
-// clean pass of forward differences, kFD only); eps_b: fp16 bits of eps.
+// acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave. cb0: the
+// packed column block of the workgroup's first column (8 per 256 columns).
+// colmap(rho, &n) maps workgroup column rho (0..TN-1) to the weight row n in
+// theta that carries its probe coordinates (columns beyond the matrix map to
+// a valid row; they are never scored). sgn: the sign of eps for this wave's
+// rows (+1, -1, or 0 for the clean pass of forward differences); eps_b: fp16
+// bits of eps.
 // kTrans: accumulate the transposed product (weight columns on the rows of
 // each 32x32 tile, activation rows on its columns): both operands of
 // v_mfma_f32_32x32x16_f16 have the same fragment layout, so only their order
@@ -205,77 +205,103 @@ struct SegB {
 // instead of acc += A.fp16(W + s eps z): a weight fragment rounded with the
 // probe added loses up to half an fp16 ulp of w per element, which is a
 // large share of eps z once eps is small against |w|.
-template <int kind, bool kTrans = false, bool kFD = false, bool kSplit = false, typename ColMap>
+template <int kind, bool kTrans = false, bool kSplit = false, typename ColMap>
 __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
-                                              int nseg, ColMap colmap, Key key, uint32_t probe, int sgn,
-                                              float eps, uint16_t eps_b) {
+                                              int nseg, int64_t cb0, ColMap colmap, Key key, uint32_t probe,
+                                              int sgn, float eps, uint16_t eps_b) {
   using T = Tiles<kind>;
   constexpr int MT = T::MT;
+  constexpr int TK = T::TK;
+  constexpr int KSTEPS = T::KSTEPS;
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
-  constexpr int TK = T::TK;
+  const int ks0 = s0.K / 16;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
+  const int nsteps = ntiles * KSTEPS;
 
-  // copy roles: copy q of copying wave w fills rows RPC (q kCopyWaves + w) .. +RPC-1
-  // of the activation (q < ACopies) or weight tile, 1 KB lane-linear in LDS:
-  // lane L writes row + L / CPR, slot L % CPR, which holds chunk (L % CPR) ^ swz(row)
-  const int crow = lane / T::CPR;
-  int arow[T::ACopies], wrow[T::WCopies];
-  uint32_t aoff[T::ACopies], woff[T::WCopies];  // element offsets of the chunk inside the row
+  // Buffer resources: the workgroup's activation rows and the packed matrices
+  // of each segment (the probe cache per probe).
+  const Rsrc ra0 = make_rsrc(s0.A, (uint32_t)(TM * s0.lda * 2));
+  const Rsrc ra1 = make_rsrc(s1.A, (uint32_t)(TM * s1.lda * 2));
+  const Rsrc rw0 = make_rsrc(s0.W, s0.wbytes), rw1 = make_rsrc(s1.W, s1.wbytes);
+  Rsrc rz0 = rw0, rz1 = rw1;
+  if constexpr (T::kZDirect) {
+    rz0 = make_rsrc(s0.Z, s0.wbytes);
+    rz1 = make_rsrc(s1.Z, s1.wbytes);
+  }
+  // activation copies: copy q of this wave fills LDS rows act_row_of_copy(q,
+  // wave, lane); its per-lane offset is row * lda * 2 + chunk * 16, the K
+  // tile adds 2 k0 bytes (wave-uniform)
+  uint32_t arow2[T::ACopies], achunk[T::ACopies];
 #pragma unroll
   for (int q = 0; q < T::ACopies; ++q) {
-    const int r = T::RPC * (q * kCopyWaves + wave % kCopyWaves) + crow;
-    arow[q] = r;
-    aoff[q] = 8u * (uint32_t)((lane % T::CPR) ^ T::swz(r));
+    const int r = act_row_of_copy(q, wave, lane, NWAVES);
+    arow2[q] = (uint32_t)r;
+    achunk[q] = 16u * (uint32_t)((lane % 8) ^ act_swizzle(r));
   }
-#pragma unroll
-  for (int q = 0; q < T::WCopies; ++q) {
-    const int r = T::RPC * (q * kCopyWaves + wave % kCopyWaves) + crow;
-    colmap(r, wrow[q]);
-    woff[q] = 8u * (uint32_t)((lane % T::CPR) ^ T::swz(r));
-  }
-  // probe roles: signs, threads t < TN SW: row t / SW, one 32-k word at 32 (t % SW);
-  //              normal, every thread: row t / ZROW_T, ZVALS k at ZVALS (t % ZROW_T)
-  const int zr = kind == ZO_RADEMACHER ? t / T::SW : t / T::ZROW_T;
-  const int zpart = kind == ZO_RADEMACHER ? (t % T::SW) : (t % T::ZROW_T);
+  const uint32_t lda2_0 = (uint32_t)(2 * s0.lda), lda2_1 = (uint32_t)(2 * s1.lda);
+  // B fragments: lane part of the packed offset (the block and k step parts
+  // are wave-uniform and go in the scalar offset)
+  const uint32_t blane = (uint32_t)lane * 16u;
+  const int64_t cbw = cb0 + 2 * wn;
+  // probe-tile roles: column zr, 32 k at 32 zpart
+  const int zr = t / T::ZROW_T, zpart = t % T::ZROW_T;
   int zn;
   colmap(zr, zn);
 
-  Words zcache{{0u, 0u, 0u, 0u}};
-  int seg = 0, k0 = 0;
-
-  // Issue the next K tile into stage S, in four parts spread over the
-  // current tile's k steps (so that no wave stalls on a burst of copies):
-  // parts 0 and 1 the global->LDS copies of the activation and weight rows,
-  // half each; part 2 the probe tile, computed in registers and written to
-  // LDS; part 3 advances to the following tile.
-  auto issue = [&](auto stage_tag, auto part_tag) {
-    constexpr int S = decltype(stage_tag)::value;
-    constexpr int P = decltype(part_tag)::value;
-    uint8_t* base = stage<kind, S>();
-    const SegB sg = seg == 0 ? s0 : s1;
-    if (wave < kCopyWaves) {
+  // B fragments in flight: slot j holds the (weight, probe) fragments of the
+  // k steps j, j + SLOTS, ... Every load below is issued unconditionally
+  // (past the last k step it repeats the last one, and past the last tile
+  // the copies repeat the last tile into the idle stage), so that the number
+  // of loads between any two points of the loop is fixed: the compiler then
+  // waits for each fragment with an exact count, and wait_and_barrier's counts
+  // hold.
+  h8 wfr[T::SLOTS][2], zfr[T::kZDirect ? T::SLOTS : 1][2];
+  // k step gs (global over both segments) -> segment and k step inside it
+  auto load_b = [&](auto slot_tag, int gs) {
+    constexpr int SL = decltype(slot_tag)::value;
+    gs = gs < nsteps ? gs : nsteps - 1;
+    const bool second = gs >= ks0;
+    const uint32_t ks = (uint32_t)(second ? gs - ks0 : gs);
+    const uint32_t KS = (uint32_t)(second ? s1.K : s0.K) / 16u;
 #pragma unroll
-      for (int c = P * T::Copies / kCopySteps; c < (P < kCopySteps ? (P + 1) * T::Copies / kCopySteps : 0); ++c) {
-        if (c < T::ACopies) {
-          copy_to_lds(sg.A + (int64_t)arow[c] * sg.lda + k0 + aoff[c], base + (c * kCopyWaves + wave) * 1024);
-        } else if (c < T::ACopies + T::WCopies) {
-          const int q = c - T::ACopies;
-          copy_to_lds(sg.W + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
-                      base + T::ABytes + (q * kCopyWaves + wave) * 1024);
-        } else {  // cached probe rows: the same rows and chunk order as the weight copy q
-          const int q = c - T::ACopies - T::WCopies;
-          copy_to_lds(sg.Z + (int64_t)wrow[q] * sg.ldw + k0 + woff[q],
-                      base + T::ABytes + T::WBytes + (q * kCopyWaves + wave) * 1024);
-        }
-      }
+    for (int nt = 0; nt < 2; ++nt) {
+      const uint32_t soff = ((uint32_t)(cbw + nt) * KS + ks) * (uint32_t)kPackBlockBytes;
+      wfr[SL][nt] = load_frag(second ? rw1 : rw0, blane, soff);
+      if constexpr (T::kZDirect) zfr[SL][nt] = load_frag(second ? rz1 : rz0, blane, soff);
     }
-    if constexpr (P == 2 && kind == ZO_RADEMACHER) {
-      if (T::TN * T::SW == NT || t < T::TN * T::SW) {
-      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + 32 * zpart;
+  };
+
+  Words zcache{{0u, 0u, 0u, 0u}};
+  int seg = 0, k0 = 0;  // the next tile to be copied (stays on the last tile once past it)
+
+  // The next K tile's activation copies into stage S (issued first in a tile,
+  // so that the loads after them are the B loads of this tile: the count
+  // wait_and_barrier leaves in flight).
+  auto issue_copies = [&](auto stage_tag) {
+    constexpr int S = decltype(stage_tag)::value;
+    uint8_t* base = stage<kind, S>();
+    const bool second = seg != 0;
+    const uint32_t lda2 = second ? lda2_1 : lda2_0;
+#pragma unroll
+    for (int q = 0; q < T::ACopies; ++q)
+      copy_to_lds(second ? ra1 : ra0, arow2[q] * lda2 + achunk[q], 2u * (uint32_t)k0,
+                  base + (q * NWAVES + wave) * 1024);
+  };
+  // The next K tile's probe tile into stage S, fp16(+eps z) of the tile's
+  // TN columns and TK k, 32 k per thread (sign probes: one Philox word,
+  // expanded; normal probes: eight Box-Muller blocks); then advance to the
+  // following tile. Cached normal probes have no probe tile.
+  const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
+  auto issue_probe = [&](auto stage_tag) {
+    constexpr int S = decltype(stage_tag)::value;
+    const SegB& sg = seg == 0 ? s0 : s1;
+    uint8_t* zrow = stage<kind, S>() + T::ABytes + zr * T::RowBytes;
+    const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
+    if constexpr (T::kSigns) {
       uint32_t word;
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
       if (aligned) {
@@ -285,110 +311,99 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       } else {
         word = rademacher_word(key, probe, j0 >> 5);
       }
-      // negative-sign flags in unshuffled order
-      sign_bits<S>()[zr * T::SW + zpart] = unshuffle_bits(~word);
-      }
-    } else if constexpr (P == 2 && kind == ZO_GAUSSIAN) {
-      const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
-      uint8_t* zrow = base + T::ABytes + T::WBytes + zr * T::RowBytes;
+      // negative-sign flags, even elements in bits 0..15 and odd ones in
+      // 16..31: the pair (2i, 2i+1) is fp16(eps) with the flags of bits i
+      // and 16 + i as sign bits
+      const uint32_t u = unshuffle_bits(~word);
 #pragma unroll
-      for (int q = 0; q < T::ZVALS / 8; ++q) {
+      for (int c = 0; c < 4; ++c) {
+        u4 v;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) v[d] = ((u << (15 - (4 * c + d))) & 0x80008000u) | ebits;
+        *(u4*)(zrow + 16 * ((4 * zpart + c) ^ act_swizzle(zr))) = v;
+      }
+    } else if constexpr (T::kZTile) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
         float za[4], zb[4];
-        gauss_block(key, probe, (j0 >> 2) + 2 * q, za);
-        gauss_block(key, probe, (j0 >> 2) + 2 * q + 1, zb);
-        const int chunk = (T::ZVALS / 8) * zpart + q;
-        *(u4*)(zrow + 16 * (chunk ^ T::swz(zr))) =
+        gauss_block(key, probe, (j0 >> 2) + 2 * c, za);
+        gauss_block(key, probe, (j0 >> 2) + 2 * c + 1, zb);
+        *(u4*)(zrow + 16 * ((4 * zpart + c) ^ act_swizzle(zr))) =
             u4{pack_f16x2(eps * za[0], eps * za[1]), pack_f16x2(eps * za[2], eps * za[3]),
                pack_f16x2(eps * zb[0], eps * zb[1]), pack_f16x2(eps * zb[2], eps * zb[3])};
       }
     }
-    if constexpr (P == 3) {
-      k0 += TK;
-      if (k0 == sg.K) {
+    k0 += TK;
+    if (k0 == sg.K) {
+      if (seg + 1 < nseg) {
         k0 = 0;
         ++seg;
+      } else {
+        k0 -= TK;
       }
     }
-  };
-  auto issue_all = [&](auto stage_tag) {
-    issue(stage_tag, std::integral_constant<int, 0>{});
-    issue(stage_tag, std::integral_constant<int, 1>{});
-    issue(stage_tag, std::integral_constant<int, 2>{});
-    issue(stage_tag, std::integral_constant<int, 3>{});
   };
 
-  // Fragments of one 16-k step: activations (MT row tiles), weights and
-  // probe values (2 column tiles). The next step's LDS reads and sign
-  // expansion are issued between the current step's MFMAs (software
-  // pipelining within the K tile). Lane (lr, lg) reads chunk 2 s + lg of its
-  // rows, in slot (2 s) ^ y with y = lg ^ swz(lr) (every row offset below is
-  // a multiple of 16, the swizzle period).
-  const uint32_t y = (uint32_t)(lg ^ T::swz(lr));
+  // Fragments of one 16-k step: activations (MT row tiles) and probe values
+  // (2 column tiles) from LDS, the next step's read while the current one
+  // computes. Lane (lr, lg) reads chunk 2 s + lg of its rows, in slot
+  // (2 s) ^ y with y = lg ^ swz(lr) (every row offset below is a multiple of
+  // 16, the swizzle period).
+  const uint32_t y = (uint32_t)(lg ^ act_swizzle(lr));
   const uint32_t a_lane = (uint32_t)(T::WROWS * wm + lr) * T::RowBytes;
-  const uint32_t w_lane = (uint32_t)(64 * wn + lr) * T::RowBytes;
-  // the pair (s eps, s eps) in fp16 (signs), or the sign flip of -eps rows (normal)
-  const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
-  const bool neg = sgn < 0;
-  const uint32_t zc = kind == ZO_RADEMACHER ? (neg ? ebits ^ 0x80008000u : ebits) : (neg ? 0x80008000u : 0u);
-  // forward differences: the clean pass multiplies its probe fragments by 0
-  const uint32_t zmask = sgn == 0 ? 0u : 0xFFFFFFFFu;
+  const uint32_t z_lane = (uint32_t)(64 * wn + lr) * T::RowBytes;
+  // the sign of eps of this wave's rows as a packed fp16 pair (+-1, or 0 for
+  // the clean pass): B = fp16(W + s eps z) is one packed fp16 fma per pair
+  const _Float16 sh = (_Float16)(float)sgn;
+  const h8 s8 = {sh, sh, sh, sh, sh, sh, sh, sh};
   struct Frag {
-    h8 a[MT], w[2], z[2];
+    h8 a[MT], z[2];
   };
-  auto compute = [&](auto stage_tag, bool more) {
+  auto compute = [&](auto stage_tag, int it) {
     constexpr int S = decltype(stage_tag)::value;
+    constexpr std::integral_constant<int, 1 - S> next{};
     const uint8_t* base = stage<kind, S>();
     const uint8_t* pa = base + a_lane;
-    const uint8_t* pw = base + T::ABytes + w_lane;
-    // per lane, the flags of its k block pre-shifted so that a constant shift
-    // per (k step, pair) brings them to bits 15 / 31 (see unshuffle_bits)
-    uint32_t bits[2][2];
-    if constexpr (kind == ZO_RADEMACHER) {
-      const uint32_t pre = 4u * (uint32_t)(1 - lg);
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        if constexpr (T::SW == 2) {
-          const uint2 v = *(const uint2*)(sign_bits<S>() + (64 * wn + 32 * nt + lr) * 2);
-          bits[nt][0] = v.x << pre;
-          bits[nt][1] = v.y << pre;
-        } else {
-          bits[nt][0] = sign_bits<S>()[64 * wn + 32 * nt + lr] << pre;
-          bits[nt][1] = 0u;
-        }
-      }
-    }
+    const uint8_t* pz = base + T::ABytes + z_lane;
     auto load = [&](int s, Frag& f) {
       const uint32_t so = 16u * ((uint32_t)(2 * s) ^ y);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) f.a[mt] = as_h8(*(const u4*)(pa + 32 * mt * T::RowBytes + so));
+      if constexpr (T::kZTile) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        f.w[nt] = as_h8(*(const u4*)(pw + 32 * nt * T::RowBytes + so));
-        u4 v;
-        if constexpr (kind == ZO_RADEMACHER) {
-          const uint32_t x = bits[nt][s >> 1];
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            v[d] = ((x << (11 - 8 * (s & 1) - d)) & 0x80008000u) ^ zc;
-            if constexpr (kFD) v[d] &= zmask;
-          }
-        } else {
-          v = *(const u4*)(pw + T::WBytes + 32 * nt * T::RowBytes + so);
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            v[d] ^= zc;
-            if constexpr (kFD) v[d] &= zmask;
-          }
-        }
-        f.z[nt] = as_h8(v);
+        for (int nt = 0; nt < 2; ++nt) f.z[nt] = as_h8(*(const u4*)(pz + 32 * nt * T::RowBytes + so));
       }
     };
     Frag f[2];
     load(0, f[0]);
 #pragma unroll
-    for (int s = 0; s < TK / 16; ++s) {
+    for (int s = 0; s < KSTEPS; ++s) {
       const Frag& c = f[s & 1];
-      if (s + 1 < TK / 16) load(s + 1, f[(s + 1) & 1]);
+      if (s == 0) {
+        // the next tile's activation copies first, then this step's B loads
+        issue_copies(next);
+        issue_fence();
+      }
+      // B fragments DIST steps ahead
+      switch ((s + T::DIST) % T::SLOTS) {
+        case 0: load_b(std::integral_constant<int, 0>{}, it * KSTEPS + s + T::DIST); break;
+        case 1: if constexpr (T::SLOTS > 1) load_b(std::integral_constant<int, 1 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
+        case 2: if constexpr (T::SLOTS > 2) load_b(std::integral_constant<int, 2 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
+        default: if constexpr (T::SLOTS > 3) load_b(std::integral_constant<int, 3 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
+      }
+      if (s + 1 < KSTEPS) load(s + 1, f[(s + 1) & 1]);
+      // this step's weight fragments (slot s % SLOTS) and probe fragments
+      h8 w[2], z[2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        switch (s % T::SLOTS) {
+          case 0: w[nt] = wfr[0][nt]; if constexpr (T::kZDirect) z[nt] = zfr[0][nt]; break;
+          case 1: w[nt] = wfr[1 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[1 % T::SLOTS][nt]; break;
+          case 2: w[nt] = wfr[2 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[2 % T::SLOTS][nt]; break;
+          default: w[nt] = wfr[3 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[3 % T::SLOTS][nt]; break;
+        }
+        if constexpr (T::kZTile) z[nt] = c.z[nt];
+      }
       auto mma = [&](const h8(&b)[2]) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
@@ -400,85 +415,49 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       if constexpr (kSplit) {
         // A.W for every accumulator, then A.(s eps z): the two products into
         // one accumulator are MT x 2 instructions apart
-        mma(c.w);
-        mma(c.z);
+        h8 sz[2];
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) sz[nt] = z[nt] * s8;
+        mma(w);
+        mma(sz);
       } else {
-        // B = fp16(W + s eps z): one packed fp16 add per pair (round to
-        // nearest even), then one MFMA per accumulator
+        // B = fp16(W + s eps z): one packed fp16 fma per pair (s z exact,
+        // one rounding to nearest even), then one MFMA per accumulator
         h8 wz[2];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) wz[nt] = c.w[nt] + c.z[nt];
+        for (int nt = 0; nt < 2; ++nt) wz[nt] = __builtin_elementwise_fma(z[nt], s8, w[nt]);
         mma(wz);
       }
-      if (more) {
-        // tile it + STAGES - 1 goes to the stage tile it - 1 used
-        constexpr std::integral_constant<int, (S + T::STAGES - 1) % T::STAGES> next{};
-        if constexpr (TK / 16 == 4) {
-          if (s == 0) issue(next, std::integral_constant<int, 0>{});
-          if (s == 1) issue(next, std::integral_constant<int, 1>{});
-          if (s == 2) issue(next, std::integral_constant<int, 2>{});
-          if (s == 3) issue(next, std::integral_constant<int, 3>{});
-        } else {
-          if (s == 0) {
-            issue(next, std::integral_constant<int, 0>{});
-            issue(next, std::integral_constant<int, 1>{});
-          }
-          if (s == 1) {
-            issue(next, std::integral_constant<int, 2>{});
-            issue(next, std::integral_constant<int, 3>{});
-          }
-        }
-      }
-      if (s + 1 < TK / 16) {
-        // per step: the next step's LDS reads first, then each MFMA followed by
-        // a few VALU instructions of the next step's probe fragments
-        __builtin_amdgcn_sched_group_barrier(0x100, MT + 2 + (kind == ZO_RADEMACHER ? 0 : 2), 0);
-#pragma unroll
-        for (int i = 0; i < (kSplit ? 4 : 2) * MT; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-        }
-      }
+      if (s == 2) issue_probe(next);
     }
   };
 
-  // K tile it lives in stage it % STAGES. Per tile: wait for this thread's
-  // copies of tile it (with three stages those of tile it + 1, issued later,
-  // may stay in flight) and its LDS writes; barrier (tile it complete for
-  // every wave, and the stage computed at it - 1 free); compute it while
-  // issuing tile it + STAGES - 1 into that stage.
-  auto step = [&](auto stage_tag, int it) {
-    // the copies of tiles it + 1 .. it + STAGES - 2 (those issued) may stay in flight
-    if constexpr (T::STAGES == 4) {
-      if (it + 2 < ntiles) wait_and_barrier<2 * T::Copies>();
-      else if (it + 1 < ntiles) wait_and_barrier<T::Copies>();
-      else wait_and_barrier<0>();
-    } else if constexpr (T::STAGES == 3) {
-      if (it + 1 < ntiles) wait_and_barrier<T::Copies>();
-      else wait_and_barrier<0>();
-    } else {
-      wait_and_barrier<0>();
-    }
-    compute(stage_tag, it + T::STAGES - 1 < ntiles);
-  };
-  issue_all(std::integral_constant<int, 0>{});
-  if constexpr (T::STAGES >= 3) {
-    if (ntiles > 1) issue_all(std::integral_constant<int, 1>{});
+  // K tile it lives in stage it % 2. Before tile it: wait for this thread's
+  // copies of tile it (the B loads issued after them may stay in flight) and
+  // its LDS writes; barrier (tile it complete for every wave, and the stage
+  // computed at it - 1 free); compute it while issuing tile it + 1 into the
+  // other stage. Prologue: tile 0's copies and probe tile, the first DIST
+  // steps' B loads.
+  issue_copies(std::integral_constant<int, 0>{});
+  issue_fence();
+  if constexpr (T::DIST >= 1) load_b(std::integral_constant<int, 0>{}, 0);
+  if constexpr (T::DIST >= 2) load_b(std::integral_constant<int, 1>{}, 1);
+  if constexpr (T::DIST >= 3) load_b(std::integral_constant<int, 2>{}, 2);
+  issue_probe(std::integral_constant<int, 0>{});
+  // loads issued after the copies of the tile a barrier waits for: the first
+  // DIST steps' B loads (prologue), then a whole tile's (every later tile)
+  constexpr int kAfter0 = T::DIST * T::LoadsPerStep;
+  constexpr int kAfter = KSTEPS * T::LoadsPerStep;
+  wait_and_barrier<kAfter0>();
+  int it = 0;
+  for (; it + 1 < ntiles; it += 2) {
+    compute(std::integral_constant<int, 0>{}, it);
+    wait_and_barrier<kAfter>();
+    compute(std::integral_constant<int, 1>{}, it + 1);
+    wait_and_barrier<kAfter>();
   }
-  if constexpr (T::STAGES >= 4) {
-    if (ntiles > 2) issue_all(std::integral_constant<int, 2>{});
-  }
-  for (int it = 0; it < ntiles; it += T::STAGES) {
-    step(std::integral_constant<int, 0>{}, it);
-    if (it + 1 < ntiles) step(std::integral_constant<int, 1>{}, it + 1);
-    if constexpr (T::STAGES >= 3) {
-      if (it + 2 < ntiles) step(std::integral_constant<int, 2 % T::STAGES>{}, it + 2);
-    }
-    if constexpr (T::STAGES >= 4) {
-      if (it + 3 < ntiles) step(std::integral_constant<int, 3 % T::STAGES>{}, it + 3);
-    }
-  }
-  __syncthreads();  // every wave done with the stages before they are reused
+  if (it < ntiles) compute(std::integral_constant<int, 0>{}, it);
+  __syncthreads();  // every wave done with the stages (and every copy landed) before they are reused
 }
 
 // Tile (row block m, column block n) of workgroup L of a 1-D grid of nm x nn
@@ -566,12 +545,12 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   f16v acc[T::MT][2];
   zero_acc(acc);
   const uint64_t zpos = (uint64_t)pair * g.zc_stride;
-  const SegB s0{g.x + m0 * g.El, g.El, g.w_ih16, g.El, g.off_ih, g.El,
+  const SegB s0{g.x + m0 * g.El, g.El, g.w_ih16, (uint32_t)((uint64_t)4 * H * g.El * 2), g.off_ih, g.El, g.El,
                 kind == kGaussCached ? g.zc_ih + zpos : nullptr};
-  const SegB s1{g.hprev + m0 * H, H, g.w_hh16, H, g.off_hh, H,
+  const SegB s1{g.hprev + m0 * H, H, g.w_hh16, (uint32_t)((uint64_t)4 * H * H * 2), g.off_hh, H, H,
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
-  mainloop_bf16<kind, false, kFD, kSplit>(acc, s0, s1, 2, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps,
-                                          g.eps_b);
+  mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, 8 * (int64_t)nb, colmap, g.key, g.i0 + (uint32_t)pair,
+                                          sgn, g.eps, g.eps_b);
 
   const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
   const int u = u0 + 16 * wn + (lr & 15);
@@ -649,10 +628,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
   f16v acc[T::MT][2];
   zero_acc(acc);
-  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, g.H, g.off_w, g.H,
+  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, (uint32_t)((uint64_t)g.nvt * T::TN * g.H * 2), g.off_w, g.H, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
-  mainloop_bf16<kind, true, kFD, kSplit>(acc, s0, s0, 1, colmap, g.key, g.i0 + (uint32_t)pair, sgn, g.eps,
-                                         g.eps_b);
+  mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, 8 * (int64_t)vt, colmap, g.key, g.i0 + (uint32_t)pair,
+                                         sgn, g.eps, g.eps_b);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)

@@ -129,15 +129,19 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // timestep and row tile, while each value is the same for the whole call.
 // With a large enough workspace the call first writes, once, the values the
 // kernels would otherwise regenerate: eps z in fp32 (fp32 weights) or
-// bf16(eps z) (bf16 weights), for probes i0 .. i0+N-1. Layout: probe n's
-// block of P_g values (the matrices in theta order, each row-major like the
-// matrix itself) at n * P_g. Sign probes are cheap to regenerate and are
-// never cached.
+// fp16(eps z) (bf16 weights), for probes i0 .. i0+N-1. Layout: probe n's
+// block of P_g values (the matrices in theta order) at n * P_g; each matrix
+// row-major like the matrix itself (fp32 weights) or fragment-packed like the
+// fp16 weight copy (bf16 weights, zo_pack.hpp). Sign probes are cheap to
+// regenerate and are never cached. The same map places the matrices of the
+// bf16 path's fp16 weight copy; there the head matrix is padded with zero
+// rows to a whole number of 256-wide vocabulary tiles.
 struct ZCacheMap {
   uint64_t pg;              // values per probe: the matrices' total size
   uint64_t ih[kMaxLayers];  // offsets of each matrix inside a probe's block
   uint64_t hh[kMaxLayers];
   uint64_t out;
+  uint64_t out_rows;        // rows of the head matrix as stored (V, or padded on the bf16 path)
 };
 
 inline ZCacheMap make_zcache_map(const zo_config& c) {
@@ -151,7 +155,8 @@ inline ZCacheMap make_zcache_map(const zo_config& c) {
     p += 4 * H * H;
   }
   m.out = p;
-  p += V * H;
+  m.out_rows = c.wdtype == ZO_WBF16 ? (V + kVocabTileWide - 1) / kVocabTileWide * kVocabTileWide : V;
+  p += m.out_rows * H;
   m.pg = p;
   return m;
 }

@@ -102,6 +102,9 @@ def main(argv=None):
                     help="draw a new batch of the workload's distribution every step (seed data + 1 + k) "
                          "and evaluate on a held-out batch; default: one fixed batch")
     ap.add_argument("--eval-every", type=int, default=500)
+    ap.add_argument("--reverse-lengths", default=None,
+                    help="c2 only: REVERSE payloads of random lengths LO:HI (the paper trains on 1:10) "
+                         "instead of the workload's fixed 64")
     args = ap.parse_args(argv)
     name = args.workload
     w, cfg, sd = wl.CONFIGS[name], wl.model_cfg(name), wl.seeds(name)
@@ -109,8 +112,18 @@ def main(argv=None):
     lr = w["lr"] if args.lr is None else args.lr
     dev = torch.device("cuda:0")
 
+    if args.reverse_lengths and name != "c2":
+        raise SystemExit("--reverse-lengths applies to the c2 workload only")
+
+    def host_batch(seed):
+        if not args.reverse_lengths:
+            return wl.batch(name, seed=seed)
+        lo, hi = (int(x) for x in args.reverse_lengths.split(":"))
+        rng = np.random.default_rng(sd["data"] if seed is None else seed)
+        return wl.reverse_task_varlen(rng, w["B"], w["C"], cfg["vocab"], lo, hi)
+
     def dev_batch(seed=None):
-        tok, mask = wl.batch(name, seed=seed)
+        tok, mask = host_batch(seed)
         return (torch.from_numpy(tok).to(dev), None if mask is None else torch.from_numpy(mask).to(dev))
 
     tokens, mask = dev_batch()
@@ -121,7 +134,8 @@ def main(argv=None):
     t0 = time.time()
 
     def report(step, window):
-        row = {"workload": name, "step": step, "eps": eps, "lr": lr, "estimator": args.estimator,
+        row = {"workload": name, "reverse_lengths": args.reverse_lengths, "step": step, "eps": eps, "lr": lr,
+               "estimator": args.estimator,
                "N": w["N"], "fresh_batches": args.fresh_batches,
                "window_estimate": None if window is None else float(np.mean(window)),
                "clean_loss_train_batch": clean_loss(cfg, theta, tokens, mask),

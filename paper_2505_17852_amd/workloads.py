@@ -93,6 +93,27 @@ def reverse_task(rng: np.random.Generator, B: int, C: int, V: int, payload: int 
     return toks, mask
 
 
+def reverse_task_varlen(rng: np.random.Generator, B: int, C: int, V: int, lmin: int = 1, lmax: int = 10):
+    """REVERSE rows with random payload lengths, as the paper trains its
+    transduction models (payloads of 1 to 10 random characters): each row is
+    a run of [payload, SEP, payload reversed] blocks, every payload of its
+    own length drawn uniformly from lmin..lmax and ids uniform over 0..V-2,
+    cut to C+1 tokens. mask[b][t] = 1 iff target t+1 lies in a reversed
+    part."""
+    toks = np.empty((B, C + 1), np.int32)
+    mask = np.zeros((B, C), np.uint8)
+    for b in range(B):
+        row, m = [], []
+        while len(row) < C + 1:
+            n = int(rng.integers(lmin, lmax + 1))
+            pay = rng.integers(0, V - 1, size=n).tolist()
+            row += pay + [V - 1] + pay[::-1]
+            m += [0] * (n + 1) + [1] * n
+        toks[b] = row[:C + 1]
+        mask[b] = np.array(m[1:C + 1], np.uint8)
+    return toks, mask
+
+
 def batch(name: str, B: int | None = None, C: int | None = None, seed: int | None = None):
     """(tokens [B][C+1] int32, mask [B][C] uint8 or None) for workload `name`."""
     c = CONFIGS[name]

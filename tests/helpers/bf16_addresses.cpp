@@ -1,0 +1,140 @@
+// Host replay of the bf16 kernels' operand addressing (zo_pack.hpp, the same
+// functions the kernels call): for one model shape and batch, every
+// workgroup, wave, lane, copy and k step of the gate and head launches, it
+// checks that each activation copy and each packed B-fragment load lies
+// inside the buffer resource it is issued against (and inside the tensor that
+// resource covers), that every offset fits in 32 bits, that the copies fill
+// each LDS row and slot of a tile exactly once with the chunk the swizzle
+// puts there, and that the packed layout and the gate column order are
+// bijections. Usage: bf16_addresses L V E H N B fd -> prints "ok" or the
+// first violation (exit status 1).
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#include "../../paper_2505_17852_amd/csrc/zo_pack.hpp"
+
+using namespace zo;
+
+static int fails = 0;
+#define CHECK(cond, ...)                                    \
+  do {                                                      \
+    if (!(cond)) {                                          \
+      if (fails++ < 10) {                                   \
+        std::printf("violation: " __VA_ARGS__);             \
+        std::printf("\n");                                  \
+      }                                                     \
+    }                                                       \
+  } while (0)
+
+constexpr int TM = 256, TN = 256, TK = 64, NWAVES = 8, ACOPIES = 4;
+
+// the activation copies of one workgroup tile against a resource of TM rows of lda
+static void check_copies(int64_t lda, int64_t K, const char* what) {
+  const uint64_t records = (uint64_t)TM * lda * 2;
+  CHECK(records < (1ull << 31), "%s: resource of %llu bytes", what, (unsigned long long)records);
+  std::vector<int> seen(TM * 8, 0);
+  for (int q = 0; q < ACOPIES; ++q)
+    for (int w = 0; w < NWAVES; ++w)
+      for (int lane = 0; lane < 64; ++lane) {
+        const int row = act_row_of_copy(q, w, lane, NWAVES);
+        CHECK(row >= 0 && row < TM, "%s: copy row %d", what, row);
+        const int lds = (q * NWAVES + w) * 1024 + 16 * lane;  // LDS byte this lane writes
+        CHECK(lds == row * 128 + 16 * (lane % 8), "%s: LDS byte %d for row %d", what, lds, row);
+        seen[row * 8 + lane % 8] += 1;
+        const uint64_t off0 = act_copy_offset(q, w, lane, NWAVES, lda);
+        const int chunk = (int)((off0 - (uint64_t)row * lda * 2) / 16);
+        CHECK(chunk == ((lane % 8) ^ act_swizzle(row)), "%s: chunk %d in slot %d of row %d", what, chunk,
+              lane % 8, row);
+        for (int64_t k0 : {(int64_t)0, K - TK}) {
+          const uint64_t off = off0 + 2 * (uint64_t)k0;
+          CHECK(off + 16 <= records && off < (1ull << 32), "%s: copy offset %llu of %llu (k0 %lld)", what,
+                (unsigned long long)off, (unsigned long long)records, (long long)k0);
+        }
+      }
+  for (int i = 0; i < TM * 8; ++i) CHECK(seen[i] == 1, "%s: LDS row %d slot %d written %d times", what, i / 8, i % 8, seen[i]);
+}
+
+// the packed B loads of column block nb (waves wn, tiles nt, every lane and k step)
+static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what) {
+  const uint64_t records = (uint64_t)cols * K * 2;
+  CHECK(records < (1ull << 31), "%s: packed matrix of %llu bytes", what, (unsigned long long)records);
+  const int64_t KS = K / kPackKStep;
+  for (int wn = 0; wn < 4; ++wn)
+    for (int nt = 0; nt < 2; ++nt)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int64_t ks : {(int64_t)0, KS - 1}) {
+          const int64_t cb = packed_block_of(nb, wn, nt);
+          const uint64_t off = packed_lane_offset(cb, K, lane) + packed_step_offset(ks);
+          CHECK(off + 16 <= records && off < (1ull << 32), "%s: B offset %llu of %llu", what,
+                (unsigned long long)off, (unsigned long long)records);
+          // the chunk read is the fragment piece of column 32 cb + lr at k 16 ks + 8 lg
+          const PackedChunk pc = packed_chunk(off / 16, K);
+          CHECK(pc.col == 32 * cb + (lane & 31) && pc.k == 16 * ks + 8 * (lane >> 5), "%s: packed chunk", what);
+        }
+}
+
+int main(int argc, char** argv) {
+  if (argc != 8) {
+    std::printf("usage: bf16_addresses L V E H N B fd\n");
+    return 2;
+  }
+  const int L = std::atoi(argv[1]);
+  const int64_t V = std::atoll(argv[2]), E = std::atoll(argv[3]), H = std::atoll(argv[4]);
+  const int64_t N = std::atoll(argv[5]), B = std::atoll(argv[6]);
+  const bool fd = std::atoi(argv[7]) != 0;
+  const int64_t gran = fd ? 256 : 128;
+  const int64_t Bp = (B + gran - 1) / gran * gran;
+  const int64_t M = fd ? (N + 1) * Bp : 2 * N * Bp;
+  const int64_t nvt = (V + TN - 1) / TN;
+  const int64_t out_rows = nvt * TN;
+  CHECK(M % TM == 0, "rows %lld not a whole number of tiles", (long long)M);
+  // the gate column order is a permutation of the 4H weight rows
+  {
+    std::vector<int> hit(4 * H, 0);
+    for (int64_t rho = 0; rho < 4 * H; ++rho) {
+      const int64_t r = gate_row_of_column(rho, H);
+      CHECK(r >= 0 && r < 4 * H, "gate column %lld -> row %lld", (long long)rho, (long long)r);
+      if (r >= 0 && r < 4 * H) hit[r]++;
+    }
+    for (int64_t r = 0; r < 4 * H; ++r) CHECK(hit[r] == 1, "gate row %lld hit %d times", (long long)r, hit[r]);
+  }
+  // the packed layout: chunk u <-> (column, k) is a bijection on one matrix
+  for (int64_t K : {E, H}) {
+    const int64_t cols = 4 * H;
+    std::vector<uint8_t> hit((size_t)(cols * K / 8), 0);
+    for (uint64_t u = 0; u < (uint64_t)(cols * K / 8); ++u) {
+      const PackedChunk pc = packed_chunk(u, K);
+      CHECK(pc.col >= 0 && pc.col < cols && pc.k >= 0 && pc.k + 8 <= K && pc.k % 8 == 0, "packed chunk %llu",
+            (unsigned long long)u);
+      if (pc.col >= 0 && pc.col < cols && pc.k >= 0 && pc.k + 8 <= K) hit[(size_t)(pc.col * (K / 8) + pc.k / 8)]++;
+    }
+    for (size_t i = 0; i < hit.size(); ++i) CHECK(hit[i] == 1, "packed (col, k) %zu hit %d times", i, hit[i]);
+  }
+  // gate launches: every layer's two segments, every workgroup
+  const int64_t nm = M / TM, nn = H / 64;
+  for (int l = 0; l < L; ++l) {
+    const int64_t El = l == 0 ? E : H;
+    check_copies(El, El, "gate x");
+    check_copies(H, H, "gate h");
+    for (int64_t mb = 0; mb < nm; ++mb) CHECK((mb + 1) * TM <= M, "gate row block %lld", (long long)mb);
+    for (int64_t nb = 0; nb < nn; ++nb) {
+      check_b_loads(nb, 4 * H, El, "gate W_ih");
+      check_b_loads(nb, 4 * H, H, "gate W_hh");
+    }
+  }
+  // head launches: Tc timesteps of M rows (Tc <= 16), every vocabulary tile
+  for (int64_t Tc : {(int64_t)1, (int64_t)16}) {
+    const int64_t rows = Tc * M;
+    CHECK(rows % TM == 0, "head rows");
+    check_copies(H, H, "head h");
+    for (int64_t vt = 0; vt < nvt; ++vt) check_b_loads(vt, out_rows, H, "head W_out");
+  }
+  if (fails) {
+    std::printf("%d violations\n", fails);
+    return 1;
+  }
+  std::printf("ok\n");
+  return 0;
+}

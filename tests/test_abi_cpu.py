@@ -72,14 +72,18 @@ def test_workspace_bytes(zo):
 def test_workspace_probe_cache_size(zo, name):
     """Normal probes: the preferred workspace adds exactly the probe cache,
     N values of the weight matrices' size in the weight type (rounded up to
-    the 256-byte allocation granule); sign probes cache nothing."""
+    the 256-byte allocation granule; with bf16 weights the head matrix is
+    stored padded to whole 256-wide vocabulary tiles); sign probes cache
+    nothing."""
     w = wl.CONFIGS[name]
     cfg = wl.model_cfg(name)
     full = zo.workspace_bytes(cfg, w["N"], w["B"], w["C"])
     small = zo.workspace_bytes_min(cfg, w["N"], w["B"], w["C"])
     if cfg["probe"] == wl.GAUSSIAN:
         L, E, H, V = cfg["n_layers"], cfg["embed"], cfg["hidden"], cfg["vocab"]
-        pg = sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + V * H
+        # bf16: the head matrix is stored padded to whole 256-wide vocabulary tiles
+        Vs = (V + 255) // 256 * 256 if cfg["wdtype"] == wl.BF16 else V
+        pg = sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + Vs * H
         el = 2 if cfg["wdtype"] == wl.BF16 else 4
         assert full - small == (w["N"] * pg * el + 255) // 256 * 256
     else:

@@ -106,3 +106,34 @@ def test_log_replay_reconstructs_theta(zo, wdtype, probe):
         zo.update(cfg, resumed, base + k, eps, lr, Lp, Lm)
     assert torch.equal(resumed.view(bits), theta.view(bits))
     assert not torch.equal(theta.view(bits), theta0.view(bits))
+
+
+def test_c2_reverse_training_lowers_held_out_loss(zo):
+    """The transduction shape (c2: 2 layers, V = 256, E = 128, H = 256; B = 64,
+    C = 256 REVERSE rows, loss on the reversed payloads; N = 32 sign probes) at
+    its full size, 1000 steps on fresh batches (step k draws data seed
+    1002 + 1 + k) with eps = lr = 0.1, the largest value the paper explores: the
+    clean loss on a held-out batch falls by more than 1e-3 nats (measured:
+    5.54614 -> 5.54455, and 5.54089 after 10,000 steps; the no-memory floor
+    ln 255 = 5.54126)."""
+    from paper_2505_17852_amd import train
+    name = "c2"
+    w = wl.CONFIGS[name]
+    cfg = wl.model_cfg(name)
+    sd = wl.seeds(name)
+
+    def dev_batch(seed):
+        tok, mask = wl.batch(name, seed=seed)
+        return torch.from_numpy(tok).cuda(), torch.from_numpy(mask).cuda()
+
+    held = dev_batch(sd["data"] + 10_000_000)
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, sd["init"])
+    before = train.clean_loss(cfg, theta, *held)
+    first = dev_batch(sd["data"] + 1)
+    hist = train.train(cfg, theta, first[0], first[1], N=w["N"], eps=0.1, lr=0.1, steps=1000, seed0=sd["step"],
+                       batches=lambda k: dev_batch(sd["data"] + 1 + k)).numpy()
+    after = train.clean_loss(cfg, theta, *held)
+    say(f"held-out clean loss {before:.6f} -> {after:.6f}; estimate {hist[:3]} .. {hist[-3:]}")
+    assert np.all(np.isfinite(hist))
+    assert after < before - 1e-3
