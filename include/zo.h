@@ -16,7 +16,8 @@
  * workspace, out) is a device pointer on the current HIP device, allocated
  * and owned by the caller. The library never allocates, frees or retains
  * caller memory. It keeps no state between calls apart from the optional
- * kernel-timing records (zo_profile_enable).
+ * kernel-timing records (zo_profile_enable) and, for zo_perturbed_losses_noalloc,
+ * one fixed scratch array per device.
  *
  * Streams. `stream` is a hipStream_t (NULL = the default stream). Every call
  * only enqueues work on that stream and returns; outputs are valid once the
@@ -178,6 +179,24 @@ int zo_perturbed_losses_ex(const zo_config* cfg, const void* theta, uint64_t see
                            int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
                            int32_t B, int32_t C, float* Lplus, float* Lminus, void* workspace,
                            size_t ws_bytes, int32_t products, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * zo_perturbed_losses without a workspace argument. The workspace is a fixed
+ * device array of ZO_NOALLOC_WORKSPACE_BYTES inside the library, one per
+ * device, held from the first call on that device until the process ends
+ * (the probe cache is used when zo_workspace_bytes() fits in it as well).
+ * The call allocates and frees nothing, and does no kernel timing. A shape
+ * whose zo_workspace_bytes_min() exceeds the array returns ZO_ENOMEM before
+ * anything is enqueued. Every call on a device shares that device's array:
+ * calls that overlap on one device (concurrent streams or threads) race and
+ * must be serialised by the caller. Each call clears what it reads before
+ * writing it, so no state carries from one call to the next. Other arguments,
+ * results and return codes as for zo_perturbed_losses. */
+#define ZO_NOALLOC_WORKSPACE_BYTES (128u << 20)
+int zo_perturbed_losses_noalloc(const zo_config* cfg, const void* theta, uint64_t seed, float eps,
+                                int32_t N, uint32_t i0, const int32_t* tokens, const uint8_t* mask,
+                                int32_t B, int32_t C, float* Lplus, float* Lminus, void* stream);
 
 /* The update of Eq. 7 in its general form (Algorithm 1's closing loop):
  *   c_n = fp32( (lr / N) * (L+_n - L-_n) / (2 eps) )  (computed in double)

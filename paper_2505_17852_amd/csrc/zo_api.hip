@@ -7,10 +7,12 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/zo.h"
 #include "zo_common.hpp"
 #include "zo_kernels.hpp"
+#include "zo_profile.hpp"
 
 namespace {
 
@@ -47,6 +49,35 @@ int check_config(const zo_config* c) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Workspace of zo_perturbed_losses_noalloc: a fixed device array, one copy per
+// device, held until the process ends. In host code `scratch` names a host
+// stand-in; its device address on the current device comes from
+// hipGetSymbolAddress, once per device, and only that address is ever used.
+constexpr size_t kScratchBytes = (size_t)ZO_NOALLOC_WORKSPACE_BYTES;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (looked up on the first call on that
+// device, with the device current).
+int scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(ZO_EDEVICE, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return device_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(ZO_EDEVICE, "no device address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ZO_OK;
+}
 
 }  // namespace
 
@@ -153,6 +184,31 @@ int zo_perturbed_losses_ex(const zo_config* cfg, const void* theta, uint64_t see
                            void* stream) {
   return forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, Lplus, Lminus, workspace, ws_bytes,
                       products, stream, false, "zo_perturbed_losses_ex");
+}
+
+int zo_perturbed_losses_noalloc(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N,
+                                uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
+                                float* Lplus, float* Lminus, void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (N < 1 || B < 1 || C < 1) return fail(ZO_EINVAL, "N, B and C must be >= 1");
+  // the sizes are checked before the scratch array is first touched
+  const size_t need = zo_workspace_bytes_min(cfg, N, B, C);
+  if (need == 0) return fail(ZO_EINVAL, "invalid workspace request");
+  if (need > kScratchBytes)
+    return fail(ZO_ENOMEM, "zo_perturbed_losses_noalloc: %zu bytes of workspace needed, the fixed scratch holds %zu",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st) return st;
+  // the probe cache too when it fits (the results are the same either way)
+  const size_t full = zo_workspace_bytes(cfg, N, B, C);
+  const size_t bytes = full <= kScratchBytes ? full : need;
+  zo::g_profile_suppressed = true;
+  st = forward_call(cfg, theta, seed, eps, N, i0, tokens, mask, B, C, Lplus, Lminus, ws, bytes, ZO_PRODUCTS_AUTO,
+                    stream, false, "zo_perturbed_losses_noalloc");
+  zo::g_profile_suppressed = false;
+  return st;
 }
 
 int zo_fd_losses(const zo_config* cfg, const void* theta, uint64_t seed, float eps, int32_t N, uint32_t i0,

@@ -9,6 +9,7 @@
 namespace zo {
 
 std::atomic<int> g_profile_on{0};
+thread_local bool g_profile_suppressed = false;
 
 namespace {
 struct Slot {

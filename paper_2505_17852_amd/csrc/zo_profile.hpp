@@ -13,6 +13,9 @@ enum KernelClass { kKGate = 0, kKHead = 1, kKEmbed = 2, kKCombine = 3, kKUpdate 
                    kKWeights16 = 6, kKClasses = 7 };
 
 extern std::atomic<int> g_profile_on;  // 0: off; n >= 1: time every n-th launch of a class
+// Set by entry points that must not allocate (timing creates HIP events on
+// first use): their launches are neither counted nor timed.
+extern thread_local bool g_profile_suppressed;
 
 // Counts the launch; returns a slot index to pass to prof_end when this launch
 // is timed, else -1.
@@ -23,7 +26,8 @@ struct ProfScope {
   int slot;
   hipStream_t s;
   ProfScope(KernelClass k, hipStream_t st)
-      : slot(g_profile_on.load(std::memory_order_relaxed) ? prof_begin(k, st) : -1), s(st) {}
+      : slot(g_profile_on.load(std::memory_order_relaxed) && !g_profile_suppressed ? prof_begin(k, st) : -1),
+        s(st) {}
   ~ProfScope() {
     if (slot >= 0) prof_end(slot, s);
   }

@@ -71,6 +71,8 @@ def lib():
         L.zo_perturbed_losses_ex.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
                                              vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t,
                                              C.c_int32, vp]
+        L.zo_perturbed_losses_noalloc.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
+                                                  vp, vp, C.c_int32, C.c_int32, vp, vp, vp]
         L.zo_fd_losses_ex.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
                                       vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, C.c_int32, vp]
         L.zo_fd_update.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
@@ -82,7 +84,7 @@ def lib():
                                       C.POINTER(C.c_int64)]
         L.zo_last_error.restype = C.c_char_p
         for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_fd_losses", "zo_fd_update",
-                  "zo_perturbed_losses_ex", "zo_fd_losses_ex",
+                  "zo_perturbed_losses_ex", "zo_fd_losses_ex", "zo_perturbed_losses_noalloc",
                   "zo_debug_probe",
                   "zo_debug_gauss_pairs", "zo_profile_enable", "zo_profile_read"):
             getattr(L, f).restype = C.c_int
@@ -202,6 +204,33 @@ def perturbed_losses(cfg, theta: torch.Tensor, seed: int, eps: float, N: int,
         st = lib().zo_perturbed_losses(*args, _stream(stream))
     else:
         st = lib().zo_perturbed_losses_ex(*args, int(products), _stream(stream))
+    _check(st)
+    return Lplus, Lminus
+
+
+NOALLOC_WORKSPACE_BYTES = 128 << 20  # ZO_NOALLOC_WORKSPACE_BYTES
+
+
+def perturbed_losses_noalloc(cfg, theta: torch.Tensor, seed: int, eps: float, N: int,
+                             tokens: torch.Tensor, mask: torch.Tensor | None, Lplus: torch.Tensor,
+                             Lminus: torch.Tensor, i0: int = 0, stream=None):
+    """zo_perturbed_losses_noalloc: the perturbed losses into the caller's
+    Lplus / Lminus (device fp32, >= N elements) with the library's fixed
+    device scratch as the workspace (nothing is allocated, here or in the
+    library; token ids are not checked on the host)."""
+    c = _cfg(cfg)
+    if tokens.dim() != 2:
+        raise ValueError("tokens must be [B][C+1]")
+    B, C1 = tokens.shape
+    Cn = C1 - 1
+    if mask is not None and tuple(mask.shape) != (B, Cn):
+        raise ValueError("mask must be [B][C]")
+    if Lplus.numel() < N or Lminus.numel() < N:
+        raise ValueError("loss buffers smaller than N")
+    st = lib().zo_perturbed_losses_noalloc(
+        C.byref(c), _theta(cfg, theta), seed, eps, N, i0, _dev(tokens, torch.int32, "tokens"),
+        None if mask is None else _dev(mask, torch.uint8, "mask"), B, Cn,
+        _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"), _stream(stream))
     _check(st)
     return Lplus, Lminus
 

@@ -184,6 +184,28 @@ def test_products_and_eps_floor_errors(zo):
     assert zo.BF16_EPS_MIN == 2.0 ** -17 and zo.BF16_FUSED_EPS_MIN == 2.0 ** -10
 
 
+def test_noalloc_size_check_on_the_host(zo):
+    """zo_perturbed_losses_noalloc rejects a shape whose workspace exceeds its
+    fixed scratch (ZO_ENOMEM) and bad sizes (ZO_EINVAL) before any device
+    work; the c1 and c2 workloads fit the scratch, the billion-parameter ones
+    do not."""
+    L = zo.lib()
+    fake = C.c_void_p(0x10000)
+    for name in ("c1", "c2"):
+        w = wl.CONFIGS[name]
+        assert zo.workspace_bytes_min(wl.model_cfg(name), w["N"], w["B"], w["C"]) <= zo.NOALLOC_WORKSPACE_BYTES
+    for name in ("c3", "c4", "c5"):
+        w = wl.CONFIGS[name]
+        c = zo._cfg(wl.model_cfg(name))
+        assert zo.workspace_bytes_min(wl.model_cfg(name), w["N"], w["B"], w["C"]) > zo.NOALLOC_WORKSPACE_BYTES
+        assert L.zo_perturbed_losses_noalloc(C.byref(c), fake, 1, 1e-3, w["N"], 0, fake, None, w["B"], w["C"],
+                                             fake, fake, None) == zo.ZO_ENOMEM
+        assert "scratch" in L.zo_last_error().decode()
+    c = zo._cfg(wl.model_cfg("c1"))
+    assert L.zo_perturbed_losses_noalloc(C.byref(c), fake, 1, 1e-3, 0, 0, fake, None, 4, 32, fake, fake,
+                                         None) == zo.ZO_EINVAL
+
+
 def test_header_is_c_and_the_library_links_from_c(zo, tmp_path):
     """include/zo.h compiles as C11, and a C program linked against the
     library calls its host-only entry points (sizes and argument checks; no
