@@ -123,7 +123,8 @@ size_t zo_param_count(const zo_config* cfg);
  * eps z (fp32 weights) or fp16(eps z) (bf16 weights) for the same matrices,
  * written once per call and read by every timestep instead of regenerating
  * the probe in every tile (the results are bit-identical either way). With
- * sign probes it equals zo_workspace_bytes_min. */
+ * sign probes and bf16 weights it includes the sign-probe cache (below); with
+ * sign probes and fp32 weights it equals zo_workspace_bytes_min. */
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
 
 /* The smallest workspace zo_perturbed_losses accepts: without the probe
@@ -211,6 +212,29 @@ int zo_perturbed_losses_noalloc(const zo_config* cfg, const void* theta, uint64_
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
               uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
               void* stream);
+
+/* Sign-probe cache (bf16 weights with sign probes; the paper notes that sign
+ * probes can be stored as bits). A workspace of at least zo_workspace_bytes()
+ * holds, at byte offset zo_probe_bits_offset(cfg, N, B, C), the sign words of
+ * the call's probes i0 .. i0+N-1 over the whole of theta: probe n's word w at
+ * n * 4 * ceil(P / 128) + w (uint32), bit b of word w set when
+ * z_{i0+n}[32 w + b] = +1. zo_perturbed_losses writes it once per call and its
+ * kernels read the words from it instead of regenerating them (the losses are
+ * bit-identical either way); a smaller workspace regenerates them.
+ * zo_probe_bits_offset returns 0 for shapes without the cache or invalid
+ * arguments. Host only. */
+size_t zo_probe_bits_offset(const zo_config* cfg, int32_t N, int32_t B, int32_t C);
+
+/* zo_update reading the probes' sign words from a sign-probe cache
+ * (probe_bits: device, 16-byte aligned, the words of probes i0 .. i0+N-1 as
+ * written by the zo_perturbed_losses call of the same seed, i0 and N, at its
+ * workspace's zo_probe_bits_offset) instead of regenerating them. theta comes
+ * out bit-identical to zo_update's. Sign probes only (ZO_EINVAL otherwise);
+ * other arguments and return codes as for zo_update. For measuring the
+ * update's cost in memory traffic against regeneration. */
+int zo_update_cached(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                     uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
+                     const uint32_t* probe_bits, void* stream);
 
 /* Forward differences (Eq. 1's one-sided difference; the paper's FD-RGE,
  * compared with CD-RGE in its appendix): N + 1 passes instead of 2N.

@@ -952,6 +952,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   // probes, when the workspace holds it)
   if (bf16) ZO_TRY(launch_w16_fill(a, st));
   if (a.zc) ZO_TRY(launch_zcache_fill(a, st));
+  if (a.bits) ZO_TRY(launch_bits_fill(a.bits, a.lay.total, a.seed, a.i0, R.N, st));
 
   // bias probes
   {

@@ -64,7 +64,8 @@ constexpr int NT = 64 * NWAVES;  // threads per workgroup
 // Per probe kind: K tile, LDS layout, copy roles, B-operand prefetch depth.
 template <int kind>
 struct Tiles {
-  static constexpr bool kSigns = kind == ZO_RADEMACHER;
+  static constexpr bool kSigns = kind == ZO_RADEMACHER || kind == kSignsCached;
+  static constexpr bool kBits = kind == kSignsCached;      // sign words read from the sign-probe cache
   static constexpr bool kZDirect = kind == kGaussCached;  // probe fragments loaded like the weights
   static constexpr bool kZTile = !kZDirect;               // probe tile formed in LDS (signs or normals)
   static constexpr int TK = 64;                            // K per tile
@@ -86,6 +87,7 @@ struct Tiles {
   static constexpr int DIST = kZDirect ? 1 : 3;
   static constexpr int SLOTS = DIST + 1;
   static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
+  static constexpr int WordLoads = kBits ? 1 : 0;  // sign-word loads per tile (one tile ahead)
   // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
   static constexpr int ZROW_T = NT / TN;
   static constexpr int ZVALS = TK / ZROW_T;
@@ -106,6 +108,7 @@ __shared__ __align__(16) uint8_t lds_s1[Tiles<ZO_RADEMACHER>::StageBytes];
 __shared__ __align__(16) uint8_t lds_c0[Tiles<kGaussCached>::StageBytes];
 __shared__ __align__(16) uint8_t lds_c1[Tiles<kGaussCached>::StageBytes];
 static_assert(Tiles<ZO_GAUSSIAN>::StageBytes == Tiles<ZO_RADEMACHER>::StageBytes, "probe-tile stages");
+static_assert(Tiles<kSignsCached>::StageBytes == Tiles<ZO_RADEMACHER>::StageBytes, "probe-tile stages");
 static_assert(2 * sizeof(lds_s0) <= 160 * 1024, "LDS");
 
 template <int kind, int S>
@@ -188,6 +191,13 @@ struct SegB {
   const uint16_t* Z;  // kGaussCached: fp16(eps z) of this probe and matrix, packed like W
 };
 
+// The sign-probe cache of this workgroup's probe (kSignsCached): bit_words(P)
+// words, word w holding the signs of parameters 32 w .. 32 w + 31.
+struct BitsB {
+  const uint32_t* words;
+  uint32_t bytes;
+};
+
 // acc: [MT row tiles][2 column tiles] of 32x32 fp32 for this wave. cb0: the
 // packed column block of the workgroup's first column (8 per 256 columns).
 // colmap(rho, &n) maps workgroup column rho (0..TN-1) to the weight row n in
@@ -208,7 +218,7 @@ struct SegB {
 template <int kind, bool kTrans = false, bool kSplit = false, typename ColMap>
 __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], const SegB s0, const SegB s1,
                                               int nseg, int64_t cb0, ColMap colmap, Key key, uint32_t probe,
-                                              int sgn, float eps, uint16_t eps_b) {
+                                              int sgn, float eps, uint16_t eps_b, const BitsB bits) {
   using T = Tiles<kind>;
   constexpr int MT = T::MT;
   constexpr int TK = T::TK;
@@ -277,6 +287,32 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
 
   Words zcache{{0u, 0u, 0u, 0u}};
   int seg = 0, k0 = 0;  // the next tile to be copied (stays on the last tile once past it)
+  // advance (seg, k0) by one K tile, staying on the last tile once past it
+  auto next_tile = [&](int& sg_, int& k_) {
+    const int K = sg_ == 0 ? s0.K : s1.K;
+    k_ += TK;
+    if (k_ == K) {
+      if (sg_ + 1 < nseg) {
+        k_ = 0;
+        ++sg_;
+      } else {
+        k_ -= TK;
+      }
+    }
+  };
+  // cached sign words: the word of this thread's 32 k of a tile, loaded one
+  // tile before issue_probe needs it (wseg, wk0: the next tile to load)
+  Rsrc rbits = rw0;
+  if constexpr (T::kBits) rbits = make_rsrc(bits.words, bits.bytes);
+  int wseg = 0, wk0 = 0;
+  uint32_t wcur = 0u, wnext = 0u;
+  auto load_word = [&]() {
+    const SegB& sg = wseg == 0 ? s0 : s1;
+    const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)wk0 + T::ZVALS * zpart;
+    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rbits, (uint32_t)(j0 >> 5) * 4u, 0, 0);
+    next_tile(wseg, wk0);
+    return w;
+  };
 
   // The next K tile's activation copies into stage S (issued first in a tile,
   // so that the loads after them are the B loads of this tile: the count
@@ -304,7 +340,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     if constexpr (T::kSigns) {
       uint32_t word;
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
-      if (aligned) {
+      if constexpr (T::kBits) {
+        word = wcur;
+        wcur = wnext;
+      } else if (aligned) {
         if ((k0 & 127) == 0) zcache = stream_block(key, j0 >> 7, probe, kTagRademacher);
         const int q = (int)((j0 >> 5) & 3u);
         word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
@@ -333,15 +372,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
                pack_f16x2(eps * zb[0], eps * zb[1]), pack_f16x2(eps * zb[2], eps * zb[3])};
       }
     }
-    k0 += TK;
-    if (k0 == sg.K) {
-      if (seg + 1 < nseg) {
-        k0 = 0;
-        ++seg;
-      } else {
-        k0 -= TK;
-      }
-    }
+    next_tile(seg, k0);
   };
 
   // Fragments of one 16-k step: activations (MT row tiles) and probe values
@@ -380,9 +411,11 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     for (int s = 0; s < KSTEPS; ++s) {
       const Frag& c = f[s & 1];
       if (s == 0) {
-        // the next tile's activation copies first, then this step's B loads
+        // the next tile's activation copies first, then the sign word two
+        // tiles ahead and this step's B loads
         issue_copies(next);
         issue_fence();
+        if constexpr (T::kBits) wnext = load_word();
       }
       // B fragments DIST steps ahead
       switch ((s + T::DIST) % T::SLOTS) {
@@ -440,14 +473,19 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // steps' B loads.
   issue_copies(std::integral_constant<int, 0>{});
   issue_fence();
+  if constexpr (T::kBits) {
+    wcur = load_word();   // tile 0, used by the prologue's issue_probe
+    wnext = load_word();  // tile 1
+  }
   if constexpr (T::DIST >= 1) load_b(std::integral_constant<int, 0>{}, 0);
   if constexpr (T::DIST >= 2) load_b(std::integral_constant<int, 1>{}, 1);
   if constexpr (T::DIST >= 3) load_b(std::integral_constant<int, 2>{}, 2);
   issue_probe(std::integral_constant<int, 0>{});
   // loads issued after the copies of the tile a barrier waits for: the first
-  // DIST steps' B loads (prologue), then a whole tile's (every later tile)
-  constexpr int kAfter0 = T::DIST * T::LoadsPerStep;
-  constexpr int kAfter = KSTEPS * T::LoadsPerStep;
+  // DIST steps' B loads and two sign words (prologue), then a whole tile's B
+  // loads and one sign word (every later tile)
+  constexpr int kAfter0 = T::DIST * T::LoadsPerStep + 2 * T::WordLoads;
+  constexpr int kAfter = KSTEPS * T::LoadsPerStep + T::WordLoads;
   wait_and_barrier<kAfter0>();
   int it = 0;
   for (; it + 1 < ntiles; it += 2) {
@@ -519,6 +557,8 @@ struct GateArgsB {
   uint64_t zc_stride;
   const uint16_t* w_ih16;  // fp16 copies of W_ih and W_hh
   const uint16_t* w_hh16;
+  const uint32_t* bits;    // sign-probe cache (kSignsCached): probe 0's words; probe n at + n * bits_stride
+  uint64_t bits_stride;
 };
 
 // Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
@@ -549,8 +589,10 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
                 kind == kGaussCached ? g.zc_ih + zpos : nullptr};
   const SegB s1{g.hprev + m0 * H, H, g.w_hh16, (uint32_t)((uint64_t)4 * H * H * 2), g.off_hh, H, H,
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
+  const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
+                   (uint32_t)(g.bits_stride * 4)};
   mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, 8 * (int64_t)nb, colmap, g.key, g.i0 + (uint32_t)pair,
-                                          sgn, g.eps, g.eps_b);
+                                     sgn, g.eps, g.eps_b, bits);
 
   const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
   const int u = u0 + 16 * wn + (lr & 15);
@@ -608,6 +650,8 @@ struct HeadArgsB {
   const uint16_t* zc_out;  // probe cache: W_out's values of probe 0; probe n at + n * zc_stride
   uint64_t zc_stride;
   const uint16_t* w_out16;  // fp16 copy of W_out
+  const uint32_t* bits;     // sign-probe cache (kSignsCached), as in GateArgsB
+  uint64_t bits_stride;
 };
 
 template <int kind, bool kFD, bool kSplit>
@@ -630,8 +674,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   zero_acc(acc);
   const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, (uint32_t)((uint64_t)g.nvt * T::TN * g.H * 2), g.off_w, g.H, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
+  const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
+                   (uint32_t)(g.bits_stride * 4)};
   mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, 8 * (int64_t)vt, colmap, g.key, g.i0 + (uint32_t)pair,
-                                         sgn, g.eps, g.eps_b);
+                                    sgn, g.eps, g.eps_b, bits);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
@@ -801,7 +847,8 @@ void dispatch_bf16(const ForwardArgs& a, Go&& go) {
     if (a.rows.fd) by_split(kind_tag, integral_constant<bool, true>{});
     else by_split(kind_tag, integral_constant<bool, false>{});
   };
-  if (a.cfg.probe == ZO_RADEMACHER) by_fd(integral_constant<int, ZO_RADEMACHER>{});
+  if (a.cfg.probe == ZO_RADEMACHER && a.bits) by_fd(integral_constant<int, kSignsCached>{});
+  else if (a.cfg.probe == ZO_RADEMACHER) by_fd(integral_constant<int, ZO_RADEMACHER>{});
   else if (a.zc) by_fd(integral_constant<int, kGaussCached>{});
   else by_fd(integral_constant<int, ZO_GAUSSIAN>{});
 }
@@ -855,6 +902,8 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
   g.zc_ih = a.zc ? (const uint16_t*)a.zc + a.zmap.ih[l] : nullptr;
   g.zc_hh = a.zc ? (const uint16_t*)a.zc + a.zmap.hh[l] : nullptr;
   g.zc_stride = a.zmap.pg;
+  g.bits = a.bits;
+  g.bits_stride = bit_words(a.lay.total);
   auto go = [&](auto kind_tag, auto fd_tag, auto split_tag) {
     constexpr int kind = decltype(kind_tag)::value;
     constexpr bool fd = decltype(fd_tag)::value;
@@ -896,6 +945,8 @@ hipError_t launch_head_bf16(const ForwardArgs& a, const void* hist, int t0, int 
   h.nvt = a.ws.nvt;
   h.zc_out = a.zc ? (const uint16_t*)a.zc + a.zmap.out : nullptr;
   h.zc_stride = a.zmap.pg;
+  h.bits = a.bits;
+  h.bits_stride = bit_words(a.lay.total);
   const dim3 grid((unsigned)((int64_t)a.ws.nvt * (h.rows / TM)));
   auto go = [&](auto kind_tag, auto fd_tag, auto split_tag) {
     constexpr int kind = decltype(kind_tag)::value;

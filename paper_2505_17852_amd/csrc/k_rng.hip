@@ -1,6 +1,8 @@
 // Probe dump, initialisation and the parameter update of the CD-RGE step.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "zo_kernels.hpp"
 #include "zo_profile.hpp"
 #include "zo_rng.hpp"
@@ -202,6 +204,15 @@ __device__ __forceinline__ void decode_raw8(const Raw8<T>& r, float v[8]) {
   }
 }
 
+// The 4 sign words of Philox block blk of probe n from the sign-probe cache
+// (layout: bit_words); zeros past the parameters, as their signs only ever
+// meet parameters that are not stored.
+__device__ __forceinline__ Words cached_block(const uint32_t* bits, uint64_t P, int n, uint64_t blk) {
+  if (blk >= (P + 127) / 128) return Words{{0u, 0u, 0u, 0u}};
+  const uint4 v = *(const uint4*)(bits + (uint64_t)n * bit_words(P) + 4 * blk);
+  return Words{{v.x, v.y, v.z, v.w}};
+}
+
 // Workgroup barrier for LDS data only: waits for this thread's LDS accesses
 // (lgkmcnt(0)), not for its global loads, which stay in flight across it.
 // The empty asm statements keep the compiler from moving memory accesses
@@ -213,13 +224,14 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <typename T>
+template <typename T, bool kBits>
 __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ theta, uint64_t P, Key key,
                                                                 float eps, float lr, int N, uint32_t i0,
                                                                 const float* __restrict__ Lp,
                                                                 const float* __restrict__ Lm,
                                                                 int32_t* __restrict__ skipped,
-                                                                uint64_t nchunks, int lm_stride) {
+                                                                uint64_t nchunks, int lm_stride,
+                                                                const uint32_t* __restrict__ bits) {
   // sign words laid out [word][probe] (rows padded by 4 words) so that one
   // thread reads 8 probes' words of its parameters with two 128-bit loads
   constexpr int kRow = kUpdGroup + 4;
@@ -316,7 +328,8 @@ __global__ __launch_bounds__(256) void update_rademacher_kernel(T* __restrict__ 
       // Philox blocks: cnt probes x 64 blocks (probes past cnt only ever meet zero coefficients)
       for (int q = t; q < cnt * (kUpdWords / 4); q += 256) {
         const int pn = q / (kUpdWords / 4), pb = q % (kUpdWords / 4);
-        const Words x = stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
+        const Words x = kBits ? cached_block(bits, P, n0 + pn, (base >> 7) + pb)
+                              : stream_block(key, (base >> 7) + pb, i0 + (uint32_t)(n0 + pn), kTagRademacher);
 #pragma unroll
         for (int w = 0; w < 4; ++w) words[(4 * pb + w) * kRow + pn] = x.w[w];
       }
@@ -430,11 +443,11 @@ __device__ __forceinline__ void wave_lds_sync() {
   asm volatile("" ::: "memory");
 }
 
-template <typename T>
+template <typename T, bool kBits>
 __global__ __launch_bounds__(kR16Threads) void update_rad16_kernel(
     T* __restrict__ theta, uint64_t P, Key key, float eps, float lr, int N, uint32_t i0,
     const float* __restrict__ Lp, const float* __restrict__ Lm, int32_t* __restrict__ skipped,
-    int lm_stride) {
+    int lm_stride, const uint32_t* __restrict__ bits) {
   // tables (64 KiB) first, so that a lookup address fits a 16-bit LDS offset;
   // then the rows (16 KiB), which also hold the coefficients and the 4-probe
   // partial sums while the tables are built
@@ -516,7 +529,7 @@ __global__ __launch_bounds__(kR16Threads) void update_rad16_kernel(
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
         const int p = 8 * g + 2 * w + m;  // zeros past N: their coefficients are 0
-        if (p < N) x[m] = stream_block(key, blk, i0 + (uint32_t)p, kTagRademacher);
+        if (p < N) x[m] = kBits ? cached_block(bits, P, p, blk) : stream_block(key, blk, i0 + (uint32_t)p, kTagRademacher);
         else x[m] = Words{{0u, 0u, 0u, 0u}};
       }
       // word v of these two probes goes to the row of lane (b, v, g), at 2 w
@@ -620,7 +633,33 @@ __global__ __launch_bounds__(256) void update_gaussian_kernel(T* theta, uint64_t
   store4(theta, j, P, out);
 }
 
+template <typename T>
+struct TypeTag {
+  using type = T;
+};
+
+// The sign-probe cache: probe n's Philox blocks (tag 0), 4 words each, at
+// n * bit_words(P) + 4 blk. One thread per block and probe.
+__global__ __launch_bounds__(256) void bits_fill_kernel(uint32_t* bits, uint64_t P, Key key, uint32_t i0, int N) {
+  const uint64_t nblk = (P + 127) / 128;
+  for (int n = blockIdx.y; n < N; n += gridDim.y)
+    for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nblk; b += (uint64_t)gridDim.x * blockDim.x) {
+      const Words x = stream_block(key, b, i0 + (uint32_t)n, kTagRademacher);
+      *(uint4*)(bits + (uint64_t)n * bit_words(P) + 4 * b) = uint4{x.w[0], x.w[1], x.w[2], x.w[3]};
+    }
+}
+
 }  // namespace
+
+hipError_t launch_bits_fill(uint32_t* bits, uint64_t P, uint64_t seed, uint32_t i0, int32_t N, hipStream_t s) {
+  const uint64_t nblk = (P + 127) / 128;
+  uint64_t gx = (nblk + 255) / 256;
+  if (gx > 8192) gx = 8192;
+  const unsigned gy = (unsigned)(N < 65535 ? N : 65535);
+  ProfScope ps(kKProbeCache, s);
+  bits_fill_kernel<<<dim3((unsigned)gx, gy), dim3(256), 0, s>>>(bits, P, make_key(seed), i0, N);
+  return hipGetLastError();
+}
 
 hipError_t launch_debug_probe(int kind, uint64_t seed, uint32_t i, uint64_t j0, uint64_t n,
                               float* out, hipStream_t s) {
@@ -650,7 +689,7 @@ hipError_t launch_init(int wdtype, void* theta, uint64_t P, uint64_t seed, float
 
 hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t seed, float eps,
                          float lr, int32_t N, uint32_t i0, const float* Lp, const float* Lm,
-                         int32_t* skipped, hipStream_t s, int lm_stride) {
+                         int32_t* skipped, hipStream_t s, int lm_stride, const uint32_t* bits) {
   const Key key = make_key(seed);
   ProfScope ps(kKUpdate, s);
   if (kind == ZO_RADEMACHER && N <= kUpdGroup) {
@@ -662,12 +701,19 @@ hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t
     if (e != hipSuccess) return e;
     const uint64_t slots = (uint64_t)(cus > 0 ? cus : 1) * kR16PerCu;
     const unsigned grid = (unsigned)(tiles < slots ? tiles : slots);
+    auto go = [&](auto t_tag, auto b_tag) {
+      using T = typename decltype(t_tag)::type;
+      constexpr bool kB = decltype(b_tag)::value;
+      update_rad16_kernel<T, kB><<<dim3(grid), dim3(kR16Threads), 0, s>>>((T*)theta, P, key, eps, lr, N, i0, Lp,
+                                                                        Lm, skipped, lm_stride, bits);
+    };
+    using std::integral_constant;
     if (wdtype == ZO_WBF16)
-      update_rad16_kernel<uint16_t><<<dim3(grid), dim3(kR16Threads), 0, s>>>(
-          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
+      bits ? go(TypeTag<uint16_t>{}, integral_constant<bool, true>{})
+           : go(TypeTag<uint16_t>{}, integral_constant<bool, false>{});
     else
-      update_rad16_kernel<float><<<dim3(grid), dim3(kR16Threads), 0, s>>>(
-          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, lm_stride);
+      bits ? go(TypeTag<float>{}, integral_constant<bool, true>{})
+           : go(TypeTag<float>{}, integral_constant<bool, false>{});
   } else if (kind == ZO_RADEMACHER) {
     // persistent workgroups: as many as fit on the device at once, each
     // walking chunks of kUpdChunk parameters
@@ -677,17 +723,24 @@ hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e == hipSuccess)
       e = wdtype == ZO_WBF16
-              ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<uint16_t>, 256, 0)
-              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<float>, 256, 0);
+              ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<uint16_t, false>, 256, 0)
+              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, update_rademacher_kernel<float, false>, 256, 0);
     if (e != hipSuccess) return e;
     const uint64_t slots = (uint64_t)(cus > 0 ? cus : 1) * (uint64_t)(per_cu > 0 ? per_cu : 1);
     const unsigned grid = (unsigned)(nchunks < slots ? nchunks : slots);
+    auto go = [&](auto t_tag, auto b_tag) {
+      using T = typename decltype(t_tag)::type;
+      constexpr bool kB = decltype(b_tag)::value;
+      update_rademacher_kernel<T, kB><<<dim3(grid), dim3(256), 0, s>>>((T*)theta, P, key, eps, lr, N, i0, Lp, Lm,
+                                                                     skipped, nchunks, lm_stride, bits);
+    };
+    using std::integral_constant;
     if (wdtype == ZO_WBF16)
-      update_rademacher_kernel<uint16_t><<<dim3(grid), dim3(256), 0, s>>>(
-          (uint16_t*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks, lm_stride);
+      bits ? go(TypeTag<uint16_t>{}, integral_constant<bool, true>{})
+           : go(TypeTag<uint16_t>{}, integral_constant<bool, false>{});
     else
-      update_rademacher_kernel<float><<<dim3(grid), dim3(256), 0, s>>>(
-          (float*)theta, P, key, eps, lr, N, i0, Lp, Lm, skipped, nchunks, lm_stride);
+      bits ? go(TypeTag<float>{}, integral_constant<bool, true>{})
+           : go(TypeTag<float>{}, integral_constant<bool, false>{});
   } else {
     const uint64_t grid = ((P + 3) / 4 + 255) / 256;
     if (wdtype == ZO_WBF16)

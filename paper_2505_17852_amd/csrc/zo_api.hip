@@ -166,6 +166,7 @@ static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, 
     a.split = products == ZO_PRODUCTS_SPLIT;
   // the probe cache is used when the workspace has room for it
   a.zc = (zo::probe_cache_kind(*cfg) && ws_bytes >= plan.total) ? (char*)workspace + plan.zcache : nullptr;
+  a.bits = (zo::bit_cache_kind(*cfg) && ws_bytes >= plan.total) ? (uint32_t*)((char*)workspace + plan.bits) : nullptr;
   a.zmap = zo::make_zcache_map(*cfg);
   a.w16 = cfg->wdtype == ZO_WBF16 ? (char*)workspace + plan.w16 : nullptr;
   return device_status(zo::launch_forward(a, (hipStream_t)stream), name);
@@ -241,6 +242,31 @@ int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float
   return device_status(zo::launch_update(cfg->wdtype, cfg->probe, theta, P, seed, eps, lr, N, i0,
                                          Lplus, Lminus, skipped_out, (hipStream_t)stream),
                        "zo_update");
+}
+
+size_t zo_probe_bits_offset(const zo_config* cfg, int32_t N, int32_t B, int32_t C) {
+  if (!zo::config_valid(cfg) || N < 1 || B < 1 || C < 1 || !zo::bit_cache_kind(*cfg)) return 0;
+  return plan_for(cfg, N, B, C, false).bits;
+}
+
+int zo_update_cached(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
+                     uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
+                     const uint32_t* probe_bits, void* stream) {
+  int st = check_config(cfg);
+  if (st) return st;
+  if (cfg->probe != ZO_RADEMACHER) return fail(ZO_EINVAL, "zo_update_cached: sign probes only");
+  if (!theta || !Lplus || !Lminus || !probe_bits) return fail(ZO_EINVAL, "a required pointer is NULL");
+  if (!aligned16(theta) || !aligned16(probe_bits))
+    return fail(ZO_EINVAL, "theta and probe_bits must be 16-byte aligned");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(ZO_EINVAL, "eps must be finite and > 0");
+  if (!std::isfinite(lr)) return fail(ZO_EINVAL, "lr must be finite");
+  if (N < 1) return fail(ZO_EINVAL, "N must be >= 1");
+  if ((uint64_t)i0 + (uint64_t)N > 0x100000000ull)
+    return fail(ZO_EINVAL, "probe indices i0 .. i0+N-1 must fit in 32 bits");
+  const uint64_t P = zo::make_layout(*cfg).total;
+  return device_status(zo::launch_update(cfg->wdtype, cfg->probe, theta, P, seed, eps, lr, N, i0, Lplus, Lminus,
+                                         skipped_out, (hipStream_t)stream, 1, probe_bits),
+                       "zo_update_cached");
 }
 
 int zo_fd_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,

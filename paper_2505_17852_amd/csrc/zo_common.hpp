@@ -163,9 +163,21 @@ inline ZCacheMap make_zcache_map(const zo_config& c) {
 
 inline bool probe_cache_kind(const zo_config& c) { return c.probe == ZO_GAUSSIAN; }
 
-// Kernel variant for normal probes read from the probe cache (next to the
-// probe kinds ZO_RADEMACHER and ZO_GAUSSIAN, which regenerate them).
+// Bit-packed sign-probe cache (bf16 weights with sign probes): the sign words
+// of probes i0 .. i0+N-1 over the whole parameter vector, written once per call
+// (one Philox block per 128 parameters and probe) and read by the forward
+// kernels in place of regenerating them in every K tile: probe n's word w
+// (the signs of parameters 32 w .. 32 w + 31, bit b set for z = +1) at
+// n * bit_words(P) + w. The update can read the same words
+// (zo_update_cached) instead of regenerating them.
+inline bool bit_cache_kind(const zo_config& c) { return c.probe == ZO_RADEMACHER && c.wdtype == ZO_WBF16; }
+__host__ __device__ inline uint64_t bit_words(uint64_t P) { return (P + 127) / 128 * 4; }
+
+// Kernel variants for normal probes read from the probe cache and for sign
+// probes read from the sign-probe cache (next to the probe kinds ZO_RADEMACHER
+// and ZO_GAUSSIAN, which regenerate them).
 constexpr int kGaussCached = 2;
+constexpr int kSignsCached = 3;
 
 // Workspace plan (byte offsets from the workspace base, 256-aligned).
 struct WsPlan {
@@ -182,7 +194,8 @@ struct WsPlan {
   size_t w16;        // f16 [P_g]          bf16 weights: the product matrices in fp16 (ZCacheMap layout)
   size_t min_total;  // bytes without the probe cache
   size_t zcache;     // probe cache [N][P_g] (normal probes; see ZCacheMap)
-  size_t total;      // bytes with the probe cache (= min_total for sign probes)
+  size_t bits;       // sign-probe cache [N][bit_words(P)] u32 (bf16 weights with sign probes)
+  size_t total;      // bytes with the probe cache
   int nvt;           // vocabulary tiles
   int T;             // time chunk
 };
@@ -217,6 +230,8 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
   w.min_total = p;
   w.zcache = p;
   if (probe_cache_kind(c)) take((size_t)r.N * make_zcache_map(c).pg * (c.wdtype == ZO_WBF16 ? 2 : 4));
+  w.bits = p;
+  if (bit_cache_kind(c)) take((size_t)r.N * bit_words(make_layout(c).total) * 4);
   w.total = p;
   return w;
 }

@@ -18,9 +18,13 @@ hipError_t launch_init(int wdtype, void* theta, uint64_t P, uint64_t seed, float
 // lm_stride 1: Lm holds one loss per probe (central differences); 0: one
 // loss for all probes (forward differences: the clean pass, with eps halved
 // by the caller so that the coefficient divides by eps).
+// bits: the sign words of the probes (zo_update_cached; sign probes only), or
+// nullptr to regenerate them.
 hipError_t launch_update(int wdtype, int kind, void* theta, uint64_t P, uint64_t seed, float eps,
                          float lr, int32_t N, uint32_t i0, const float* Lp, const float* Lm,
-                         int32_t* skipped, hipStream_t s, int lm_stride = 1);
+                         int32_t* skipped, hipStream_t s, int lm_stride = 1, const uint32_t* bits = nullptr);
+// The sign words of probes i0 .. i0+N-1 into bits (layout: bit_words).
+hipError_t launch_bits_fill(uint32_t* bits, uint64_t P, uint64_t seed, uint32_t i0, int32_t N, hipStream_t s);
 
 // k_forward.hip: one call of the perturbed forward passes.
 struct ForwardArgs {
@@ -41,6 +45,7 @@ struct ForwardArgs {
   bool split;       // two-stream products: A.W and A.(s eps z) as separate MFMA streams into one
                     // accumulator (bf16 weights: eps below the fused form's floor; fp32: measurement)
   void* zc;         // probe cache inside work, or nullptr (probes regenerated in every tile)
+  uint32_t* bits;   // sign-probe cache inside work (bf16 weights, sign probes), or nullptr
   void* w16;        // bf16 weights: fp16 copy of the product matrices inside work (ZCacheMap layout)
   ZCacheMap zmap;
 };

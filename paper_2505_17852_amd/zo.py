@@ -75,6 +75,10 @@ def lib():
                                                   vp, vp, C.c_int32, C.c_int32, vp, vp, vp]
         L.zo_fd_losses_ex.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_int32, C.c_uint32,
                                       vp, vp, C.c_int32, C.c_int32, vp, vp, vp, C.c_size_t, C.c_int32, vp]
+        L.zo_probe_bits_offset.argtypes = [cfgp, C.c_int32, C.c_int32, C.c_int32]
+        L.zo_probe_bits_offset.restype = C.c_size_t
+        L.zo_update_cached.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
+                                       vp, vp, vp, vp, vp]
         L.zo_fd_update.argtypes = [cfgp, vp, C.c_uint64, C.c_float, C.c_float, C.c_int32, C.c_uint32,
                                    vp, vp, vp, vp]
         L.zo_debug_probe.argtypes = [C.c_int32, C.c_uint64, C.c_uint32, C.c_uint64, C.c_uint64, vp, vp]
@@ -84,7 +88,7 @@ def lib():
                                       C.POINTER(C.c_int64)]
         L.zo_last_error.restype = C.c_char_p
         for f in ("zo_init", "zo_perturbed_losses", "zo_update", "zo_fd_losses", "zo_fd_update",
-                  "zo_perturbed_losses_ex", "zo_fd_losses_ex", "zo_perturbed_losses_noalloc",
+                  "zo_perturbed_losses_ex", "zo_fd_losses_ex", "zo_perturbed_losses_noalloc", "zo_update_cached",
                   "zo_debug_probe",
                   "zo_debug_gauss_pairs", "zo_profile_enable", "zo_profile_read"):
             getattr(L, f).restype = C.c_int
@@ -246,6 +250,38 @@ def update(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, Lplus: to
                          _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
                          None if skipped is None else _dev(skipped, torch.int32, "skipped"),
                          _stream(stream))
+    _check(st)
+
+
+def probe_bits(cfg, N: int, B: int, C_: int, workspace: torch.Tensor) -> torch.Tensor | None:
+    """The sign-probe cache inside a workspace of workspace_bytes() (a view of
+    it as int32 words), or None when the shape has none."""
+    c = _cfg(cfg)
+    off = int(lib().zo_probe_bits_offset(C.byref(c), N, B, C_))
+    if off == 0:
+        return None
+    P = param_count(cfg)
+    nbytes = N * ((P + 127) // 128) * 4 * 4
+    if workspace.numel() < off + nbytes:
+        raise ValueError("the workspace does not hold the sign-probe cache")
+    return workspace[off:off + nbytes].view(torch.int32)
+
+
+def update_cached(cfg, theta: torch.Tensor, seed: int, eps: float, lr: float, Lplus: torch.Tensor,
+                  Lminus: torch.Tensor, bits: torch.Tensor, i0: int = 0, skipped: torch.Tensor | None = None,
+                  stream=None):
+    """zo_update_cached: the update reading the probes' sign words from bits
+    (probe_bits() of the workspace of the matching perturbed_losses call)."""
+    c = _cfg(cfg)
+    N = Lplus.numel()
+    if Lminus.numel() != N:
+        raise ValueError("Lplus and Lminus differ in length")
+    if bits.numel() < N * ((param_count(cfg) + 127) // 128) * 4:
+        raise ValueError("bits smaller than the N probes' sign words")
+    st = lib().zo_update_cached(C.byref(c), _theta(cfg, theta), seed, eps, lr, N, i0,
+                                _dev(Lplus, torch.float32, "Lplus"), _dev(Lminus, torch.float32, "Lminus"),
+                                None if skipped is None else _dev(skipped, torch.int32, "skipped"),
+                                _dev(bits, torch.int32, "bits"), _stream(stream))
     _check(st)
 
 

@@ -73,8 +73,8 @@ def test_workspace_probe_cache_size(zo, name):
     """Normal probes: the preferred workspace adds exactly the probe cache,
     N values of the weight matrices' size in the weight type (rounded up to
     the 256-byte allocation granule; with bf16 weights the head matrix is
-    stored padded to whole 256-wide vocabulary tiles); sign probes cache
-    nothing."""
+    stored padded to whole 256-wide vocabulary tiles); sign probes with bf16
+    weights add the sign-probe cache, with fp32 weights nothing."""
     w = wl.CONFIGS[name]
     cfg = wl.model_cfg(name)
     full = zo.workspace_bytes(cfg, w["N"], w["B"], w["C"])
@@ -86,8 +86,32 @@ def test_workspace_probe_cache_size(zo, name):
         pg = sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + Vs * H
         el = 2 if cfg["wdtype"] == wl.BF16 else 4
         assert full - small == (w["N"] * pg * el + 255) // 256 * 256
+    elif cfg["wdtype"] == wl.BF16:
+        # sign probes with bf16 weights: the sign-probe cache, N words of 32 signs per 32 parameters
+        P = zo.param_count(cfg)
+        words = (P + 127) // 128 * 4
+        assert full - small == (w["N"] * words * 4 + 255) // 256 * 256
+        assert zo.lib().zo_probe_bits_offset(C.byref(zo._cfg(cfg)), w["N"], w["B"], w["C"]) == small
     else:
         assert full == small
+        assert zo.lib().zo_probe_bits_offset(C.byref(zo._cfg(cfg)), w["N"], w["B"], w["C"]) == 0
+
+
+def test_update_cached_argument_errors(zo):
+    """zo_update_cached takes sign probes only and checks its pointers on the
+    host; zo_probe_bits_offset is 0 without a cache."""
+    L = zo.lib()
+    fake = C.c_void_p(0x10000)
+    bf = zo._cfg(dict(n_layers=1, vocab=256, embed=64, hidden=64, wdtype=wl.BF16, probe=wl.RADEMACHER))
+    gauss = zo._cfg(dict(n_layers=1, vocab=256, embed=64, hidden=64, wdtype=wl.BF16, probe=wl.GAUSSIAN))
+    assert L.zo_update_cached(C.byref(gauss), fake, 1, 1e-3, 1e-3, 2, 0, fake, fake, None, fake, None) == zo.ZO_EINVAL
+    assert L.zo_update_cached(C.byref(bf), fake, 1, 1e-3, 1e-3, 2, 0, fake, fake, None, None, None) == zo.ZO_EINVAL
+    assert L.zo_update_cached(C.byref(bf), fake, 1, 1e-3, 1e-3, 2, 0, fake, fake, None, C.c_void_p(0x10004),
+                              None) == zo.ZO_EINVAL
+    assert L.zo_update_cached(C.byref(bf), fake, 1, 0.0, 1e-3, 2, 0, fake, fake, None, fake, None) == zo.ZO_EINVAL
+    assert L.zo_probe_bits_offset(C.byref(gauss), 2, 2, 2) == 0
+    assert L.zo_probe_bits_offset(C.byref(bf), 0, 2, 2) == 0
+    assert L.zo_probe_bits_offset(C.byref(bf), 2, 2, 2) > 0
 
 
 def _call_losses(zo, cfg, eps=1e-3, N=2, B=2, Cn=4, ptrs=True):

@@ -256,3 +256,54 @@ def test_bf16_two_stream_matches_fused_at_1e3(zo, name):
     err = np.abs((fp - fm) - (sp - sm))
     say(f"{name}: fused {fp - fm}\ntwo-stream {sp - sm}\nerr/ulp {err / ulp}")
     assert np.all(err <= 2 * ulp + 6e-3 * np.abs(sp - sm))
+
+
+SIGN_CACHE_CASES = [
+    # (name, cfg, N, B, C): several unit tiles and a ragged vocabulary; a forward-difference-sized
+    # batch; the 1024-wide layers and 50,000-word vocabulary
+    ("ragged", dict(n_layers=2, vocab=300, embed=64, hidden=128, wdtype=wl.BF16, probe=wl.RADEMACHER), 3, 5, 20),
+    ("deep3", dict(n_layers=3, vocab=130, embed=64, hidden=192, wdtype=wl.BF16, probe=wl.RADEMACHER), 2, 130, 7),
+    ("c3-widths", wl.model_cfg("c3", probe=wl.RADEMACHER), 3, 2, 3),
+]
+
+
+@pytest.mark.parametrize("name,cfg,N,B,C", SIGN_CACHE_CASES, ids=[c[0] for c in SIGN_CACHE_CASES])
+def test_sign_probe_cache(zo, oracle, name, cfg, N, B, C):
+    """The bit-packed sign-probe cache (a workspace of zo_workspace_bytes):
+    its words are the oracle's probe signs; the losses read from it are
+    bit-identical to the regenerating path (the smallest workspace), for
+    central and forward differences and with the two-stream products; and
+    the update reading the same words (zo_update_cached) gives theta bit for
+    bit as zo_update."""
+    say(f"sign-probe cache {name} N={N} B={B} C={C}")
+    rng = np.random.default_rng(41)
+    tok = torch.from_numpy(wl.uniform_tokens(rng, B, C, cfg["vocab"])).cuda()
+    theta = zo.new_theta(cfg)
+    zo.init(cfg, theta, 12)
+    ws_full = zo.new_workspace(cfg, N, B, C)
+    ws_min = zo.new_workspace(cfg, N, B, C, probe_cache=False)
+    assert ws_full.numel() > ws_min.numel()
+    for eps in (1e-3, 1e-4):
+        a = zo.perturbed_losses(cfg, theta, 303, eps, N, tok, i0=7, workspace=ws_full)
+        b = zo.perturbed_losses(cfg, theta, 303, eps, N, tok, i0=7, workspace=ws_min)
+        assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]), (eps, a, b)
+    fa = zo.fd_losses(cfg, theta, 303, 1e-3, N, tok, i0=7, workspace=ws_full)
+    fb = zo.fd_losses(cfg, theta, 303, 1e-3, N, tok, i0=7, workspace=ws_min)
+    assert torch.equal(fa[0], fb[0]) and torch.equal(fa[1], fb[1])
+    # the cache as the last central call left it (eps 1e-3, seed 303, probes 7 .. 7+N-1)
+    Lp, Lm = zo.perturbed_losses(cfg, theta, 303, 1e-3, N, tok, i0=7, workspace=ws_full)
+    bits = zo.probe_bits(cfg, N, B, C, ws_full)
+    P = zo.param_count(cfg)
+    wpp = (P + 127) // 128 * 4
+    words = bits.cpu().numpy().view(np.uint32)
+    for n in range(N):
+        for w0 in (0, wpp // 2 - 3, (P - 1) // 32 - 3):
+            z = oracle.probe(wl.RADEMACHER, 303, 7 + n, 32 * w0, 96)
+            want = [int(sum(1 << b for b in range(32) if z[32 * q + b] > 0)) for q in range(3)]
+            got = [int(x) for x in words[n * wpp + w0:n * wpp + w0 + 3]]
+            assert got == want, (n, w0)
+    t1, t2 = theta.clone(), theta.clone()
+    zo.update(cfg, t1, 303, 1e-3, 0.5, Lp, Lm, i0=7)
+    zo.update_cached(cfg, t2, 303, 1e-3, 0.5, Lp, Lm, bits, i0=7)
+    assert torch.equal(t1.view(torch.int16), t2.view(torch.int16))
+    assert not torch.equal(t1.view(torch.int16), theta.view(torch.int16))

@@ -13,7 +13,9 @@ second and later iterations for any grid of k x 256 workgroups), in the
 middle, around 2^30 and at the end (the last tile ragged); the first and
 last elements of every tensor of the layout; and 10^4 indices drawn
 uniformly. The c2 update (N = 32, the sign-probe kernel for any N) is
-compared in full.
+compared in full. Where the forward call kept a sign-probe cache (bf16
+weights, sign probes), the update reading it (zo_update_cached) must give
+the same theta bit for bit.
 
 Bars: bf16 theta within one bf16 ulp of the oracle (the GPU sums the probe
 terms in fp32, the oracle in double, before the one rounding) plus 2^-16 of
@@ -48,7 +50,7 @@ def say(*a):
     print(*a, flush=True)
 
 
-def bits(theta, cfg):
+def as_host(theta, cfg):
     return theta.view(torch.int16 if cfg["wdtype"] == wl.BF16 else torch.int32).cpu().numpy().view(
         np.uint16 if cfg["wdtype"] == wl.BF16 else np.float32)
 
@@ -114,12 +116,15 @@ def run_step(zo, name, cfg, N, C=None):
     ws = zo.new_workspace(cfg, N, tok.shape[0], tok.shape[1] - 1)
     Lp, Lm = zo.perturbed_losses(cfg, theta, sd["step"], w["eps"], N, td, md, workspace=ws)
     torch.cuda.synchronize()
+    # the sign-probe cache of this call (bf16 weights, sign probes), kept for zo_update_cached
+    pb = zo.probe_bits(cfg, N, tok.shape[0], tok.shape[1] - 1, ws)
+    pb = None if pb is None else pb.clone()
     del ws
     torch.cuda.empty_cache()
     lp, lm = Lp.cpu().numpy(), Lm.cpu().numpy()
     assert np.all(np.isfinite(lp)) and np.all(np.isfinite(lm))
     assert np.any(lp != lm)
-    return theta, Lp, Lm, lp, lm
+    return theta, Lp, Lm, lp, lm, pb
 
 
 # name, workload, probe override, N, C (the update does not depend on C; the
@@ -140,15 +145,15 @@ def test_update_full_size_sampled(zo, oracle, case, name, probe, N, C, whole):
     cfg = wl.model_cfg(name) if probe is None else wl.model_cfg(name, probe=probe)
     P = zo.param_count(cfg)
     say(f"full-size update {case}: P={P} N={N} C={C}")
-    theta, Lp, Lm, lp, lm = run_step(zo, name, cfg, N, C)
-    before = bits(theta, cfg)
+    theta, Lp, Lm, lp, lm, bits = run_step(zo, name, cfg, N, C)
+    before = as_host(theta, cfg)
     skipped = torch.full((1,), -1, dtype=torch.int32, device="cuda")
     lr = w["lr"] * (64 if cfg["wdtype"] == wl.BF16 else 1)
     zo.update(cfg, theta, sd["step"], w["eps"], lr, Lp, Lm, skipped=skipped)
     torch.cuda.synchronize()
     assert skipped.item() == 0
     idx = sample_indices(zo, cfg, whole)
-    after = bits(theta, cfg)
+    after = as_host(theta, cfg)
     del theta
     torch.cuda.empty_cache()
     got = after[idx]
@@ -162,6 +167,11 @@ def test_update_full_size_sampled(zo, oracle, case, name, probe, N, C, whole):
     moved = np.count_nonzero(got != before[idx])
     say(f"{case}: all {idx.size} within the bar; {moved} changed")
     assert moved > idx.size // 2
+    if bits is not None:
+        # the same update reading the call's sign-probe cache: theta bit for bit
+        theta2 = torch.from_numpy(before.view(np.int16)).cuda()
+        zo.update_cached(cfg, theta2.view(torch.bfloat16), sd["step"], w["eps"], lr, Lp, Lm, bits)
+        assert np.array_equal(theta2.cpu().numpy().view(np.uint16), after)
 
 
 def test_update_c2_full(zo, oracle):
@@ -171,11 +181,11 @@ def test_update_c2_full(zo, oracle):
     w = wl.CONFIGS[name]
     sd = wl.seeds(name)
     cfg = wl.model_cfg(name)
-    theta, Lp, Lm, lp, lm = run_step(zo, name, cfg, w["N"])
-    ref = bits(theta, cfg).copy()
+    theta, Lp, Lm, lp, lm, _ = run_step(zo, name, cfg, w["N"])
+    ref = as_host(theta, cfg).copy()
     before = ref.copy()
     zo.update(cfg, theta, sd["step"], w["eps"], w["lr"], Lp, Lm)
-    got = bits(theta, cfg)
+    got = as_host(theta, cfg)
     assert oracle.update(cfg, ref, sd["step"], w["eps"], w["lr"], lp, lm) == 0
     bad = close(got, ref, cfg, before)
     assert bad.size == 0, f"{bad.size} differ, first {bad[:5].tolist()}"
