@@ -227,7 +227,59 @@ def cpu_baseline(name, budget_s=20.0, fd=False):
             break
         n *= 2
     return {"value": rate, "unit": "tokens/s", "cores": ref.threads(), "kind": "oracle",
-            "sample": sample}
+            "sample": sample, "cpu_model": cpu_model(), "host_cpus": host_cpus()}
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def host_cpus():
+    """CPUs this process may run on."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        return os.cpu_count()
+
+
+def start_one_thread(name, fd=False):
+    """Starts the same oracle sample on one thread, in a child process with
+    OMP_NUM_THREADS=1 (the oracle reads its thread count at load). Called
+    before this process touches the GPU, so the child never inherits a GPU
+    context; it runs while the GPU steps are timed."""
+    import atexit
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    cmd = [sys.executable, os.path.abspath(__file__), "--cpu-baseline-only", "--workload", name,
+           "--estimator", "fd" if fd else "cd"]
+    proc = subprocess.Popen(cmd, env=env, stdout=subprocess.PIPE, stderr=subprocess.DEVNULL, text=True)
+    atexit.register(lambda: proc.poll() is None and proc.kill())  # an early exit ends the child too
+    return proc
+
+
+def finish_one_thread(proc, timeout_s=300):
+    """The one-thread figure of start_one_thread's child; None when it fails
+    or does not finish within timeout_s more seconds."""
+    import subprocess
+    try:
+        stdout, _ = proc.communicate(timeout=timeout_s)
+    except subprocess.TimeoutExpired:
+        proc.kill()
+        proc.communicate()
+        return None
+    lines = [l for l in stdout.splitlines() if l.startswith("{")]
+    if proc.returncode != 0 or not lines:
+        return None
+    d = json.loads(lines[-1])
+    return {"value": d["value"], "unit": d["unit"], "cores": d["cores"], "sample": d["sample"]}
 
 
 def main():
@@ -237,6 +289,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="c4", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-baseline-only", action="store_true",
+                    help="time only the CPU oracle on the workload's sample and print it as JSON (the "
+                         "one-thread figure runs this way, with OMP_NUM_THREADS=1)")
     ap.add_argument("--seq-len", type=int, default=None,
                     help="profiling runs only: score the first C positions of each sequence "
                          "(every gate launch keeps the workload's full shape; the JSON line "
@@ -258,11 +313,19 @@ def main():
                     help="cd: central differences, 2N passes (default); fd: forward "
                          "differences, N perturbed passes and one clean pass")
     args = ap.parse_args()
+    if args.cpu_baseline_only:
+        print(json.dumps(cpu_baseline(args.workload, budget_s=10.0, fd=args.estimator == "fd")), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs one GPU's share of the step; --gpus {args.gpus} is not supported "
               "(perturbations would be sharded across GPUs with one all-gather of the 2N "
               "losses per step; that path is not built)", file=sys.stderr)
         sys.exit(2)
+
+    special = args.calibrate_copy or args.calibrate_stream or args.library_gemm
+    one_thread = None
+    if not args.no_cpu_baseline and not special:
+        one_thread = start_one_thread(args.workload, fd=args.estimator == "fd")
 
     import numpy as np
     import torch
@@ -402,8 +465,13 @@ def main():
         "losses_finite": losses_ok,
     }
     if not args.no_cpu_baseline:
+        # the one-thread child first (it ran beside the GPU steps), so that the
+        # multi-thread figure has the host's cores to itself
+        print("[bench] waiting for the one-thread CPU oracle sample", file=sys.stderr, flush=True)
+        single = finish_one_thread(one_thread)
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(name, fd=fd)
+        out["cpu_baseline"]["one_thread"] = single
     print(json.dumps(out), flush=True)
 
 
