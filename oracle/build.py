@@ -12,15 +12,16 @@ LIB = os.path.join(HERE, "libzo_oracle.so")
 
 
 def build(verbose: bool = False) -> str:
+    tmp = f"{LIB}.{os.getpid()}.tmp"  # concurrent builds (parallel test workers) each write their own
     cmd = [
         "gcc", "-std=c11", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
         "-fPIC", "-shared", "-Wall", "-Wextra", "-Wno-unused-parameter",
-        os.path.join(HERE, "zo_oracle.c"), "-o", LIB + ".tmp", "-lm",
+        os.path.join(HERE, "zo_oracle.c"), "-o", tmp, "-lm",
     ]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(tmp, LIB)
     return LIB
 
 

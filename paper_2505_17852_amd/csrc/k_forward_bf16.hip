@@ -37,9 +37,11 @@
 // instruction. Every global access is a buffer access against a resource
 // sized to its matrix (or to the workgroup's activation rows), so an offset
 // outside it reads zeros rather than faulting. The probe term: sign probes as
-// sign bits in LDS (one Philox word per 32 k), expanded per fragment; normal
-// probes either regenerated into an LDS tile per K tile or loaded like the
-// weights from the probe cache.
+// two words of sign flags per column and K tile (regenerated, one Philox word
+// per 32 k, or read from the sign-probe cache) in a small LDS array of their
+// own, which every lane expands into +-fp16(eps) fragments in registers;
+// normal probes either regenerated into an LDS tile per K tile or loaded like
+// the weights from the probe cache.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -67,7 +69,7 @@ struct Tiles {
   static constexpr bool kSigns = kind == ZO_RADEMACHER || kind == kSignsCached;
   static constexpr bool kBits = kind == kSignsCached;      // sign words read from the sign-probe cache
   static constexpr bool kZDirect = kind == kGaussCached;  // probe fragments loaded like the weights
-  static constexpr bool kZTile = !kZDirect;               // probe tile formed in LDS (signs or normals)
+  static constexpr bool kZTile = kind == ZO_GAUSSIAN;     // probe tile of regenerated normals formed in LDS
   static constexpr int TK = 64;                            // K per tile
   static constexpr int KSTEPS = TK / 16;                   // MFMA k steps per tile
   static constexpr int SW = TK / 32;                       // sign words per column and tile
@@ -103,22 +105,42 @@ static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole num
 // LDS stages (static, so that every offset is a constant): activation tile
 // and probe tile (sign and regenerated normal probes), or the activation tile
 // alone (cached normal probes).
-__shared__ __align__(16) uint8_t lds_s0[Tiles<ZO_RADEMACHER>::StageBytes];
-__shared__ __align__(16) uint8_t lds_s1[Tiles<ZO_RADEMACHER>::StageBytes];
+__shared__ __align__(16) uint8_t lds_s0[Tiles<ZO_GAUSSIAN>::StageBytes];
+__shared__ __align__(16) uint8_t lds_s1[Tiles<ZO_GAUSSIAN>::StageBytes];
 __shared__ __align__(16) uint8_t lds_c0[Tiles<kGaussCached>::StageBytes];
 __shared__ __align__(16) uint8_t lds_c1[Tiles<kGaussCached>::StageBytes];
-static_assert(Tiles<ZO_GAUSSIAN>::StageBytes == Tiles<ZO_RADEMACHER>::StageBytes, "probe-tile stages");
-static_assert(Tiles<kSignsCached>::StageBytes == Tiles<ZO_RADEMACHER>::StageBytes, "probe-tile stages");
+static_assert(Tiles<ZO_RADEMACHER>::StageBytes == Tiles<kGaussCached>::StageBytes, "activation-only stages");
+static_assert(Tiles<kSignsCached>::StageBytes == Tiles<kGaussCached>::StageBytes, "activation-only stages");
 static_assert(2 * sizeof(lds_s0) <= 160 * 1024, "LDS");
+// Sign words of a K tile (two per workgroup column, unshuffled), per stage,
+// in arrays of their own: the compiler orders an LDS store after every copy
+// in flight into the same array.
+constexpr int kWordBytes = kVocabTileWide * 2 * 4;
+__shared__ __align__(16) uint8_t lds_words0[kWordBytes];
+__shared__ __align__(16) uint8_t lds_words1[kWordBytes];
 
 template <int kind, int S>
 __device__ __forceinline__ uint8_t* stage() {
   static_assert(S == 0 || S == 1, "stage index");
-  if constexpr (kind == kGaussCached)
+  if constexpr (!Tiles<kind>::kZTile)
     return S == 0 ? lds_c0 : lds_c1;
   else
     return S == 0 ? lds_s0 : lds_s1;
 }
+template <int S>
+__device__ __forceinline__ uint8_t* words4() {
+  static_assert(S == 0 || S == 1, "stage index");
+  return S == 0 ? lds_words0 : lds_words1;
+}
+
+// The workgroup geometry of the loop, as the gate and head epilogues use it:
+// 8 waves, 2 row halves x 4 column quarters, wave tiles of 128 rows x 64
+// columns (4 x 2 tiles of 32x32).
+struct Geo {
+  static constexpr int WAVES_M = Tiles<ZO_GAUSSIAN>::WAVES_M, WAVES_N = Tiles<ZO_GAUSSIAN>::WAVES_N;
+  static constexpr int WROWS = Tiles<ZO_GAUSSIAN>::WROWS, WCOLS = 64;
+  static constexpr int MT = Tiles<ZO_GAUSSIAN>::MT, NTW = 2;
+};
 
 __device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
 
@@ -331,11 +353,9 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // TN columns and TK k, 32 k per thread (sign probes: one Philox word,
   // expanded; normal probes: eight Box-Muller blocks); then advance to the
   // following tile. Cached normal probes have no probe tile.
-  const uint32_t ebits = (uint32_t)eps_b | ((uint32_t)eps_b << 16);
   auto issue_probe = [&](auto stage_tag) {
     constexpr int S = decltype(stage_tag)::value;
     const SegB& sg = seg == 0 ? s0 : s1;
-    uint8_t* zrow = stage<kind, S>() + T::ABytes + zr * T::RowBytes;
     const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
     if constexpr (T::kSigns) {
       uint32_t word;
@@ -350,18 +370,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       } else {
         word = rademacher_word(key, probe, j0 >> 5);
       }
-      // negative-sign flags, even elements in bits 0..15 and odd ones in
-      // 16..31: the pair (2i, 2i+1) is fp16(eps) with the flags of bits i
-      // and 16 + i as sign bits
-      const uint32_t u = unshuffle_bits(~word);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        u4 v;
-#pragma unroll
-        for (int d = 0; d < 4; ++d) v[d] = ((u << (15 - (4 * c + d))) & 0x80008000u) | ebits;
-        *(u4*)(zrow + 16 * ((4 * zpart + c) ^ act_swizzle(zr))) = v;
-      }
+      // the word of column zr's 32 k at 32 zpart, unshuffled
+      *(uint32_t*)(words4<S>() + zr * 8 + zpart * 4) = unshuffle_bits(word);
     } else if constexpr (T::kZTile) {
+      uint8_t* zrow = stage<kind, S>() + T::ABytes + zr * T::RowBytes;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         float za[4], zb[4];
@@ -387,6 +399,15 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // the clean pass): B = fp16(W + s eps z) is one packed fp16 fma per pair
   const _Float16 sh = (_Float16)(float)sgn;
   const h8 s8 = {sh, sh, sh, sh, sh, sh, sh, sh};
+  // sign probes: the fragment of lane (lr, lg) at k step s holds k = 16 s +
+  // 8 lg + e of the tile, i.e. flags 8 (s % 2) + 4 lg + d (d = e / 2) of the
+  // unshuffled word s / 2 of its column; the pre-shift by 4 lg leaves
+  // 8 (s % 2) + d. A set flag means z = +1; the pass sign flips them all
+  // (the clean pass of forward differences gives +-0).
+  const uint32_t flip = sgn < 0 ? 0u : 0xFFFFFFFFu;
+  const uint32_t lshift = 4u * (uint32_t)lg;
+  const uint32_t ebits = sgn == 0 ? 0u : ((uint32_t)eps_b | ((uint32_t)eps_b << 16));
+  const uint32_t w_lane = (uint32_t)((64 * wn + lr) * 8);
   struct Frag {
     h8 a[MT], z[2];
   };
@@ -396,6 +417,15 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     const uint8_t* base = stage<kind, S>();
     const uint8_t* pa = base + a_lane;
     const uint8_t* pz = base + T::ABytes + z_lane;
+    uint32_t us[2][2] = {};
+    if constexpr (T::kSigns) {
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const uint2 wd = *(const uint2*)(words4<S>() + w_lane + 32 * 8 * nt);
+        us[nt][0] = (wd.x ^ flip) >> lshift;
+        us[nt][1] = (wd.y ^ flip) >> lshift;
+      }
+    }
     auto load = [&](int s, Frag& f) {
       const uint32_t so = 16u * ((uint32_t)(2 * s) ^ y);
 #pragma unroll
@@ -436,6 +466,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
           default: w[nt] = wfr[3 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[3 % T::SLOTS][nt]; break;
         }
         if constexpr (T::kZTile) z[nt] = c.z[nt];
+        if constexpr (T::kSigns) {
+          const uint32_t u = us[nt][s >> 1];
+          u4 v;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) v[d] = ((u << (15 - 8 * (s & 1) - d)) & 0x80008000u) | ebits;
+          z[nt] = as_h8(v);  // s eps z, the pass sign included
+        }
       }
       auto mma = [&](const h8(&b)[2]) {
 #pragma unroll
@@ -450,7 +487,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         // one accumulator are MT x 2 instructions apart
         h8 sz[2];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) sz[nt] = z[nt] * s8;
+        for (int nt = 0; nt < 2; ++nt) sz[nt] = T::kSigns ? z[nt] : z[nt] * s8;
         mma(w);
         mma(sz);
       } else {
@@ -458,7 +495,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         // one rounding to nearest even), then one MFMA per accumulator
         h8 wz[2];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) wz[nt] = __builtin_elementwise_fma(z[nt], s8, w[nt]);
+        for (int nt = 0; nt < 2; ++nt)
+          wz[nt] = T::kSigns ? w[nt] + z[nt] : __builtin_elementwise_fma(z[nt], s8, w[nt]);
         mma(wz);
       }
       if (s == 2) issue_probe(next);
@@ -523,17 +561,16 @@ __device__ __forceinline__ float tanh_(float x) { return 1.0f - 2.0f / (__expf(2
 
 // Row (within the workgroup's TM) of accumulator element v of row tile mt
 // for this lane: 32x32 MFMA output layout.
-template <int kind>
 __device__ __forceinline__ int acc_row(int wm, int mt, int lg, int v) {
-  return Tiles<kind>::WROWS * wm + 32 * mt + 8 * (v >> 2) + 4 * lg + (v & 3);
+  return Geo::WROWS * wm + 32 * mt + 8 * (v >> 2) + 4 * lg + (v & 3);
 }
 
-template <int MT>
-__device__ __forceinline__ void zero_acc(f16v (&acc)[MT][2]) {
+template <int MT, int NTW>
+__device__ __forceinline__ void zero_acc(f16v (&acc)[MT][NTW]) {
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = f16v{};
+    for (int nt = 0; nt < NTW; ++nt) acc[mt][nt] = f16v{};
 }
 
 // ---------------------------------------------------------------------------
@@ -561,28 +598,31 @@ struct GateArgsB {
   uint64_t bits_stride;
 };
 
-// Workgroup: TM rows x TN / 4 hidden units. Wave column c (0..63) of wave wn
-// is gate c / 16 of unit 16 wn + c % 16, so lane lr holds gates i, g (lr < 16)
-// or f, o (lr >= 16) of unit lr % 16 in its two column tiles, and one
-// exchange with lane lr ^ 16 brings all four gates of a (row, unit) together.
+// Workgroup: TM rows x 64 hidden units (256 gate columns). Column rho = 64 ug
+// + c of the workgroup is gate c / 16 of unit 16 ug + c % 16; a wave's
+// column tiles come in pairs (2 p, 2 p + 1) covering one group ug of 16
+// units, so lane lr holds gates i, g (lr < 16) or f, o (lr >= 16) of unit
+// lr % 16 in the pair, and one exchange with lane lr ^ 16 brings all four
+// gates of a (row, unit) together.
 template <int kind, bool kFD, bool kSplit>
 __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
-  using T = Tiles<kind>;
+  using G = Geo;
+  constexpr int TN = kVocabTileWide;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
+  const int wm = wave % G::WAVES_M, wn = wave / G::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   int mb, nb;
-  tile_of(blockIdx.x, g.n_row_blocks, g.H / (T::TN / 4), mb, nb);
-  const int u0 = nb * (T::TN / 4);
+  tile_of(blockIdx.x, g.n_row_blocks, g.H / (TN / 4), mb, nb);
+  const int u0 = nb * (TN / 4);
   const int64_t m0 = (int64_t)mb * TM;
   const int pair = pass_of(g.rm, m0).probe;
-  const int sgn = pass_of(g.rm, m0 + T::WROWS * wm).sign;  // a wave tile lies inside one pass
+  const int sgn = pass_of(g.rm, m0 + G::WROWS * wm).sign;  // a wave tile lies inside one pass
   const int H = g.H;
   auto colmap = [&](int rho, int& n) {
     const int c = rho & 63;
     n = (c >> 4) * H + u0 + 16 * (rho >> 6) + (c & 15);
   };
-  f16v acc[T::MT][2];
+  f16v acc[G::MT][G::NTW];
   zero_acc(acc);
   const uint64_t zpos = (uint64_t)pair * g.zc_stride;
   const SegB s0{g.x + m0 * g.El, g.El, g.w_ih16, (uint32_t)((uint64_t)4 * H * g.El * 2), g.off_ih, g.El, g.El,
@@ -594,36 +634,45 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, 8 * (int64_t)nb, colmap, g.key, g.i0 + (uint32_t)pair,
                                      sgn, g.eps, g.eps_b, bits);
 
-  const int hi = lr >> 4;  // 0: gates i, g; 1: gates f, o
-  const int u = u0 + 16 * wn + (lr & 15);
-  float bias[2];
+  constexpr int NP = G::NTW / 2;  // unit groups per wave
+  const int hi = lr >> 4;         // 0: gates i, g; 1: gates f, o
+  int u[NP];
+  float bias[NP][2];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
-    const int gate = 2 * nt + hi;
-    const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)(gate * H + u)]);
-    const float z = g.zb[(int64_t)pair * 4 * H + gate * H + u];
-    bias[nt] = b + (float)sgn * z;
+  for (int p = 0; p < NP; ++p) {
+    u[p] = u0 + 16 * (NP * wn + p) + (lr & 15);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int gate = 2 * q + hi;
+      const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)(gate * H + u[p])]);
+      const float z = g.zb[(int64_t)pair * 4 * H + gate * H + u[p]];
+      bias[p][q] = b + (float)sgn * z;
+    }
   }
 #pragma unroll
-  for (int mt = 0; mt < T::MT; ++mt) {
+  for (int mt = 0; mt < G::MT; ++mt) {
 #pragma unroll
-    for (int v = 0; v < 16; v += 2) {
-      // lanes lr < 16 update row element v, lanes lr >= 16 element v + 1
-      float mine[2], send[2], got[2];
+    for (int p = 0; p < NP; ++p) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const float p0 = acc[mt][nt][v] + bias[nt], p1 = acc[mt][nt][v + 1] + bias[nt];
-        mine[nt] = hi ? p1 : p0;
-        send[nt] = hi ? p0 : p1;
-        got[nt] = __shfl_xor(send[nt], 16, 64);
+      for (int v = 0; v < 16; v += 2) {
+        // lanes lr < 16 update row element v, lanes lr >= 16 element v + 1
+        float mine[2], send[2], got[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const f16v& a = acc[mt][2 * p + q];
+          const float p0 = a[v] + bias[p][q], p1 = a[v + 1] + bias[p][q];
+          mine[q] = hi ? p1 : p0;
+          send[q] = hi ? p0 : p1;
+          got[q] = __shfl_xor(send[q], 16, 64);
+        }
+        const float ip = hi ? got[0] : mine[0], fp = hi ? mine[0] : got[0];
+        const float gp = hi ? got[1] : mine[1], op = hi ? mine[1] : got[1];
+        const int lrow = acc_row(wm, mt, lg, v + hi);
+        const int64_t o = (m0 + lrow) * H + u[p];
+        const float c = sigm(fp) * g.cst[o] + sigm(ip) * tanh_(gp);
+        g.cst[o] = c;
+        g.hout[o] = f16_bits(sigm(op) * tanh_(c));
       }
-      const float ip = hi ? got[0] : mine[0], fp = hi ? mine[0] : got[0];
-      const float gp = hi ? got[1] : mine[1], op = hi ? mine[1] : got[1];
-      const int lrow = acc_row<kind>(wm, mt, lg, v + hi);
-      const int64_t o = (m0 + lrow) * H + u;
-      const float c = sigm(fp) * g.cst[o] + sigm(ip) * tanh_(gp);
-      g.cst[o] = c;
-      g.hout[o] = f16_bits(sigm(op) * tanh_(c));
     }
   }
 }
@@ -656,37 +705,39 @@ struct HeadArgsB {
 
 template <int kind, bool kFD, bool kSplit>
 __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
-  using T = Tiles<kind>;
+  using G = Geo;
+  constexpr int TN = kVocabTileWide;
+  constexpr int NTW = G::NTW;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
+  const int wm = wave % G::WAVES_M, wn = wave / G::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   int mb, vt;
   tile_of(blockIdx.x, (int)(g.rows / TM), g.nvt, mb, vt);
-  const int v0 = vt * T::TN;
+  const int v0 = vt * TN;
   const int64_t rr0 = (int64_t)mb * TM;
   const int tt = (int)(rr0 / g.M);
   const int64_t r0 = rr0 - (int64_t)tt * g.M;
   const int pair = pass_of(g.rm, r0).probe;
-  const int sgn = pass_of(g.rm, r0 + T::WROWS * wm).sign;  // a wave tile lies inside one pass
+  const int sgn = pass_of(g.rm, r0 + G::WROWS * wm).sign;  // a wave tile lies inside one pass
   const int V = g.V;
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
-  f16v acc[T::MT][2];
+  f16v acc[G::MT][NTW];
   zero_acc(acc);
-  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, (uint32_t)((uint64_t)g.nvt * T::TN * g.H * 2), g.off_w, g.H, g.H,
+  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, (uint32_t)((uint64_t)g.nvt * TN * g.H * 2), g.off_w, g.H, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
-  mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, 8 * (int64_t)vt, colmap, g.key, g.i0 + (uint32_t)pair,
-                                    sgn, g.eps, g.eps_b, bits);
+  mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, 8 * (int64_t)vt, colmap, g.key, g.i0 + (uint32_t)pair, sgn,
+                                    g.eps, g.eps_b, bits);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
-  const int cbase = v0 + 64 * wn;
+  const int cbase = v0 + G::WCOLS * wn;
   auto vcol = [&](int v) { return 8 * (v >> 2) + 4 * lg + (v & 3); };
   // bias and bias probe of each column held (-inf past the vocabulary)
-  float add[2][16];
+  float add[NTW][16];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt) {
+  for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int col = cbase + 32 * nt + vcol(v);
@@ -700,17 +751,17 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
     }
   }
   // cross-wave reduction in the first stage buffer (free after the loop)
-  float* red_m = (float*)stage<kind, 0>();         // [WAVES_N][TM]
-  float* red_s = red_m + T::WAVES_N * TM;          // [WAVES_N][TM]
+  float* red_m = (float*)stage<kind, 0>();  // [WAVES_N][TM]
+  float* red_s = red_m + G::WAVES_N * TM;   // [WAVES_N][TM]
 #pragma unroll
-  for (int mt = 0; mt < T::MT; ++mt) {
-    const int lrow = T::WROWS * wm + 32 * mt + lr;
+  for (int mt = 0; mt < G::MT; ++mt) {
+    const int lrow = G::WROWS * wm + 32 * mt + lr;
     const int b = pass_of(g.rm, r0 + lrow).b;
     const int tgt = b < g.B ? g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1] - cbase : -1;
     float mx = -INFINITY, yt = 0.f;
     bool has_t = false;
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
+    for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const float y = acc[mt][nt][v] + add[nt][v];
@@ -722,12 +773,12 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
       }
     }
     if (has_t) g.ptgt[rr0 + lrow] = yt;
-    // the row's 64 columns of this wave: 32 here, 32 in lane lr + 32
+    // the row's WCOLS columns of this wave: half here, half in lane lr + 32
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     float se = 0.f;
     if (mx != -INFINITY) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
+      for (int nt = 0; nt < NTW; ++nt)
 #pragma unroll
         for (int v = 0; v < 16; ++v) se += __expf(acc[mt][nt][v] - mx);
     }
@@ -741,10 +792,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   if (t < TM) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < T::WAVES_N; ++w) mx = fmaxf(mx, red_m[w * TM + t]);
+    for (int w = 0; w < G::WAVES_N; ++w) mx = fmaxf(mx, red_m[w * TM + t]);
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < T::WAVES_N; ++w) {
+    for (int w = 0; w < G::WAVES_N; ++w) {
       const float m = red_m[w * TM + t];
       sum += m == -INFINITY ? 0.f : red_s[w * TM + t] * __expf(m - mx);
     }
@@ -908,7 +959,7 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
     constexpr int kind = decltype(kind_tag)::value;
     constexpr bool fd = decltype(fd_tag)::value;
     constexpr bool split = decltype(split_tag)::value;
-    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (Tiles<kind>::TN / 4))));
+    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (kVocabTileWide / 4))));
     ProfScope ps(kKGate, st);
     gate_bf16_kernel<kind, fd, split><<<grid, NT, 0, st>>>(g);
   };

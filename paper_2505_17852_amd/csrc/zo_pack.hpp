@@ -55,10 +55,10 @@ __host__ __device__ inline uint64_t packed_lane_offset(int64_t cb, int64_t K, in
 }
 __host__ __device__ inline uint32_t packed_step_offset(int64_t ks) { return (uint32_t)ks * kPackBlockBytes; }
 
-// Packed column block of wave column tile nt of wave wn in workgroup column
-// block nb (256 columns, 4 waves of 64 columns, 2 tiles of 32 per wave): the
-// same for the gate (nb = block of 64 hidden units) and the head (nb =
-// vocabulary tile of 256).
+// Packed column block of wave column tile nt of wave column wn in workgroup
+// column block nb (256 columns, 4 wave columns of 64 columns, 2 tiles of 32
+// per wave, in both the 8-wave and the 4-wave loop): the same for the gate
+// (nb = block of 64 hidden units) and the head (nb = vocabulary tile of 256).
 __host__ __device__ inline int64_t packed_block_of(int64_t nb, int wn, int nt) { return 8 * nb + 2 * wn + nt; }
 
 // Activation tile copies (global -> LDS, 1 KB per wave instruction): copy q
@@ -76,5 +76,9 @@ __host__ __device__ inline uint64_t act_copy_offset(int q, int w, int lane, int 
   const int r = act_row_of_copy(q, w, lane, nwaves);
   return (uint64_t)r * (uint64_t)lda * 2u + 16u * (uint64_t)((lane % 8) ^ act_swizzle(r));
 }
+
+// Byte offset, in the sign-probe cache of one probe, of the word holding the
+// sign of parameter j (32 per word).
+__host__ __device__ inline uint32_t sign_word_offset(uint64_t j) { return (uint32_t)(j >> 5) * 4u; }
 
 }  // namespace zo

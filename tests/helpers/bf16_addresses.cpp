@@ -1,15 +1,18 @@
 // Host replay of the bf16 kernels' operand addressing (zo_pack.hpp, the same
 // functions the kernels call): for one model shape and batch, every
 // workgroup, wave, lane, copy and k step of the gate and head launches, it
-// checks that each activation copy and each packed B-fragment load lies
+// checks that
+// each activation copy, packed B-fragment load and sign-probe cache load lies
 // inside the buffer resource it is issued against (and inside the tensor that
 // resource covers), that every offset fits in 32 bits, that the copies fill
 // each LDS row and slot of a tile exactly once with the chunk the swizzle
-// puts there, and that the packed layout and the gate column order are
+// puts there, that each wave loads the weight fragments of its own columns
+// and k, and that the packed layout and the gate column order are
 // bijections. Usage: bf16_addresses L V E H N B fd -> prints "ok" or the
 // first violation (exit status 1).
 #include <cstdint>
 #include <cstdio>
+#include <algorithm>
 #include <cstdlib>
 #include <vector>
 
@@ -28,22 +31,27 @@ static int fails = 0;
     }                                                       \
   } while (0)
 
-constexpr int TM = 256, TN = 256, TK = 64, NWAVES = 8, ACOPIES = 4;
+constexpr int TM = 256, TN = 256, TK = 64;
+// the loop's copy roles: 8 waves, 4 activation copies each per K tile
+struct Geometry {
+  int nwaves, acopies;
+};
+constexpr Geometry kGeo8{8, 4};
 
 // the activation copies of one workgroup tile against a resource of TM rows of lda
-static void check_copies(int64_t lda, int64_t K, const char* what) {
+static void check_copies(int64_t lda, int64_t K, const char* what, Geometry g) {
   const uint64_t records = (uint64_t)TM * lda * 2;
   CHECK(records < (1ull << 31), "%s: resource of %llu bytes", what, (unsigned long long)records);
   std::vector<int> seen(TM * 8, 0);
-  for (int q = 0; q < ACOPIES; ++q)
-    for (int w = 0; w < NWAVES; ++w)
+  for (int q = 0; q < g.acopies; ++q)
+    for (int w = 0; w < g.nwaves; ++w)
       for (int lane = 0; lane < 64; ++lane) {
-        const int row = act_row_of_copy(q, w, lane, NWAVES);
+        const int row = act_row_of_copy(q, w, lane, g.nwaves);
         CHECK(row >= 0 && row < TM, "%s: copy row %d", what, row);
-        const int lds = (q * NWAVES + w) * 1024 + 16 * lane;  // LDS byte this lane writes
+        const int lds = (q * g.nwaves + w) * 1024 + 16 * lane;  // LDS byte this lane writes
         CHECK(lds == row * 128 + 16 * (lane % 8), "%s: LDS byte %d for row %d", what, lds, row);
         seen[row * 8 + lane % 8] += 1;
-        const uint64_t off0 = act_copy_offset(q, w, lane, NWAVES, lda);
+        const uint64_t off0 = act_copy_offset(q, w, lane, g.nwaves, lda);
         const int chunk = (int)((off0 - (uint64_t)row * lda * 2) / 16);
         CHECK(chunk == ((lane % 8) ^ act_swizzle(row)), "%s: chunk %d in slot %d of row %d", what, chunk,
               lane % 8, row);
@@ -56,7 +64,9 @@ static void check_copies(int64_t lda, int64_t K, const char* what) {
   for (int i = 0; i < TM * 8; ++i) CHECK(seen[i] == 1, "%s: LDS row %d slot %d written %d times", what, i / 8, i % 8, seen[i]);
 }
 
-// the packed B loads of column block nb (waves wn, tiles nt, every lane and k step)
+// the packed B loads of column block nb (wave columns wn, tiles nt, every
+// lane and k step; both loops use 4 wave columns of 2 tiles): each wave's
+// tiles are its own columns
 static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what) {
   const uint64_t records = (uint64_t)cols * K * 2;
   CHECK(records < (1ull << 31), "%s: packed matrix of %llu bytes", what, (unsigned long long)records);
@@ -66,6 +76,7 @@ static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what)
       for (int lane = 0; lane < 64; ++lane)
         for (int64_t ks : {(int64_t)0, KS - 1}) {
           const int64_t cb = packed_block_of(nb, wn, nt);
+          CHECK(cb == 8 * nb + (64 * wn + 32 * nt) / 32, "%s: block of wave column %d tile %d", what, wn, nt);
           const uint64_t off = packed_lane_offset(cb, K, lane) + packed_step_offset(ks);
           CHECK(off + 16 <= records && off < (1ull << 32), "%s: B offset %llu of %llu", what,
                 (unsigned long long)off, (unsigned long long)records);
@@ -73,6 +84,20 @@ static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what)
           const PackedChunk pc = packed_chunk(off / 16, K);
           CHECK(pc.col == 32 * cb + (lane & 31) && pc.k == 16 * ks + 8 * (lane >> 5), "%s: packed chunk", what);
         }
+}
+
+// the sign-probe cache loads: the two words (32 k each, one per thread of a
+// column's pair) of K tile k0 of the parameter row n of a matrix at zoff (row
+// stride ldw), inside the bit_words(P) words of one probe
+static void check_words(uint64_t zoff, int64_t n, int64_t ldw, int64_t K, uint64_t P, const char* what) {
+  const uint64_t bytes = 4 * (4 * ((P + 127) / 128));
+  for (int64_t k0 : {(int64_t)0, K - TK})
+    for (int i = 0; i < 2; ++i) {
+      const uint64_t j = zoff + (uint64_t)n * (uint64_t)ldw + (uint64_t)k0 + 32u * (uint64_t)i;
+      const uint64_t off = sign_word_offset(j);
+      CHECK(j < P && off + 4 <= bytes && off == (j / 32) * 4, "%s: sign word of parameter %llu at %llu of %llu",
+            what, (unsigned long long)j, (unsigned long long)off, (unsigned long long)bytes);
+    }
 }
 
 int main(int argc, char** argv) {
@@ -112,24 +137,51 @@ int main(int argc, char** argv) {
     }
     for (size_t i = 0; i < hit.size(); ++i) CHECK(hit[i] == 1, "packed (col, k) %zu hit %d times", i, hit[i]);
   }
-  // gate launches: every layer's two segments, every workgroup
+  // the flat parameter layout: EMB, per layer W_ih, W_hh, b, then W_out, b_out
+  std::vector<uint64_t> off_ih(L), off_hh(L);
+  uint64_t P = (uint64_t)V * E;
+  for (int l = 0; l < L; ++l) {
+    const int64_t El = l == 0 ? E : H;
+    off_ih[l] = P;
+    P += 4 * H * El;
+    off_hh[l] = P;
+    P += 4 * H * H;
+    P += 4 * H;
+  }
+  const uint64_t off_out = P;
+  P += (uint64_t)V * H + V;
+  // gate launches: every layer's two segments, every workgroup, both loops
   const int64_t nm = M / TM, nn = H / 64;
   for (int l = 0; l < L; ++l) {
     const int64_t El = l == 0 ? E : H;
-    check_copies(El, El, "gate x");
-    check_copies(H, H, "gate h");
+    check_copies(El, El, "gate x", kGeo8);
+    check_copies(H, H, "gate h", kGeo8);
     for (int64_t mb = 0; mb < nm; ++mb) CHECK((mb + 1) * TM <= M, "gate row block %lld", (long long)mb);
     for (int64_t nb = 0; nb < nn; ++nb) {
       check_b_loads(nb, 4 * H, El, "gate W_ih");
       check_b_loads(nb, 4 * H, H, "gate W_hh");
+      // the sign words of every workgroup column (the gate column order)
+      for (int rho = 0; rho < TN; ++rho) {
+        const int c = rho & 63;
+        const int64_t n = (c >> 4) * H + 64 * nb + 16 * (rho >> 6) + (c & 15);
+        CHECK(n == gate_row_of_column(TN * nb + rho, H), "gate sign-word row of column %d", rho);
+        check_words(off_ih[l], n, El, El, P, "gate W_ih");
+        check_words(off_hh[l], n, H, H, P, "gate W_hh");
+      }
     }
   }
   // head launches: Tc timesteps of M rows (Tc <= 16), every vocabulary tile
   for (int64_t Tc : {(int64_t)1, (int64_t)16}) {
     const int64_t rows = Tc * M;
     CHECK(rows % TM == 0, "head rows");
-    check_copies(H, H, "head h");
-    for (int64_t vt = 0; vt < nvt; ++vt) check_b_loads(vt, out_rows, H, "head W_out");
+    check_copies(H, H, "head h", kGeo8);
+  }
+  for (int64_t vt = 0; vt < nvt; ++vt) {
+    check_b_loads(vt, out_rows, H, "head W_out");
+    for (int rho = 0; rho < TN; ++rho) {
+      const int64_t n = std::min<int64_t>(TN * vt + rho, V - 1);
+      check_words(off_out, n, H, H, P, "head W_out");
+    }
   }
   if (fails) {
     std::printf("%d violations\n", fails);
