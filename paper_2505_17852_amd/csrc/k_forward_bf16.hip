@@ -17,21 +17,19 @@
 // the two-stream form acc += A . W; acc += A . (s eps z) is used instead
 // (kSplit).
 //
-// Tiles: a workgroup of 8 waves computes TM = 256 rows x TN = 256 columns
-// (waves 2 x 4, wave tiles 128 x 64 = 4 x 2 tiles of 32x32 MFMA output); two
-// waves share each SIMD, so one wave's loads, probe expansion and address
-// work run under the other's matrix instructions. Lane l feeds row/column
-// l % 32 and k block l / 32.
+// Tiles: a workgroup of 8 waves computes TM rows x TN columns, TM x TN =
+// 65536 (TN = kVocabTileWide: 128 x 512, or 256 x 256); its waves split the
+// columns into TN / 64 wave columns and the rows into 8 / (TN / 64) wave
+// rows, each wave computing 128 rows x 64 columns (4 x 2 tiles of 32x32 MFMA
+// output). Two waves share each SIMD, so one wave's loads, probe expansion
+// and address work run under the other's matrix instructions. Lane l feeds
+// row/column l % 32 and k block l / 32.
 //
-// Operands. The LDS of a compute unit serves about 128 bytes per clock, shared
-// between copies into it and fragment reads, and that is what bounds a
-// 256 x 256 tile whose two operands both pass through it (256 KB per K tile of
-// 64: 64 KB copied in, 192 KB read). So only the A operand (the activations,
-// read by the 4 waves of a row half) goes through LDS: each K tile of the 256
-// rows (32 KB) is copied from global memory straight into LDS (buffer loads
-// with the LDS destination, 1 KB per wave instruction), one tile ahead, into
-// one of two stages. The B operand (the fp16 weight copy, and the cached
-// fp16(eps z) of normal probes), read by 2 waves each, is loaded by each wave
+// Operands. The activations (A) pass through LDS: each K tile of the TM rows
+// is copied from global memory straight into LDS (buffer loads with the LDS
+// destination, 1 KB per wave instruction), one tile ahead, into one of two
+// stages, and read by every wave of its rows. The B operand (the fp16 weight
+// copy, and the cached fp16(eps z) of normal probes) is loaded by each wave
 // straight into registers, a few k steps ahead, from the fragment-packed
 // copies the call writes (zo_pack.hpp): one contiguous 1 KB per wave
 // instruction. Every global access is a buffer access against a resource
@@ -59,7 +57,7 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
-constexpr int TM = 256;         // rows per workgroup
+constexpr int TM = 65536 / kVocabTileWide;  // rows per workgroup (kVocabTileWide columns)
 constexpr int NWAVES = 8;
 constexpr int NT = 64 * NWAVES;  // threads per workgroup
 
@@ -89,18 +87,19 @@ struct Tiles {
   static constexpr int DIST = kZDirect ? 1 : 3;
   static constexpr int SLOTS = DIST + 1;
   static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
-  static constexpr int WordLoads = kBits ? 1 : 0;  // sign-word loads per tile (one tile ahead)
   // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
   static constexpr int ZROW_T = NT / TN;
   static constexpr int ZVALS = TK / ZROW_T;
+  static constexpr int WPT = ZVALS / 32;  // sign words (or blocks of 32 normals) per thread and tile
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
   static_assert(ACopies * NWAVES * 1024 == ABytes, "copy split");
   static_assert(KSTEPS % SLOTS == 0, "the B slots repeat every tile");
-  static_assert(ZVALS == 32 && ZROW_T * TN == NT, "probe roles: one 32-k sign word per thread");
+  static_assert(ZVALS % 32 == 0 && ZROW_T * TN == NT, "probe roles: whole 32-k sign words per thread");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
   static_assert(RowBytes == 128, "swizzle of 128-byte rows (act_swizzle)");
 };
 static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole number of row tiles");
+static_assert(TM % 128 == 0 && TM * kVocabTileWide == 65536, "workgroup tile");
 
 // LDS stages (static, so that every offset is a constant): activation tile
 // and probe tile (sign and regenerated normal probes), or the activation tile
@@ -322,23 +321,25 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       }
     }
   };
-  // cached sign words: the word of this thread's 32 k of a tile, loaded one
-  // tile before issue_probe needs it (wseg, wk0: the next tile to load)
+  // cached sign words: the WPT words of this thread's k of a tile, loaded
+  // one tile before issue_probe needs them (wseg, wk0: the next tile to
+  // load), into the buffer of the tile's parity (a register move would wait
+  // for the load)
   Rsrc rbits = rw0;
   if constexpr (T::kBits) rbits = make_rsrc(bits.words, bits.bytes);
   int wseg = 0, wk0 = 0;
-  uint32_t wcur = 0u, wnext = 0u;
-  auto load_word = [&]() {
+  uint32_t wbuf[2][T::WPT] = {};
+  auto load_words = [&](uint32_t (&dst)[T::WPT]) {
     const SegB& sg = wseg == 0 ? s0 : s1;
     const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)wk0 + T::ZVALS * zpart;
-    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rbits, (uint32_t)(j0 >> 5) * 4u, 0, 0);
+#pragma unroll
+    for (int i = 0; i < T::WPT; ++i)
+      dst[i] = __builtin_amdgcn_raw_buffer_load_b32(rbits, sign_word_offset(j0 + 32u * (uint64_t)i), 0, 0);
     next_tile(wseg, wk0);
-    return w;
   };
 
-  // The next K tile's activation copies into stage S (issued first in a tile,
-  // so that the loads after them are the B loads of this tile: the count
-  // wait_and_barrier leaves in flight).
+  // The next K tile's activation copies into stage S (the last loads of a
+  // tile before its B loads: the count wait_and_barrier leaves in flight).
   auto issue_copies = [&](auto stage_tag) {
     constexpr int S = decltype(stage_tag)::value;
     uint8_t* base = stage<kind, S>();
@@ -349,37 +350,42 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       copy_to_lds(second ? ra1 : ra0, arow2[q] * lda2 + achunk[q], 2u * (uint32_t)k0,
                   base + (q * NWAVES + wave) * 1024);
   };
-  // The next K tile's probe tile into stage S, fp16(+eps z) of the tile's
-  // TN columns and TK k, 32 k per thread (sign probes: one Philox word,
-  // expanded; normal probes: eight Box-Muller blocks); then advance to the
-  // following tile. Cached normal probes have no probe tile.
+  // The next K tile's probe part into stage S, then advance to the
+  // following tile: the sign words of the tile's TN columns (WPT words per
+  // thread: regenerated, or read from the sign-probe cache), or the tile of
+  // fp16(eps z) of regenerated normal probes (eight Box-Muller blocks per 32
+  // k). Cached normal probes have no probe part.
   auto issue_probe = [&](auto stage_tag) {
     constexpr int S = decltype(stage_tag)::value;
     const SegB& sg = seg == 0 ? s0 : s1;
     const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
     if constexpr (T::kSigns) {
-      uint32_t word;
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
-      if constexpr (T::kBits) {
-        word = wcur;
-        wcur = wnext;
-      } else if (aligned) {
-        if ((k0 & 127) == 0) zcache = stream_block(key, j0 >> 7, probe, kTagRademacher);
-        const int q = (int)((j0 >> 5) & 3u);
-        word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
-      } else {
-        word = rademacher_word(key, probe, j0 >> 5);
+#pragma unroll
+      for (int i = 0; i < T::WPT; ++i) {
+        const uint64_t j = j0 + 32u * (uint64_t)i;
+        uint32_t word;
+        if constexpr (T::kBits) {
+          word = wbuf[S][i];
+        } else if (aligned) {
+          // one Philox block holds the words of 128 k
+          if ((j & 127u) == 0 || i == 0) zcache = stream_block(key, j >> 7, probe, kTagRademacher);
+          const int q = (int)((j >> 5) & 3u);
+          word = q == 0 ? zcache.w[0] : q == 1 ? zcache.w[1] : q == 2 ? zcache.w[2] : zcache.w[3];
+        } else {
+          word = rademacher_word(key, probe, j >> 5);
+        }
+        // the word of column zr's 32 k at 32 (WPT zpart + i), unshuffled
+        *(uint32_t*)(words4<S>() + zr * 8 + (T::WPT * zpart + i) * 4) = unshuffle_bits(word);
       }
-      // the word of column zr's 32 k at 32 zpart, unshuffled
-      *(uint32_t*)(words4<S>() + zr * 8 + zpart * 4) = unshuffle_bits(word);
     } else if constexpr (T::kZTile) {
       uint8_t* zrow = stage<kind, S>() + T::ABytes + zr * T::RowBytes;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
+#pragma unroll 2
+      for (int c = 0; c < 4 * T::WPT; ++c) {
         float za[4], zb[4];
         gauss_block(key, probe, (j0 >> 2) + 2 * c, za);
         gauss_block(key, probe, (j0 >> 2) + 2 * c + 1, zb);
-        *(u4*)(zrow + 16 * ((4 * zpart + c) ^ act_swizzle(zr))) =
+        *(u4*)(zrow + 16 * ((4 * T::WPT * zpart + c) ^ act_swizzle(zr))) =
             u4{pack_f16x2(eps * za[0], eps * za[1]), pack_f16x2(eps * za[2], eps * za[3]),
                pack_f16x2(eps * zb[0], eps * zb[1]), pack_f16x2(eps * zb[2], eps * zb[3])};
       }
@@ -441,11 +447,14 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     for (int s = 0; s < KSTEPS; ++s) {
       const Frag& c = f[s & 1];
       if (s == 0) {
-        // the next tile's activation copies first, then the sign word two
-        // tiles ahead and this step's B loads
+        // the sign words two tiles ahead (cached), then the next tile's
+        // activation copies, then this step's B loads
+        if constexpr (T::kBits) {
+          load_words(wbuf[S]);
+          issue_fence();
+        }
         issue_copies(next);
         issue_fence();
-        if constexpr (T::kBits) wnext = load_word();
       }
       // B fragments DIST steps ahead
       switch ((s + T::DIST) % T::SLOTS) {
@@ -507,23 +516,24 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // copies of tile it (the B loads issued after them may stay in flight) and
   // its LDS writes; barrier (tile it complete for every wave, and the stage
   // computed at it - 1 free); compute it while issuing tile it + 1 into the
-  // other stage. Prologue: tile 0's copies and probe tile, the first DIST
-  // steps' B loads.
+  // other stage. Prologue: the sign words of tiles 0 and 1 (cached), tile 0's
+  // copies and probe part, the first DIST steps' B loads.
+  if constexpr (T::kBits) {
+    load_words(wbuf[0]);
+    load_words(wbuf[1]);
+    issue_fence();
+  }
   issue_copies(std::integral_constant<int, 0>{});
   issue_fence();
-  if constexpr (T::kBits) {
-    wcur = load_word();   // tile 0, used by the prologue's issue_probe
-    wnext = load_word();  // tile 1
-  }
   if constexpr (T::DIST >= 1) load_b(std::integral_constant<int, 0>{}, 0);
   if constexpr (T::DIST >= 2) load_b(std::integral_constant<int, 1>{}, 1);
   if constexpr (T::DIST >= 3) load_b(std::integral_constant<int, 2>{}, 2);
   issue_probe(std::integral_constant<int, 0>{});
   // loads issued after the copies of the tile a barrier waits for: the first
-  // DIST steps' B loads and two sign words (prologue), then a whole tile's B
-  // loads and one sign word (every later tile)
-  constexpr int kAfter0 = T::DIST * T::LoadsPerStep + 2 * T::WordLoads;
-  constexpr int kAfter = KSTEPS * T::LoadsPerStep + T::WordLoads;
+  // DIST steps' B loads (prologue), then a whole tile's B loads (every later
+  // tile); the cached sign words are issued before the copies
+  constexpr int kAfter0 = T::DIST * T::LoadsPerStep;
+  constexpr int kAfter = KSTEPS * T::LoadsPerStep;
   wait_and_barrier<kAfter0>();
   int it = 0;
   for (; it + 1 < ntiles; it += 2) {
@@ -598,7 +608,7 @@ struct GateArgsB {
   uint64_t bits_stride;
 };
 
-// Workgroup: TM rows x 64 hidden units (256 gate columns). Column rho = 64 ug
+// Workgroup: TM rows x TN / 4 hidden units (TN gate columns). Column rho = 64 ug
 // + c of the workgroup is gate c / 16 of unit 16 ug + c % 16; a wave's
 // column tiles come in pairs (2 p, 2 p + 1) covering one group ug of 16
 // units, so lane lr holds gates i, g (lr < 16) or f, o (lr >= 16) of unit
@@ -612,15 +622,17 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   const int wm = wave % G::WAVES_M, wn = wave / G::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
   int mb, nb;
-  tile_of(blockIdx.x, g.n_row_blocks, g.H / (TN / 4), mb, nb);
+  tile_of(blockIdx.x, g.n_row_blocks, (4 * g.H + TN - 1) / TN, mb, nb);
   const int u0 = nb * (TN / 4);
   const int64_t m0 = (int64_t)mb * TM;
   const int pair = pass_of(g.rm, m0).probe;
   const int sgn = pass_of(g.rm, m0 + G::WROWS * wm).sign;  // a wave tile lies inside one pass
   const int H = g.H;
+  // (columns past the 4H of the matrix, in a last workgroup column block
+  // that 4H does not fill, map to its last row; they are never scored)
   auto colmap = [&](int rho, int& n) {
     const int c = rho & 63;
-    n = (c >> 4) * H + u0 + 16 * (rho >> 6) + (c & 15);
+    n = min((c >> 4) * H + u0 + 16 * (rho >> 6) + (c & 15), 4 * H - 1);
   };
   f16v acc[G::MT][G::NTW];
   zero_acc(acc);
@@ -631,10 +643,11 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
                 kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
-  mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, 8 * (int64_t)nb, colmap, g.key, g.i0 + (uint32_t)pair,
-                                     sgn, g.eps, g.eps_b, bits);
+  mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, (TN / kPackBlockCols) * (int64_t)nb, colmap, g.key,
+                                     g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b, bits);
 
   constexpr int NP = G::NTW / 2;  // unit groups per wave
+  if (u0 + 16 * NP * wn >= H) return;  // a wave past the hidden units (wave-uniform)
   const int hi = lr >> 4;         // 0: gates i, g; 1: gates f, o
   int u[NP];
   float bias[NP][2];
@@ -727,8 +740,8 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
-  mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, 8 * (int64_t)vt, colmap, g.key, g.i0 + (uint32_t)pair, sgn,
-                                    g.eps, g.eps_b, bits);
+  mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, (TN / kPackBlockCols) * (int64_t)vt, colmap, g.key,
+                                    g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b, bits);
 
   // transposed tiles: acc[mt][nt][v] is the logit of activation row
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
@@ -959,7 +972,7 @@ hipError_t launch_gate_bf16(const ForwardArgs& a, int l, const void* x, const vo
     constexpr int kind = decltype(kind_tag)::value;
     constexpr bool fd = decltype(fd_tag)::value;
     constexpr bool split = decltype(split_tag)::value;
-    const dim3 grid((unsigned)(g.n_row_blocks * (g.H / (kVocabTileWide / 4))));
+    const dim3 grid((unsigned)(g.n_row_blocks * ((4 * g.H + kVocabTileWide - 1) / kVocabTileWide)));
     ProfScope ps(kKGate, st);
     gate_bf16_kernel<kind, fd, split><<<grid, NT, 0, st>>>(g);
   };

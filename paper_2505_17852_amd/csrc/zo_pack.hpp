@@ -55,11 +55,13 @@ __host__ __device__ inline uint64_t packed_lane_offset(int64_t cb, int64_t K, in
 }
 __host__ __device__ inline uint32_t packed_step_offset(int64_t ks) { return (uint32_t)ks * kPackBlockBytes; }
 
-// Packed column block of wave column tile nt of wave column wn in workgroup
-// column block nb (256 columns, 4 wave columns of 64 columns, 2 tiles of 32
-// per wave, in both the 8-wave and the 4-wave loop): the same for the gate
-// (nb = block of 64 hidden units) and the head (nb = vocabulary tile of 256).
-__host__ __device__ inline int64_t packed_block_of(int64_t nb, int wn, int nt) { return 8 * nb + 2 * wn + nt; }
+// Packed column block of column tile nt (of 2) of wave column wn (64
+// columns each) in workgroup column block nb of tn columns: the same for the
+// gate (nb = block of tn / 4 hidden units) and the head (nb = vocabulary tile
+// of tn).
+__host__ __device__ inline int64_t packed_block_of(int64_t nb, int wn, int nt, int tn) {
+  return (int64_t)(tn / kPackBlockCols) * nb + 2 * wn + nt;
+}
 
 // Activation tile copies (global -> LDS, 1 KB per wave instruction): copy q
 // of wave w fills LDS rows 8 (q NW + w) .. + 7 of the 256-row tile (128-byte

@@ -16,6 +16,7 @@
 #include <cstdlib>
 #include <vector>
 
+#include "../../paper_2505_17852_amd/csrc/zo_common.hpp"
 #include "../../paper_2505_17852_amd/csrc/zo_pack.hpp"
 
 using namespace zo;
@@ -31,12 +32,12 @@ static int fails = 0;
     }                                                       \
   } while (0)
 
-constexpr int TM = 256, TN = 256, TK = 64;
-// the loop's copy roles: 8 waves, 4 activation copies each per K tile
+constexpr int TN = kVocabTileWide, TM = 65536 / TN, TK = 64;
+// the loop's copy roles: 8 waves, TM / 64 activation copies each per K tile
 struct Geometry {
   int nwaves, acopies;
 };
-constexpr Geometry kGeo8{8, 4};
+constexpr Geometry kGeo8{8, TM * 128 / 1024 / 8};
 
 // the activation copies of one workgroup tile against a resource of TM rows of lda
 static void check_copies(int64_t lda, int64_t K, const char* what, Geometry g) {
@@ -64,22 +65,29 @@ static void check_copies(int64_t lda, int64_t K, const char* what, Geometry g) {
   for (int i = 0; i < TM * 8; ++i) CHECK(seen[i] == 1, "%s: LDS row %d slot %d written %d times", what, i / 8, i % 8, seen[i]);
 }
 
-// the packed B loads of column block nb (wave columns wn, tiles nt, every
-// lane and k step; both loops use 4 wave columns of 2 tiles): each wave's
-// tiles are its own columns
+// the packed B loads of column block nb (TN / 64 wave columns wn of 2 tiles
+// nt, every lane and k step): each wave's tiles are its own columns
 static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what) {
   const uint64_t records = (uint64_t)cols * K * 2;
   CHECK(records < (1ull << 31), "%s: packed matrix of %llu bytes", what, (unsigned long long)records);
   const int64_t KS = K / kPackKStep;
-  for (int wn = 0; wn < 4; ++wn)
+  for (int wn = 0; wn < TN / 64; ++wn)
     for (int nt = 0; nt < 2; ++nt)
       for (int lane = 0; lane < 64; ++lane)
         for (int64_t ks : {(int64_t)0, KS - 1}) {
-          const int64_t cb = packed_block_of(nb, wn, nt);
-          CHECK(cb == 8 * nb + (64 * wn + 32 * nt) / 32, "%s: block of wave column %d tile %d", what, wn, nt);
+          const int64_t cb = packed_block_of(nb, wn, nt, TN);
+          CHECK(cb == (TN * nb + 64 * wn + 32 * nt) / 32, "%s: block of wave column %d tile %d", what, wn, nt);
           const uint64_t off = packed_lane_offset(cb, K, lane) + packed_step_offset(ks);
-          CHECK(off + 16 <= records && off < (1ull << 32), "%s: B offset %llu of %llu", what,
-                (unsigned long long)off, (unsigned long long)records);
+          // no 32-bit wrap: an offset past the resource reads zeros, one that
+          // wrapped would read real data
+          CHECK(off < (1ull << 32), "%s: B offset %llu wraps", what, (unsigned long long)off);
+          if (32 * cb >= cols) {
+            // a column block past the matrix (a last workgroup it does not fill)
+            CHECK(off >= records, "%s: block %lld past the matrix reads inside it", what, (long long)cb);
+            continue;
+          }
+          CHECK(off + 16 <= records, "%s: B offset %llu of %llu", what, (unsigned long long)off,
+                (unsigned long long)records);
           // the chunk read is the fragment piece of column 32 cb + lr at k 16 ks + 8 lg
           const PackedChunk pc = packed_chunk(off / 16, K);
           CHECK(pc.col == 32 * cb + (lane & 31) && pc.k == 16 * ks + 8 * (lane >> 5), "%s: packed chunk", what);
@@ -150,8 +158,9 @@ int main(int argc, char** argv) {
   }
   const uint64_t off_out = P;
   P += (uint64_t)V * H + V;
-  // gate launches: every layer's two segments, every workgroup, both loops
-  const int64_t nm = M / TM, nn = H / 64;
+  // gate launches: every layer's two segments, every workgroup (TN / 4
+  // hidden units each; the last may be partly past the 4H columns)
+  const int64_t nm = M / TM, nn = (4 * H + TN - 1) / TN;
   for (int l = 0; l < L; ++l) {
     const int64_t El = l == 0 ? E : H;
     check_copies(El, El, "gate x", kGeo8);
@@ -163,8 +172,9 @@ int main(int argc, char** argv) {
       // the sign words of every workgroup column (the gate column order)
       for (int rho = 0; rho < TN; ++rho) {
         const int c = rho & 63;
-        const int64_t n = (c >> 4) * H + 64 * nb + 16 * (rho >> 6) + (c & 15);
-        CHECK(n == gate_row_of_column(TN * nb + rho, H), "gate sign-word row of column %d", rho);
+        const int64_t n = std::min<int64_t>((c >> 4) * H + TN / 4 * nb + 16 * (rho >> 6) + (c & 15), 4 * H - 1);
+        if (TN * nb + rho < 4 * H)
+          CHECK(n == gate_row_of_column(TN * nb + rho, H), "gate sign-word row of column %d", rho);
         check_words(off_ih[l], n, El, El, P, "gate W_ih");
         check_words(off_hh[l], n, H, H, P, "gate W_hh");
       }
