@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <optional>
 #include <type_traits>
 
 #include "zo_kernels.hpp"
@@ -941,6 +942,8 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   } while (0)
 
   const int T = W.T;
+  std::optional<PhaseRange> phase;
+  phase.emplace("forward: prepare");
   // every pass starts from h = c = 0: zero what is read before it is written
   // (the state slots that timestep 0 reads, the cell states) and the row sums
   for (int l = 0; l + 1 < L; ++l) ZO_TRY(zero_async(hbuf + (size_t)(2 * l + 1) * state, state, st));
@@ -986,7 +989,9 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
   // chunk's.
   const int ndiag = bf16 ? a.C : a.C + L - 1;
   const size_t x0_step = (size_t)M * c.embed * el;  // one timestep of embeddings
+  phase.reset();
   for (int d = 0; d < ndiag; ++d) {
+    PhaseRange step_range("forward: layer steps of one timestep");
     if (bf16) ZO_TRY(launch_embed_bf16(a, d, x0, st));
     else if (d < a.C && d % T == 0) ZO_TRY(launch_embed_f32(a, d, std::min(T, a.C - d), x0, st));
     if (bf16) {
@@ -1025,6 +1030,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
     if (t >= 0 && (t % T == T - 1 || t == a.C - 1)) {
       const int t0 = t - t % T;
       const int Tc = t - t0 + 1;
+      PhaseRange head_range("forward: head and cross entropy of a time chunk");
       ZO_TRY(head(a, hist, t0, Tc, zbo, pmax, psum, ptgt, st));
       ProfScope ps(kKCombine, st);
       const int64_t rows = (int64_t)Tc * M;
@@ -1035,6 +1041,7 @@ hipError_t launch_forward(const ForwardArgs& a, hipStream_t st) {
       ZO_TRY(hipGetLastError());
     }
   }
+  PhaseRange reduce_range("forward: loss reduction");
   reduce_kernel<<<1, 256, 0, st>>>(row_loss, R.N, R.B, a.C, rm, a.mask, a.Lplus, a.Lminus);
   ZO_TRY(hipGetLastError());
 #undef ZO_TRY

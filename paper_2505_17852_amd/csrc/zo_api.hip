@@ -104,6 +104,7 @@ size_t zo_workspace_bytes_min(const zo_config* cfg, int32_t N, int32_t B, int32_
 }
 
 int zo_init(const zo_config* cfg, void* theta, uint64_t seed, void* stream) {
+  zo::PhaseRange range("zo_init");
   int st = check_config(cfg);
   if (st) return st;
   if (!theta) return fail(ZO_EINVAL, "theta is NULL");
@@ -117,6 +118,7 @@ static int forward_call(const zo_config* cfg, const void* theta, uint64_t seed, 
                         uint32_t i0, const int32_t* tokens, const uint8_t* mask, int32_t B, int32_t C,
                         float* L1, float* L2, void* workspace, size_t ws_bytes, int32_t products,
                         void* stream, bool fd, const char* name) {
+  zo::PhaseRange range(name);
   int st = check_config(cfg);
   if (st) return st;
   // the bf16 forward walks K in tiles of 64
@@ -229,6 +231,7 @@ int zo_fd_losses_ex(const zo_config* cfg, const void* theta, uint64_t seed, floa
 int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
               uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
               void* stream) {
+  zo::PhaseRange range("zo_update");
   int st = check_config(cfg);
   if (st) return st;
   if (!theta || !Lplus || !Lminus) return fail(ZO_EINVAL, "a required pointer is NULL");
@@ -252,6 +255,7 @@ size_t zo_probe_bits_offset(const zo_config* cfg, int32_t N, int32_t B, int32_t 
 int zo_update_cached(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
                      uint32_t i0, const float* Lplus, const float* Lminus, int32_t* skipped_out,
                      const uint32_t* probe_bits, void* stream) {
+  zo::PhaseRange range("zo_update_cached");
   int st = check_config(cfg);
   if (st) return st;
   if (cfg->probe != ZO_RADEMACHER) return fail(ZO_EINVAL, "zo_update_cached: sign probes only");
@@ -271,6 +275,7 @@ int zo_update_cached(const zo_config* cfg, void* theta, uint64_t seed, float eps
 
 int zo_fd_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float lr, int32_t N,
                  uint32_t i0, const float* L, const float* L0, int32_t* skipped_out, void* stream) {
+  zo::PhaseRange range("zo_fd_update");
   int st = check_config(cfg);
   if (st) return st;
   if (!theta || !L || !L0) return fail(ZO_EINVAL, "a required pointer is NULL");

@@ -1,6 +1,8 @@
 // Event-based kernel timing behind zo_profile_enable / zo_profile_read.
 #include "zo_profile.hpp"
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include <mutex>
 #include <vector>
 
@@ -21,6 +23,9 @@ std::vector<Slot> g_slots;  // event pairs, reused across enable/read cycles
 size_t g_used = 0;
 int64_t g_all[kKClasses] = {};  // launches per class since the last enable
 }  // namespace
+
+PhaseRange::PhaseRange(const char* name) { roctxRangePushA(name); }
+PhaseRange::~PhaseRange() { roctxRangePop(); }
 
 int prof_begin(KernelClass k, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_mu);

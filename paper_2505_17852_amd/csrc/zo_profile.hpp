@@ -33,4 +33,15 @@ struct ProfScope {
   }
 };
 
+// A named phase range for profilers that trace markers (rocprofv3
+// --marker-trace): pushed on construction, popped on destruction, on the
+// calling host thread. The forward's phases and the entry points carry one;
+// without a tracing tool attached a range costs one library call each way.
+struct PhaseRange {
+  explicit PhaseRange(const char* name);
+  ~PhaseRange();
+  PhaseRange(const PhaseRange&) = delete;
+  PhaseRange& operator=(const PhaseRange&) = delete;
+};
+
 }  // namespace zo

@@ -37,7 +37,8 @@ def test_api_host_side_under_asan_and_ubsan(tmp_path):
     run([HIPCC, *common, "-x", "c++", "-I/opt/rocm/include", "-D__HIP_PLATFORM_AMD__", "-c",
          os.path.join(ROOT, "tests", "helpers", "api_sanitize_driver.cpp"), "-o", drv])
     exe = str(tmp_path / "api_sanitize")
-    run([HIPCC, "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", *objs, drv, "-o", exe])
+    run([HIPCC, "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", *objs, drv,
+         "-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib", "-o", exe])
     # leaks: the HIP runtime keeps allocations of its own until exit
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
