@@ -82,9 +82,12 @@ struct Tiles {
   static constexpr int StageBytes = ABytes + (kZTile ? ZTileBytes : 0);
   static constexpr int ACopies = ABytes / 1024 / NWAVES;  // activation copies per wave and tile
   // B fragments for k step s + DIST are loaded at step s, into SLOTS rotating
-  // register sets (the cached probe doubles the loads, so it looks less far
-  // ahead to stay within the registers of two waves per SIMD)
-  static constexpr int DIST = kZDirect ? 1 : 3;
+  // register sets, as far ahead as the registers of two waves per SIMD allow
+  // without spilling (the cached normal probe doubles the loads; regenerated
+  // probes hold the generator's state): cached sign probes 7 k steps (c4 gate
+  // 2.25 -> 2.18 ms against 3), the others 3 (c3 gate 0.90 -> 0.74 ms
+  // against 1).
+  static constexpr int DIST = kBits ? 7 : 3;
   static constexpr int SLOTS = DIST + 1;
   static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
   // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
@@ -93,7 +96,7 @@ struct Tiles {
   static constexpr int WPT = ZVALS / 32;  // sign words (or blocks of 32 normals) per thread and tile
   static_assert(WAVES_M * WAVES_N == NWAVES && WROWS % 32 == 0, "wave grid");
   static_assert(ACopies * NWAVES * 1024 == ABytes, "copy split");
-  static_assert(KSTEPS % SLOTS == 0, "the B slots repeat every tile");
+  static_assert((2 * KSTEPS) % SLOTS == 0 && SLOTS <= 8, "the B slots repeat every two tiles");
   static_assert(ZVALS % 32 == 0 && ZROW_T * TN == NT, "probe roles: whole 32-k sign words per thread");
   static_assert(kRowGranuleBF16 % WROWS == 0, "a wave tile lies inside one sign's rows");
   static_assert(RowBytes == 128, "swizzle of 128-byte rows (act_swizzle)");
@@ -142,6 +145,27 @@ struct Geo {
 };
 
 __device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
+
+// Calls f(integral_constant<int, i>) for a slot index i < N <= 8 known only
+// after unrolling (register arrays need compile-time indices).
+template <int N, typename F>
+__device__ __forceinline__ void with_slot(int i, F&& f) {
+  static_assert(N >= 1 && N <= 8, "slots");
+  auto call = [&](auto tag) {
+    if constexpr (decltype(tag)::value < N) f(tag);
+  };
+  using std::integral_constant;
+  switch (i) {
+    case 0: call(integral_constant<int, 0>{}); break;
+    case 1: call(integral_constant<int, 1>{}); break;
+    case 2: call(integral_constant<int, 2>{}); break;
+    case 3: call(integral_constant<int, 3>{}); break;
+    case 4: call(integral_constant<int, 4>{}); break;
+    case 5: call(integral_constant<int, 5>{}); break;
+    case 6: call(integral_constant<int, 6>{}); break;
+    default: call(integral_constant<int, 7>{}); break;
+  }
+}
 
 // The word of 32 consecutive sign flags with the even elements' flags moved
 // to bits 0..15 and the odd elements' to bits 16..31 (in order), so that the
@@ -457,23 +481,17 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         issue_fence();
       }
       // B fragments DIST steps ahead
-      switch ((s + T::DIST) % T::SLOTS) {
-        case 0: load_b(std::integral_constant<int, 0>{}, it * KSTEPS + s + T::DIST); break;
-        case 1: if constexpr (T::SLOTS > 1) load_b(std::integral_constant<int, 1 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
-        case 2: if constexpr (T::SLOTS > 2) load_b(std::integral_constant<int, 2 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
-        default: if constexpr (T::SLOTS > 3) load_b(std::integral_constant<int, 3 % T::SLOTS>{}, it * KSTEPS + s + T::DIST); break;
-      }
+      with_slot<T::SLOTS>((S * KSTEPS + s + T::DIST) % T::SLOTS, [&](auto slot_tag) { load_b(slot_tag, it * KSTEPS + s + T::DIST); });
       if (s + 1 < KSTEPS) load(s + 1, f[(s + 1) & 1]);
       // this step's weight fragments (slot s % SLOTS) and probe fragments
       h8 w[2], z[2];
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        switch (s % T::SLOTS) {
-          case 0: w[nt] = wfr[0][nt]; if constexpr (T::kZDirect) z[nt] = zfr[0][nt]; break;
-          case 1: w[nt] = wfr[1 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[1 % T::SLOTS][nt]; break;
-          case 2: w[nt] = wfr[2 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[2 % T::SLOTS][nt]; break;
-          default: w[nt] = wfr[3 % T::SLOTS][nt]; if constexpr (T::kZDirect) z[nt] = zfr[3 % T::SLOTS][nt]; break;
-        }
+        with_slot<T::SLOTS>((S * KSTEPS + s) % T::SLOTS, [&](auto slot_tag) {
+          constexpr int SL = decltype(slot_tag)::value;
+          w[nt] = wfr[SL][nt];
+          if constexpr (T::kZDirect) z[nt] = zfr[SL][nt];
+        });
         if constexpr (T::kZTile) z[nt] = c.z[nt];
         if constexpr (T::kSigns) {
           const uint32_t u = us[nt][s >> 1];
@@ -525,9 +543,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   }
   issue_copies(std::integral_constant<int, 0>{});
   issue_fence();
-  if constexpr (T::DIST >= 1) load_b(std::integral_constant<int, 0>{}, 0);
-  if constexpr (T::DIST >= 2) load_b(std::integral_constant<int, 1>{}, 1);
-  if constexpr (T::DIST >= 3) load_b(std::integral_constant<int, 2>{}, 2);
+#pragma unroll
+  for (int g = 0; g < T::DIST; ++g) with_slot<T::SLOTS>(g, [&](auto slot_tag) { load_b(slot_tag, g); });
   issue_probe(std::integral_constant<int, 0>{});
   // loads issued after the copies of the tile a barrier waits for: the first
   // DIST steps' B loads (prologue), then a whole tile's B loads (every later
