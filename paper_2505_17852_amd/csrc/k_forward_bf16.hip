@@ -88,7 +88,7 @@ struct Tiles {
   // 2.25 -> 2.18 ms against 3), the others 3 (c3 gate 0.90 -> 0.74 ms
   // against 1).
   static constexpr int DIST = kBits ? 7 : 3;
-  static constexpr int SLOTS = DIST + 1;
+  static constexpr int SLOTS = DIST < 4 ? 4 : 8;  // a divisor of the two K tiles the loop body spans
   static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
   // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
   static constexpr int ZROW_T = NT / TN;
