@@ -119,10 +119,12 @@ size_t zo_param_count(const zo_config* cfg);
  * batch of B sequences of C positions; 0 if the arguments are invalid.
  * Host only. With bf16 weights every workspace holds an fp16 copy of the
  * weight matrices (every W_ih, W_hh and W_out; P_g values), written once per
- * call. With normal probes this includes the probe cache: N * P_g values of
- * eps z (fp32 weights) or fp16(eps z) (bf16 weights) for the same matrices,
- * written once per call and read by every timestep instead of regenerating
- * the probe in every tile (the results are bit-identical either way). With
+ * call. With normal probes this includes the probe cache, written once per
+ * call and read by every timestep instead of regenerating the probe in every
+ * tile (the results are bit-identical either way): N * P_g values of eps z
+ * for fp32 weights; 2 * N * P_g fp16 values for bf16 weights, each probe's
+ * perturbed weights fp16(w + fp16(eps z)) and fp16(w - fp16(eps z)) (fused
+ * products), or fp16(eps z) (two-stream products). With
  * sign probes and bf16 weights it includes the sign-probe cache (below); with
  * sign probes and fp32 weights it equals zo_workspace_bytes_min. */
 size_t zo_workspace_bytes(const zo_config* cfg, int32_t N, int32_t B, int32_t C);

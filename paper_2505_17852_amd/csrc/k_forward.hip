@@ -704,12 +704,23 @@ __global__ __launch_bounds__(256) void w16_pack_kernel(const uint16_t* theta, ui
 // thread per packed chunk: 8 consecutive elements j (a multiple of 8), two
 // Philox blocks; zeros for the head's padding rows. The values are those the
 // kernels compute when they regenerate the probe.
-__global__ __launch_bounds__(256) void zcache_pack_kernel(uint16_t* zc, PackSegs segs, Key key, uint32_t i0, int N,
-                                                          float eps) {
+// w +- z for two packed fp16 pairs, each rounded once to nearest even (the
+// value the products' fused form computes in registers from w and z).
+__device__ __forceinline__ uint32_t add_f16x2(uint32_t w, uint32_t z, bool minus) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const h2 a = __builtin_bit_cast(h2, w), b = __builtin_bit_cast(h2, z);
+  return __builtin_bit_cast(uint32_t, minus ? a - b : a + b);
+}
+
+// bf16 weights: the probe cache in the packed order of the fp16 weight copy.
+// perturbed = false: probe n's fp16(eps z) at n pg. perturbed = true: probe
+// n's perturbed weights fp16(w + fp16(eps z)) at 2n pg and fp16(w - fp16(eps
+// z)) at (2n + 1) pg, from the packed fp16 weights w16 (written before).
+__global__ __launch_bounds__(256) void zcache_pack_kernel(uint16_t* zc, const uint16_t* w16, PackSegs segs, Key key,
+                                                          uint32_t i0, int N, float eps, bool perturbed) {
   const uint64_t pg = segs.cstart[segs.n];
   const uint64_t nchunks = pg >> 3;
   for (int n = blockIdx.y; n < N; n += gridDim.y) {
-    uint16_t* zp = zc + (uint64_t)n * pg;
     for (uint64_t q = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nchunks;
          q += (uint64_t)gridDim.x * blockDim.x) {
       int m;
@@ -726,7 +737,18 @@ __global__ __launch_bounds__(256) void zcache_pack_kernel(uint16_t* zc, PackSegs
         o[2] = pack_f16x2(fmul(eps, zb[0]), fmul(eps, zb[1]));
         o[3] = pack_f16x2(fmul(eps, zb[2]), fmul(eps, zb[3]));
       }
-      *(uint4*)(zp + (q << 3)) = uint4{o[0], o[1], o[2], o[3]};
+      if (!perturbed) {
+        *(uint4*)(zc + (uint64_t)n * pg + (q << 3)) = uint4{o[0], o[1], o[2], o[3]};
+      } else {
+        // padding rows: w = 0 and z = 0
+        const uint4 w = *(const uint4*)(w16 + (q << 3));
+        *(uint4*)(zc + (uint64_t)(2 * n) * pg + (q << 3)) =
+            uint4{add_f16x2(w.x, o[0], false), add_f16x2(w.y, o[1], false), add_f16x2(w.z, o[2], false),
+                  add_f16x2(w.w, o[3], false)};
+        *(uint4*)(zc + (uint64_t)(2 * n + 1) * pg + (q << 3)) =
+            uint4{add_f16x2(w.x, o[0], true), add_f16x2(w.y, o[1], true), add_f16x2(w.z, o[2], true),
+                  add_f16x2(w.w, o[3], true)};
+      }
     }
   }
 }
@@ -799,7 +821,9 @@ hipError_t launch_zcache_fill(const ForwardArgs& a, hipStream_t st) {
     const PackSegs segs = packed_segments(a);
     uint64_t gx = (a.zmap.pg / 8 + 255) / 256;
     if (gx > 4096) gx = 4096;
-    zcache_pack_kernel<<<dim3((unsigned)gx, gy), 256, 0, st>>>((uint16_t*)a.zc, segs, key, a.i0, a.rows.N, a.eps);
+    // fused products read the perturbed weights; two-stream ones fp16(eps z)
+    zcache_pack_kernel<<<dim3((unsigned)gx, gy), 256, 0, st>>>((uint16_t*)a.zc, (const uint16_t*)a.w16, segs, key,
+                                                                a.i0, a.rows.N, a.eps, !a.split);
   } else {
     const ZSegs segs = matrix_segments(a);
     uint64_t gx = (a.zmap.pg / 4 + 255) / 256;

@@ -87,7 +87,8 @@ struct Tiles {
   // probes hold the generator's state): cached sign probes 7 k steps (c4 gate
   // 2.25 -> 2.18 ms against 3), the others 3 (c3 gate 0.90 -> 0.74 ms
   // against 1).
-  static constexpr int DIST = kBits ? 7 : 3;
+  static constexpr bool kPerturbed = kind == kGaussPerturbed;  // B is the cached fp16(W + s eps z) itself
+  static constexpr int DIST = kBits || kPerturbed ? 7 : 3;
   static constexpr int SLOTS = DIST < 4 ? 4 : 8;  // a divisor of the two K tiles the loop body spans
   static constexpr int LoadsPerStep = kZDirect ? 4 : 2;
   // probe-tile roles: thread t forms ZVALS consecutive k of column t / ZROW_T
@@ -265,6 +266,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
                                               int nseg, int64_t cb0, ColMap colmap, Key key, uint32_t probe,
                                               int sgn, float eps, uint16_t eps_b, const BitsB bits) {
   using T = Tiles<kind>;
+  static_assert(!(kSplit && T::kPerturbed), "the perturbed-weight cache holds the fused form only");
   constexpr int MT = T::MT;
   constexpr int TK = T::TK;
   constexpr int KSTEPS = T::KSTEPS;
@@ -522,8 +524,12 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         // one rounding to nearest even), then one MFMA per accumulator
         h8 wz[2];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          wz[nt] = T::kSigns ? w[nt] + z[nt] : __builtin_elementwise_fma(z[nt], s8, w[nt]);
+        for (int nt = 0; nt < 2; ++nt) {
+          if constexpr (T::kPerturbed)
+            wz[nt] = w[nt];  // formed once per call by the cache fill, the same value bit for bit
+          else
+            wz[nt] = T::kSigns ? w[nt] + z[nt] : __builtin_elementwise_fma(z[nt], s8, w[nt]);
+        }
         mma(wz);
       }
       if (s == 2) issue_probe(next);
@@ -654,10 +660,15 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
   f16v acc[G::MT][G::NTW];
   zero_acc(acc);
   const uint64_t zpos = (uint64_t)pair * g.zc_stride;
-  const SegB s0{g.x + m0 * g.El, g.El, g.w_ih16, (uint32_t)((uint64_t)4 * H * g.El * 2), g.off_ih, g.El, g.El,
-                kind == kGaussCached ? g.zc_ih + zpos : nullptr};
-  const SegB s1{g.hprev + m0 * H, H, g.w_hh16, (uint32_t)((uint64_t)4 * H * H * 2), g.off_hh, H, H,
-                kind == kGaussCached ? g.zc_hh + zpos : nullptr};
+  // kGaussPerturbed: this wave's B operand is its pass's perturbed weights
+  // (block 2 pair for +eps, 2 pair + 1 for -eps), or the plain weights for the
+  // clean pass of forward differences
+  const uint64_t ppos = (uint64_t)(2 * pair + (sgn < 0 ? 1 : 0)) * g.zc_stride;
+  const bool pert = kind == kGaussPerturbed && sgn != 0;
+  const SegB s0{g.x + m0 * g.El, g.El, pert ? g.zc_ih + ppos : g.w_ih16, (uint32_t)((uint64_t)4 * H * g.El * 2),
+                g.off_ih, g.El, g.El, kind == kGaussCached ? g.zc_ih + zpos : nullptr};
+  const SegB s1{g.hprev + m0 * H, H, pert ? g.zc_hh + ppos : g.w_hh16, (uint32_t)((uint64_t)4 * H * H * 2), g.off_hh,
+                H, H, kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
   mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, (TN / kPackBlockCols) * (int64_t)nb, colmap, g.key,
@@ -753,7 +764,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   auto colmap = [&](int rho, int& n) { n = min(v0 + rho, V - 1); };
   f16v acc[G::MT][NTW];
   zero_acc(acc);
-  const SegB s0{g.h + rr0 * g.H, g.H, g.w_out16, (uint32_t)((uint64_t)g.nvt * TN * g.H * 2), g.off_w, g.H, g.H,
+  const bool pert = kind == kGaussPerturbed && sgn != 0;  // as in the gate kernel
+  const uint64_t ppos = (uint64_t)(2 * pair + (sgn < 0 ? 1 : 0)) * g.zc_stride;
+  const SegB s0{g.h + rr0 * g.H, g.H, pert ? g.zc_out + ppos : g.w_out16,
+                (uint32_t)((uint64_t)g.nvt * TN * g.H * 2), g.off_w, g.H, g.H,
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
@@ -930,6 +944,11 @@ void dispatch_bf16(const ForwardArgs& a, Go&& go) {
   };
   if (a.cfg.probe == ZO_RADEMACHER && a.bits) by_fd(integral_constant<int, kSignsCached>{});
   else if (a.cfg.probe == ZO_RADEMACHER) by_fd(integral_constant<int, ZO_RADEMACHER>{});
+  else if (a.zc && !a.split) {
+    // perturbed weights hold the fused form only
+    if (a.rows.fd) go(integral_constant<int, kGaussPerturbed>{}, integral_constant<bool, true>{}, integral_constant<bool, false>{});
+    else go(integral_constant<int, kGaussPerturbed>{}, integral_constant<bool, false>{}, integral_constant<bool, false>{});
+  }
   else if (a.zc) by_fd(integral_constant<int, kGaussCached>{});
   else by_fd(integral_constant<int, ZO_GAUSSIAN>{});
 }

@@ -176,11 +176,14 @@ inline bool probe_cache_kind(const zo_config& c) { return c.probe == ZO_GAUSSIAN
 inline bool bit_cache_kind(const zo_config& c) { return c.probe == ZO_RADEMACHER && c.wdtype == ZO_WBF16; }
 __host__ __device__ inline uint64_t bit_words(uint64_t P) { return (P + 127) / 128 * 4; }
 
-// Kernel variants for normal probes read from the probe cache and for sign
-// probes read from the sign-probe cache (next to the probe kinds ZO_RADEMACHER
-// and ZO_GAUSSIAN, which regenerate them).
+// Kernel variants for normal probes read from the probe cache (fp16(eps z)
+// as a second operand stream; or, bf16 weights with fused products, the
+// perturbed weights fp16(w +- fp16(eps z)) as the B operand itself) and for
+// sign probes read from the sign-probe cache (next to the probe kinds
+// ZO_RADEMACHER and ZO_GAUSSIAN, which regenerate them).
 constexpr int kGaussCached = 2;
 constexpr int kSignsCached = 3;
+constexpr int kGaussPerturbed = 4;
 
 // Workspace plan (byte offsets from the workspace base, 256-aligned).
 struct WsPlan {
@@ -196,7 +199,10 @@ struct WsPlan {
   size_t row_loss;   // f64 [M]            masked loss sum of each row
   size_t w16;        // f16 [P_g]          bf16 weights: the product matrices in fp16 (ZCacheMap layout)
   size_t min_total;  // bytes without the probe cache
-  size_t zcache;     // probe cache [N][P_g] (normal probes; see ZCacheMap)
+  size_t zcache;     // probe cache (normal probes; see ZCacheMap): fp32 weights [N][P_g] eps z;
+                     // bf16 weights [N][2][P_g] fp16: probe n's perturbed weights
+                     // fp16(w + fp16(eps z)) and fp16(w - fp16(eps z)) (fused products), or
+                     // fp16(eps z) in the first N P_g values (two-stream products)
   size_t bits;       // sign-probe cache [N][bit_words(P)] u32 (bf16 weights with sign probes)
   size_t total;      // bytes with the probe cache
   int nvt;           // vocabulary tiles
@@ -232,7 +238,7 @@ inline WsPlan plan_workspace(const zo_config& c, const Rows& r, int32_t C) {
   if (c.wdtype == ZO_WBF16) take((size_t)make_zcache_map(c).pg * 2);
   w.min_total = p;
   w.zcache = p;
-  if (probe_cache_kind(c)) take((size_t)r.N * make_zcache_map(c).pg * (c.wdtype == ZO_WBF16 ? 2 : 4));
+  if (probe_cache_kind(c)) take((size_t)r.N * make_zcache_map(c).pg * (c.wdtype == ZO_WBF16 ? 2 * 2 : 4));
   w.bits = p;
   if (bit_cache_kind(c)) take((size_t)r.N * bit_words(make_layout(c).total) * 4);
   w.total = p;

@@ -73,7 +73,8 @@ def test_workspace_probe_cache_size(zo, name):
     """Normal probes: the preferred workspace adds exactly the probe cache,
     N values of the weight matrices' size in the weight type (rounded up to
     the 256-byte allocation granule; with bf16 weights the head matrix is
-    stored padded to whole 256-wide vocabulary tiles); sign probes with bf16
+    stored padded to whole 256-wide vocabulary tiles, and each probe has two
+    blocks: its perturbed weights for +eps and -eps); sign probes with bf16
     weights add the sign-probe cache, with fp32 weights nothing."""
     w = wl.CONFIGS[name]
     cfg = wl.model_cfg(name)
@@ -84,7 +85,7 @@ def test_workspace_probe_cache_size(zo, name):
         # bf16: the head matrix is stored padded to whole 256-wide vocabulary tiles
         Vs = (V + 255) // 256 * 256 if cfg["wdtype"] == wl.BF16 else V
         pg = sum(4 * H * ((E if l == 0 else H) + H) for l in range(L)) + Vs * H
-        el = 2 if cfg["wdtype"] == wl.BF16 else 4
+        el = 2 * 2 if cfg["wdtype"] == wl.BF16 else 4
         assert full - small == (w["N"] * pg * el + 255) // 256 * 256
     elif cfg["wdtype"] == wl.BF16:
         # sign probes with bf16 weights: the sign-probe cache, N words of 32 signs per 32 parameters
