@@ -12,10 +12,10 @@
 //     acc += A . fp16(W + s eps z)
 // whose B fragment each wave forms in registers from the fp16 weight fragment
 // and the probe fragment with one packed fp16 add per pair (+-fp16(eps) for
-// sign probes, expanded from bits; fp16(eps z), sign-flipped for -eps rows,
-// for normal probes). theta +- eps z is never formed in memory. For small eps
-// the two-stream form acc += A . W; acc += A . (s eps z) is used instead
-// (kSplit).
+// sign probes, expanded from bits), or loads ready-formed (normal probes: the
+// probe cache's perturbed weights, the same values). The parameter vector
+// theta +- eps z is never formed. For small eps the two-stream form
+// acc += A . W; acc += A . (s eps z) is used instead (kSplit).
 //
 // Tiles: a workgroup of 8 waves computes TM rows x TN columns, TM x TN =
 // 65536 (TN = kVocabTileWide: 128 x 512, or 256 x 256); its waves split the
@@ -38,8 +38,10 @@
 // two words of sign flags per column and K tile (regenerated, one Philox word
 // per 32 k, or read from the sign-probe cache) in a small LDS array of their
 // own, which every lane expands into +-fp16(eps) fragments in registers;
-// normal probes either regenerated into an LDS tile per K tile or loaded like
-// the weights from the probe cache.
+// normal probes regenerated into an LDS tile per K tile, or read from the
+// probe cache: with the fused form as the pass's perturbed weights
+// fp16(W + s eps z), written once per call and loaded as the only B operand,
+// with the two-stream form as fp16(eps z) loaded beside the weights.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
