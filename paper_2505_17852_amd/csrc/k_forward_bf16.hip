@@ -319,18 +319,37 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // waits for each fragment with an exact count, and wait_and_barrier's counts
   // hold.
   h8 wfr[T::SLOTS][2], zfr[T::kZDirect ? T::SLOTS : 1][2];
-  // k step gs (global over both segments) -> segment and k step inside it
-  auto load_b = [&](auto slot_tag, int gs) {
-    constexpr int SL = decltype(slot_tag)::value;
-    gs = gs < nsteps ? gs : nsteps - 1;
-    const bool second = gs >= ks0;
-    const uint32_t ks = (uint32_t)(second ? gs - ks0 : gs);
+  // The B loads of K tile ti: the segment's resources and the scalar offsets
+  // of the tile's first k step in the wave's two column blocks, worked out
+  // once per tile (k step p of the tile adds p kPackBlockBytes). Past the
+  // last tile the loads repeat
+  // the last tile (their values are never used).
+  struct TileB {
+    Rsrc rw, rz;
+    uint32_t off[2];
+  };
+  const int ntiles0 = s0.K / TK;
+  auto tile_b = [&](int ti) {
+    ti = ti < ntiles ? ti : ntiles - 1;
+    const bool second = ti >= ntiles0;
+    const uint32_t kt = (uint32_t)(second ? ti - ntiles0 : ti);
     const uint32_t KS = (uint32_t)(second ? s1.K : s0.K) / 16u;
+    TileB b;
+    b.rw = second ? rw1 : rw0;
+    b.rz = second ? rz1 : rz0;
+    b.off[0] = ((uint32_t)cbw * KS + kt * (uint32_t)KSTEPS) * (uint32_t)kPackBlockBytes;
+    b.off[1] = b.off[0] + KS * (uint32_t)kPackBlockBytes;
+    return b;
+  };
+  // k step P of the tile b into slot SL
+  auto load_b = [&](auto slot_tag, auto step_tag, const TileB& b) {
+    constexpr int SL = decltype(slot_tag)::value;
+    constexpr uint32_t P = decltype(step_tag)::value;
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      const uint32_t soff = ((uint32_t)(cbw + nt) * KS + ks) * (uint32_t)kPackBlockBytes;
-      wfr[SL][nt] = load_frag(second ? rw1 : rw0, blane, soff);
-      if constexpr (T::kZDirect) zfr[SL][nt] = load_frag(second ? rz1 : rz0, blane, soff);
+      const uint32_t soff = b.off[nt] + P * (uint32_t)kPackBlockBytes;
+      wfr[SL][nt] = load_frag(b.rw, blane, soff);
+      if constexpr (T::kZDirect) zfr[SL][nt] = load_frag(b.rz, blane, soff);
     }
   };
 
@@ -445,12 +464,17 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   struct Frag {
     h8 a[MT], z[2];
   };
+  constexpr int kQ0 = T::DIST / KSTEPS, kQ1 = (KSTEPS - 1 + T::DIST) / KSTEPS;
   auto compute = [&](auto stage_tag, int it) {
     constexpr int S = decltype(stage_tag)::value;
     constexpr std::integral_constant<int, 1 - S> next{};
     const uint8_t* base = stage<kind, S>();
     const uint8_t* pa = base + a_lane;
     const uint8_t* pz = base + T::ABytes + z_lane;
+    // the B tiles this tile's steps load from: it + kQ0 .. it + kQ1
+    TileB tb[kQ1 - kQ0 + 1];
+#pragma unroll
+    for (int q = 0; q <= kQ1 - kQ0; ++q) tb[q] = tile_b(it + kQ0 + q);
     uint32_t us[2][2] = {};
     if constexpr (T::kSigns) {
 #pragma unroll
@@ -484,8 +508,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         issue_copies(next);
         issue_fence();
       }
-      // B fragments DIST steps ahead
-      with_slot<T::SLOTS>((S * KSTEPS + s + T::DIST) % T::SLOTS, [&](auto slot_tag) { load_b(slot_tag, it * KSTEPS + s + T::DIST); });
+      // B fragments DIST steps ahead: k step (s + DIST) % KSTEPS of tile
+      // it + (s + DIST) / KSTEPS
+      with_slot<T::SLOTS>((S * KSTEPS + s + T::DIST) % T::SLOTS, [&](auto slot_tag) {
+        with_slot<KSTEPS>((s + T::DIST) % KSTEPS, [&](auto step_tag) {
+          load_b(slot_tag, step_tag, tb[(s + T::DIST) / KSTEPS - kQ0]);
+        });
+      });
       if (s + 1 < KSTEPS) load(s + 1, f[(s + 1) & 1]);
       // this step's weight fragments (slot s % SLOTS) and probe fragments
       h8 w[2], z[2];
@@ -551,8 +580,16 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   }
   issue_copies(std::integral_constant<int, 0>{});
   issue_fence();
+  {
+    TileB tb0[(T::DIST - 1) / KSTEPS + 1];
 #pragma unroll
-  for (int g = 0; g < T::DIST; ++g) with_slot<T::SLOTS>(g, [&](auto slot_tag) { load_b(slot_tag, g); });
+    for (int q = 0; q <= (T::DIST - 1) / KSTEPS; ++q) tb0[q] = tile_b(q);
+#pragma unroll
+    for (int g = 0; g < T::DIST; ++g)
+      with_slot<T::SLOTS>(g, [&](auto slot_tag) {
+        with_slot<KSTEPS>(g % KSTEPS, [&](auto step_tag) { load_b(slot_tag, step_tag, tb0[g / KSTEPS]); });
+      });
+  }
   issue_probe(std::integral_constant<int, 0>{});
   // loads issued after the copies of the tile a barrier waits for: the first
   // DIST steps' B loads (prologue), then a whole tile's B loads (every later
