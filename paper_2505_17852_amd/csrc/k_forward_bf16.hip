@@ -793,6 +793,16 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   const int lr = lane & 31, lg = lane >> 5;
   int mb, vt;
   tile_of(blockIdx.x, (int)(g.rows / TM), g.nvt, mb, vt);
+  if constexpr (kind == kGaussPerturbed || kind == kGaussCached) {
+    // Normal-probe caches: the weight operand differs per pass (or probe),
+    // so the row blocks tile_of groups on one XCD are taken as one pass
+    // block's consecutive timesteps (the order's block mb is timestep
+    // mb % Tc of pass block mb / Tc), which then share each cached W_out
+    // tile instead of each reading its own. Any order is correct.
+    const int per_t = (int)(g.M / TM), Tc = (int)(g.rows / g.M);
+    const int pb = mb / Tc, ts = mb - pb * Tc;
+    mb = ts * per_t + pb;
+  }
   const int v0 = vt * TN;
   const int64_t rr0 = (int64_t)mb * TM;
   const int tt = (int)(rr0 / g.M);
