@@ -124,6 +124,17 @@ constexpr int kWordBytes = kVocabTileWide * 2 * 4;
 __shared__ __align__(16) uint8_t lds_words0[kWordBytes];
 __shared__ __align__(16) uint8_t lds_words1[kWordBytes];
 
+// The head's bias values of its vocabulary tile, fetched before the main
+// loop so that the epilogue finds them in LDS: 256 words of theta from the
+// 4-byte boundary at or below the tile's first bias element (raw bf16), and
+// the 256 bias-probe values eps z of the tile's columns.
+__shared__ __align__(16) uint8_t lds_hbias[1024];
+__shared__ __align__(16) float lds_hzbo[kVocabTileWide];
+// bias + s eps z of each column for the rows of each sign (-inf past V)
+__shared__ __align__(16) float lds_hadd[2][kVocabTileWide];
+// the target token of each row of the head's tile (-1 for padding rows)
+__shared__ __align__(16) int lds_htgt[TM];
+
 template <int kind, int S>
 __device__ __forceinline__ uint8_t* stage() {
   static_assert(S == 0 || S == 1, "stage index");
@@ -189,6 +200,12 @@ __device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
 // A raw buffer resource over [base, base + bytes), bytes < 2^31.
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// 4 bytes per lane from global memory straight into LDS: lane L's word at
+// lds + 4 L (lds wave-uniform); reads past the resource give zeros.
+__device__ __forceinline__ void copy4_to_lds(Rsrc r, uint32_t voff, uint8_t* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 4, voff, 0, 0, 0);
 }
 
 // 16 bytes per lane from global memory straight into LDS: the wave's 64
@@ -820,6 +837,29 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
                 kind == kGaussCached ? g.zc_out + (uint64_t)pair * g.zc_stride : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
+  // the tile's bias values into LDS (waves 0-3: eps z of the bias, one column
+  // per lane; waves 4-7: the bf16 bias as 4-byte words from the aligned
+  // boundary; columns past V read zeros). Issued before the loop's first
+  // loads: its first barrier waits for them.
+  const uintptr_t bias_at = (uintptr_t)(g.theta + g.off_b);
+  const uint32_t bias_lead = (uint32_t)(bias_at & 3u);  // 0 or 2 bytes before the first element
+  {
+    const int q = __builtin_amdgcn_readfirstlane(wave);
+    if (q < 4) {
+      const Rsrc rz = make_rsrc(g.zbo + (int64_t)pair * V, (uint32_t)V * 4u);
+      copy4_to_lds(rz, 4u * (uint32_t)(v0 + 64 * q + lane), (uint8_t*)lds_hzbo + 256 * q);
+    } else {
+      const Rsrc rb = make_rsrc((const void*)(bias_at - bias_lead), (bias_lead + 2u * (uint32_t)V + 3u) & ~3u);
+      copy4_to_lds(rb, 2u * (uint32_t)v0 + 4u * (uint32_t)(64 * (q - 4) + lane), lds_hbias + 256 * (q - 4));
+    }
+  }
+  // the target token of tile row t (threads t < TM), read before the loop
+  // and held in a register through it
+  int tgt_tok = -1;
+  if (t < TM) {
+    const int b = pass_of(g.rm, r0 + t).b;
+    if (b < g.B) tgt_tok = g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1];
+  }
   mainloop_bf16<kind, true, kSplit>(acc, s0, s0, 1, (TN / kPackBlockCols) * (int64_t)vt, colmap, g.key,
                                     g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b, bits);
 
@@ -827,20 +867,28 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   // WROWS wm + 32 mt + lr and vocabulary column cbase + 32 nt + vcol(v)
   const int cbase = v0 + G::WCOLS * wn;
   auto vcol = [&](int v) { return 8 * (v >> 2) + 4 * lg + (v & 3); };
-  // bias and bias probe of each column held (-inf past the vocabulary)
+  // bias + s eps z of the tile's columns for the rows of each wave row
+  // (thread t: wave row t / TN, column t % TN), then per lane the columns it
+  // holds, four consecutive ones per read (-inf past the vocabulary)
+  static_assert(NT == G::WAVES_M * TN && G::WAVES_M == 2, "one thread per wave row and column");
+  {
+    const int c = t % TN, half = t / TN;
+    const int sg = pass_of(g.rm, r0 + G::WROWS * half).sign;
+    const float b = bf16_to_f32(*(const uint16_t*)(lds_hbias + bias_lead + 2 * c));
+    lds_hadd[half][c] = v0 + c < V ? b + (float)sg * lds_hzbo[c] : -INFINITY;
+    if (t < TM) lds_htgt[t] = tgt_tok;
+  }
+  __syncthreads();
   float add[NTW][16];
 #pragma unroll
   for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int col = cbase + 32 * nt + vcol(v);
-      float a = -INFINITY;
-      if (col < V) {
-        const float b = bf16_to_f32(g.theta[g.off_b + (uint64_t)col]);
-        const float z = g.zbo[(int64_t)pair * V + col];
-        a = b + (float)sgn * z;
-      }
-      add[nt][v] = a;
+    for (int j = 0; j < 4; ++j) {
+      const float4 a4 = *(const float4*)&lds_hadd[wm][G::WCOLS * wn + 32 * nt + vcol(4 * j)];
+      add[nt][4 * j] = a4.x;
+      add[nt][4 * j + 1] = a4.y;
+      add[nt][4 * j + 2] = a4.z;
+      add[nt][4 * j + 3] = a4.w;
     }
   }
   // cross-wave reduction in the first stage buffer (free after the loop)
@@ -849,8 +897,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
 #pragma unroll
   for (int mt = 0; mt < G::MT; ++mt) {
     const int lrow = G::WROWS * wm + 32 * mt + lr;
-    const int b = pass_of(g.rm, r0 + lrow).b;
-    const int tgt = b < g.B ? g.tokens[(int64_t)b * (g.C + 1) + g.t0 + tt + 1] - cbase : -1;
+    const int tgt = lds_htgt[lrow] - cbase;  // negative (never a held column) for padding rows
     float mx = -INFINITY, yt = 0.f;
     bool has_t = false;
 #pragma unroll
