@@ -124,6 +124,14 @@ constexpr int kWordBytes = kVocabTileWide * 2 * 4;
 __shared__ __align__(16) uint8_t lds_words0[kWordBytes];
 __shared__ __align__(16) uint8_t lds_words1[kWordBytes];
 
+// The gate's cell states c of its tile (TM rows x the TN / 4 hidden units of
+// its columns, row-major), fetched before the main loop so that the cell
+// update reads them from LDS; kinds whose stages leave room for it (not the
+// regenerated normal probes' activation + probe stages).
+constexpr int kCellCols = kVocabTileWide / 4;
+__shared__ __align__(16) float lds_gc[TM * kCellCols];
+static_assert(2 * sizeof(lds_c0) + 2 * kWordBytes + sizeof(lds_gc) <= 160 * 1024, "LDS");
+
 // The head's bias values of its vocabulary tile, fetched before the main
 // loop so that the epilogue finds them in LDS: 256 words of theta from the
 // 4-byte boundary at or below the tile's first bias element (raw bf16), and
@@ -727,6 +735,22 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
                 H, H, kind == kGaussCached ? g.zc_hh + zpos : nullptr};
   const BitsB bits{kind == kSignsCached ? g.bits + (uint64_t)pair * g.bits_stride : nullptr,
                    (uint32_t)(g.bits_stride * 4)};
+  constexpr bool kCellLds = !Tiles<kind>::kZTile;
+  if constexpr (kCellLds) {
+    // the tile's cell states into LDS: 1 KB copies of 4 rows (16 lanes of 16
+    // bytes per row), copy j of wave w is copy 8 j + w of the 64; issued
+    // before the loop's first loads, so its first barrier waits for them
+    static_assert(TM * kCellCols * 4 == 64 * 1024 && kCellCols == 64, "cell tile copies");
+    const Rsrc rc = make_rsrc(g.cst + m0 * H, (uint32_t)TM * (uint32_t)H * 4u);
+    const int w = __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int cp = 8 * j + w;
+      const uint32_t row = (uint32_t)(4 * cp + (lane >> 4));
+      copy_to_lds(rc, (row * (uint32_t)H + (uint32_t)u0) * 4u + 16u * (uint32_t)(lane & 15), 0u,
+                  (uint8_t*)lds_gc + 1024 * cp);
+    }
+  }
   mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, (TN / kPackBlockCols) * (int64_t)nb, colmap, g.key,
                                      g.i0 + (uint32_t)pair, sgn, g.eps, g.eps_b, bits);
 
@@ -766,7 +790,8 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
         const float gp = hi ? got[1] : mine[1], op = hi ? mine[1] : got[1];
         const int lrow = acc_row(wm, mt, lg, v + hi);
         const int64_t o = (m0 + lrow) * H + u[p];
-        const float c = sigm(fp) * g.cst[o] + sigm(ip) * tanh_(gp);
+        const float cprev = kCellLds ? lds_gc[lrow * kCellCols + (u[p] - u0)] : g.cst[o];
+        const float c = sigm(fp) * cprev + sigm(ip) * tanh_(gp);
         g.cst[o] = c;
         g.hout[o] = f16_bits(sigm(op) * tanh_(c));
       }
