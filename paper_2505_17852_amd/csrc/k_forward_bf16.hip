@@ -923,8 +923,7 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   for (int mt = 0; mt < G::MT; ++mt) {
     const int lrow = G::WROWS * wm + 32 * mt + lr;
     const int tgt = lds_htgt[lrow] - cbase;  // negative (never a held column) for padding rows
-    float mx = -INFINITY, yt = 0.f;
-    bool has_t = false;
+    float mx = -INFINITY;
 #pragma unroll
     for (int nt = 0; nt < NTW; ++nt) {
 #pragma unroll
@@ -932,20 +931,32 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
         const float y = acc[mt][nt][v] + add[nt][v];
         acc[mt][nt][v] = y;
         mx = fmaxf(mx, y);
-        const bool hit = tgt == 32 * nt + vcol(v);
-        yt = hit ? y : yt;
-        has_t = has_t || hit;
       }
     }
-    if (has_t) g.ptgt[rr0 + lrow] = yt;
-    // the row's WCOLS columns of this wave: half here, half in lane lr + 32
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float se = 0.f;
-    if (mx != -INFINITY) {
+    // the target logit, where a lane of the wave holds its row's target
+    // column (lane group lg holds the columns with bit 2 equal to lg); the
+    // rest of the time the wave skips the search
+    const bool holds_t = (unsigned)tgt < (unsigned)G::WCOLS && ((tgt >> 2) & 1) == lg;
+    if (__builtin_amdgcn_ballot_w64(holds_t) != 0) {
+      float yt = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTW; ++nt)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) se += __expf(acc[mt][nt][v] - mx);
+        for (int v = 0; v < 16; ++v) yt = tgt == 32 * nt + vcol(v) ? acc[mt][nt][v] : yt;
+      if (holds_t) g.ptgt[rr0 + lrow] = yt;
+    }
+    // the row's WCOLS columns of this wave: half here, half in lane lr + 32
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    // sum of exp(y - mx) as 2^(y log2(e) - mx log2(e)) (one fma and one
+    // v_exp_f32 per column)
+    constexpr float kLog2e = 1.4426950408889634f;
+    float se = 0.f;
+    if (mx != -INFINITY) {
+      const float mxl = mx * kLog2e;
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) se += __builtin_amdgcn_exp2f(fmaf(acc[mt][nt][v], kLog2e, -mxl));
     }
     se += __shfl_xor(se, 32, 64);
     if (lg == 0) {
