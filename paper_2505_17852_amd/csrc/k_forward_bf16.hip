@@ -746,9 +746,7 @@ __global__ __launch_bounds__(NT, 1) void gate_bf16_kernel(GateArgsB g) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int cp = 8 * j + w;
-      const uint32_t row = (uint32_t)(4 * cp + (lane >> 4));
-      copy_to_lds(rc, (row * (uint32_t)H + (uint32_t)u0) * 4u + 16u * (uint32_t)(lane & 15), 0u,
-                  (uint8_t*)lds_gc + 1024 * cp);
+      copy_to_lds(rc, cell_copy_offset(cp, lane, H, u0), 0u, (uint8_t*)lds_gc + 1024 * cp);
     }
   }
   mainloop_bf16<kind, false, kSplit>(acc, s0, s1, 2, (TN / kPackBlockCols) * (int64_t)nb, colmap, g.key,
@@ -872,10 +870,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
     const int q = __builtin_amdgcn_readfirstlane(wave);
     if (q < 4) {
       const Rsrc rz = make_rsrc(g.zbo + (int64_t)pair * V, (uint32_t)V * 4u);
-      copy4_to_lds(rz, 4u * (uint32_t)(v0 + 64 * q + lane), (uint8_t*)lds_hzbo + 256 * q);
+      copy4_to_lds(rz, head_probe_offset(v0, q, lane), (uint8_t*)lds_hzbo + 256 * q);
     } else {
-      const Rsrc rb = make_rsrc((const void*)(bias_at - bias_lead), (bias_lead + 2u * (uint32_t)V + 3u) & ~3u);
-      copy4_to_lds(rb, 2u * (uint32_t)v0 + 4u * (uint32_t)(64 * (q - 4) + lane), lds_hbias + 256 * (q - 4));
+      const Rsrc rb = make_rsrc((const void*)(bias_at - bias_lead), head_bias_bytes(bias_lead, V));
+      copy4_to_lds(rb, head_bias_word_offset(v0, 64 * (q - 4) + lane), lds_hbias + 256 * (q - 4));
     }
   }
   // the target token of tile row t (threads t < TM), read before the loop

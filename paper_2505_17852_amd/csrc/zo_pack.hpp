@@ -83,4 +83,30 @@ __host__ __device__ inline uint64_t act_copy_offset(int q, int w, int lane, int 
 // sign of parameter j (32 per word).
 __host__ __device__ inline uint32_t sign_word_offset(uint64_t j) { return (uint32_t)(j >> 5) * 4u; }
 
+// The gate's cell-state tile (the workgroup's 256 rows x 64 hidden units,
+// fp32, row stride H in global memory, 256 bytes per row in LDS): 64 copies
+// of 1 KB, 4 rows each; lane L of copy cp writes row 4 cp + L / 16, units
+// u0 + 4 (L % 16) .. + 3, at LDS byte 1024 cp + 16 L. Byte offset from the
+// tile's first row:
+__host__ __device__ inline int cell_row_of_copy(int cp, int lane) { return 4 * cp + (lane >> 4); }
+__host__ __device__ inline uint32_t cell_copy_offset(int cp, int lane, int64_t H, int64_t u0) {
+  return ((uint32_t)cell_row_of_copy(cp, lane) * (uint32_t)H + (uint32_t)u0) * 4u + 16u * (uint32_t)(lane & 15);
+}
+
+// The head's bias values of vocabulary tile v0 .. v0 + 255: the bias probe
+// values (fp32) one column per lane, lane L of copy q < 4 reading column
+// v0 + 64 q + L; the bf16 bias as 4-byte words from the 4-byte boundary at
+// or below its first element (lead: 0 or 2 bytes before it), word d < 256 of
+// the tile at this offset from that boundary. Column c's bias is then at
+// byte lead + 2 (c - v0) of the tile's words.
+__host__ __device__ inline uint32_t head_probe_offset(int64_t v0, int q, int lane) {
+  return 4u * (uint32_t)(v0 + 64 * q + lane);
+}
+__host__ __device__ inline uint32_t head_bias_word_offset(int64_t v0, int d) {
+  return 2u * (uint32_t)v0 + 4u * (uint32_t)d;
+}
+__host__ __device__ inline uint32_t head_bias_bytes(uint32_t lead, int64_t V) {
+  return (lead + 2u * (uint32_t)V + 3u) & ~3u;
+}
+
 }  // namespace zo

@@ -2,7 +2,8 @@
 // functions the kernels call): for one model shape and batch, every
 // workgroup, wave, lane, copy and k step of the gate and head launches, it
 // checks that
-// each activation copy, packed B-fragment load and sign-probe cache load lies
+// each activation copy, packed B-fragment load, sign-probe cache load, cell
+// state copy and head bias copy lies
 // inside the buffer resource it is issued against (and inside the tensor that
 // resource covers), that every offset fits in 32 bits, that the copies fill
 // each LDS row and slot of a tile exactly once with the chunk the swizzle
@@ -94,6 +95,62 @@ static void check_b_loads(int64_t nb, int64_t cols, int64_t K, const char* what)
         }
 }
 
+// the gate's cell-state copies of column block nb (hidden units u0 = 64 nb
+// .. + 63) against the resource of the tile's 256 rows of H fp32: inside it,
+// and each LDS row (256 bytes) and 16-byte slot written once, with the units
+// it must hold
+static void check_cell_copies(int64_t nb, int64_t H) {
+  const uint64_t records = (uint64_t)TM * (uint64_t)H * 4u;
+  CHECK(records < (1ull << 31), "cell tile resource of %llu bytes", (unsigned long long)records);
+  const int64_t u0 = (TN / 4) * nb;
+  CHECK(u0 + TN / 4 <= H, "cell tile units %lld.. of %lld", (long long)u0, (long long)H);
+  std::vector<int> seen(TM * 16, 0);
+  for (int cp = 0; cp < 64; ++cp)
+    for (int lane = 0; lane < 64; ++lane) {
+      const int row = cell_row_of_copy(cp, lane);
+      const uint64_t off = cell_copy_offset(cp, lane, H, u0);
+      CHECK(row >= 0 && row < TM, "cell copy row %d", row);
+      CHECK(off + 16 <= records, "cell copy offset %llu of %llu", (unsigned long long)off, (unsigned long long)records);
+      CHECK(off == ((uint64_t)row * H + u0 + 4 * (lane & 15)) * 4, "cell copy %d lane %d offset", cp, lane);
+      const int lds = 1024 * cp + 16 * lane;  // LDS byte this lane writes
+      CHECK(lds == row * 256 + 16 * (lane & 15), "cell copy %d lane %d LDS byte %d", cp, lane, lds);
+      if (row >= 0 && row < TM) seen[row * 16 + (lane & 15)] += 1;
+    }
+  for (int i = 0; i < TM * 16; ++i) CHECK(seen[i] == 1, "cell LDS row %d slot %d written %d times", i / 16, i % 16, seen[i]);
+}
+
+// the head's bias copies of vocabulary tile vt: the probe values (one column
+// per lane, past V reading zeros) and the bias words from the 4-byte boundary
+// (lead 0 or 2 bytes), every column of the tile inside V covered and inside
+// the resource, the epilogue's 2-byte reads inside the 1 KB of words
+static void check_head_bias(int64_t vt, int64_t V) {
+  const int64_t v0 = vt * TN;
+  for (int q = 0; q < 4; ++q)
+    for (int lane = 0; lane < 64; ++lane) {
+      const uint64_t off = head_probe_offset(v0, q, lane);
+      const int64_t col = v0 + 64 * q + lane;
+      CHECK(off == 4 * (uint64_t)col && off < (1ull << 32), "head probe copy offset %llu", (unsigned long long)off);
+      CHECK((col < V) == (off + 4 <= 4 * (uint64_t)V), "head probe column %lld against V", (long long)col);
+      CHECK(256 * q + 4 * lane < 1024, "head probe LDS byte");
+    }
+  CHECK(4 * (uint64_t)V < (1ull << 31), "head probe resource");
+  for (uint32_t lead : {0u, 2u}) {
+    const uint64_t bytes = head_bias_bytes(lead, V);
+    CHECK(bytes >= lead + 2 * (uint64_t)V && bytes < lead + 2 * (uint64_t)V + 4 && bytes % 4 == 0 && bytes < (1ull << 31),
+          "head bias resource of %llu bytes (lead %u)", (unsigned long long)bytes, lead);
+    for (int64_t c = v0; c < std::min<int64_t>(V, v0 + TN); ++c) {
+      const uint64_t at = lead + 2 * (uint64_t)c;  // byte of column c from the boundary
+      const uint64_t rel = lead + 2 * (uint64_t)(c - v0);  // and in the tile's words
+      CHECK(rel + 2 <= 1024, "head bias LDS read of column %lld", (long long)c);
+      const int d = (int)(rel / 4);  // the word holding it
+      const uint64_t woff = head_bias_word_offset(v0, d);
+      CHECK(woff <= at && at + 2 <= woff + 4 && woff + 4 <= bytes && d < 256,
+            "head bias column %lld (lead %u): word %d at %llu of %llu", (long long)c, lead, d,
+            (unsigned long long)woff, (unsigned long long)bytes);
+    }
+  }
+}
+
 // the sign-probe cache loads: the two words (32 k each, one per thread of a
 // column's pair) of K tile k0 of the parameter row n of a matrix at zoff (row
 // stride ldw), inside the bit_words(P) words of one probe
@@ -167,6 +224,7 @@ int main(int argc, char** argv) {
     check_copies(H, H, "gate h", kGeo8);
     for (int64_t mb = 0; mb < nm; ++mb) CHECK((mb + 1) * TM <= M, "gate row block %lld", (long long)mb);
     for (int64_t nb = 0; nb < nn; ++nb) {
+      if (l == 0) check_cell_copies(nb, H);
       check_b_loads(nb, 4 * H, El, "gate W_ih");
       check_b_loads(nb, 4 * H, H, "gate W_hh");
       // the sign words of every workgroup column (the gate column order)
@@ -188,6 +246,7 @@ int main(int argc, char** argv) {
   }
   for (int64_t vt = 0; vt < nvt; ++vt) {
     check_b_loads(vt, out_rows, H, "head W_out");
+    check_head_bias(vt, V);
     for (int rho = 0; rho < TN; ++rho) {
       const int64_t n = std::min<int64_t>(TN * vt + rho, V - 1);
       check_words(off_out, n, H, H, P, "head W_out");

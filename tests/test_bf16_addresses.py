@@ -1,8 +1,9 @@
 """Host replay of the bf16 kernels' operand addressing (no GPU): the
-activation copies into LDS and the fragment-packed B loads of every
-workgroup, wave, lane, copy and k step of the gate and head launches stay
-inside the buffer resources they are issued against, every offset fits in
-32 bits, the copies fill each LDS row and slot exactly once, and the packed
+activation copies into LDS, the fragment-packed B loads, the sign-probe
+cache loads, the gate's cell-state copies and the head's bias copies of
+every workgroup, wave, lane, copy and k step of the gate and head launches
+stay inside the buffer resources they are issued against, every offset fits
+in 32 bits, the copies fill each LDS row and slot exactly once, and the packed
 layout and the gate column order are bijections. The replay calls the same
 address functions as the kernels (paper_2505_17852_amd/csrc/zo_pack.hpp),
 built for the host by tests/helpers/bf16_addresses.cpp."""
