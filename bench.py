@@ -59,7 +59,7 @@ def kernel_source_hash(dtype):
     """Hash of the gate kernel's sources, to match the committed counter runs."""
     import hashlib
     src = os.path.join(ROOT, "paper_2505_17852_amd", "csrc")
-    files = ["k_forward_bf16.hip" if dtype == "bf16" else "k_forward.hip", "zo_rng.hpp", "zo_common.hpp"]
+    files = (["k_forward_bf16.hip", "zo_pack.hpp"] if dtype == "bf16" else ["k_forward.hip"]) + ["zo_rng.hpp", "zo_common.hpp"]
     m = hashlib.sha256()
     for f in files:
         with open(os.path.join(src, f), "rb") as fh:
