@@ -123,6 +123,8 @@ static_assert(2 * sizeof(lds_s0) <= 160 * 1024, "LDS");
 constexpr int kWordBytes = kVocabTileWide * 2 * 4;
 __shared__ __align__(16) uint8_t lds_words0[kWordBytes];
 __shared__ __align__(16) uint8_t lds_words1[kWordBytes];
+// Cached sign words: a ring of four tiles' words (tile t in buffer t % 4).
+__shared__ __align__(16) uint8_t lds_wring[4 * kWordBytes];
 
 // The gate's cell states c of its tile (TM rows x the TN / 4 hidden units of
 // its columns, row-major), fetched before the main loop so that the cell
@@ -302,9 +304,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int lr = lane & 31, lg = lane >> 5;
-  const int ks0 = s0.K / 16;
   const int ntiles = s0.K / TK + (nseg > 1 ? s1.K / TK : 0);
-  const int nsteps = ntiles * KSTEPS;
 
   // Buffer resources: the workgroup's activation rows and the packed matrices
   // of each segment (the probe cache per probe).
@@ -393,21 +393,25 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       }
     }
   };
-  // cached sign words: the WPT words of this thread's k of a tile, loaded
-  // one tile before issue_probe needs them (wseg, wk0: the next tile to
-  // load), into the buffer of the tile's parity (a register move would wait
-  // for the load)
+  // cached sign words: every thread reads the two words (64 k) of its column
+  // zn for one tile with one 8-byte load, two tiles per round: at each even
+  // tile it, thread (zn, zpart) loads tile it + 2 + zpart's words; at the
+  // following odd tile both tiles' words go, unshuffled, into the ring of
+  // four LDS buffers (tile t in buffer t % 4, rewritten two barriers after
+  // its tile was read)
   Rsrc rbits = rw0;
   if constexpr (T::kBits) rbits = make_rsrc(bits.words, bits.bytes);
-  int wseg = 0, wk0 = 0;
-  uint32_t wbuf[2][T::WPT] = {};
-  auto load_words = [&](uint32_t (&dst)[T::WPT]) {
-    const SegB& sg = wseg == 0 ? s0 : s1;
-    const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)wk0 + T::ZVALS * zpart;
-#pragma unroll
-    for (int i = 0; i < T::WPT; ++i)
-      dst[i] = __builtin_amdgcn_raw_buffer_load_b32(rbits, sign_word_offset(j0 + 32u * (uint64_t)i), 0, 0);
-    next_tile(wseg, wk0);
+  uint2 wq = {0u, 0u};
+  auto tile_words = [&](int ti) {
+    ti = ti < ntiles ? ti : ntiles - 1;  // past the last tile: its words again (never read)
+    const bool second = ti >= ntiles0;
+    const SegB& sg = second ? s1 : s0;
+    const uint64_t kt = (uint64_t)(second ? ti - ntiles0 : ti) * TK;
+    const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + kt;
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rbits, sign_word_offset(j0), 0, 0));
+  };
+  auto put_words = [&](int ti, uint2 w) {
+    *(uint2*)(lds_wring + (ti & 3) * kWordBytes + zr * 8) = uint2{unshuffle_bits(w.x), unshuffle_bits(w.y)};
   };
 
   // The next K tile's activation copies into stage S (the last loads of a
@@ -431,15 +435,13 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     constexpr int S = decltype(stage_tag)::value;
     const SegB& sg = seg == 0 ? s0 : s1;
     const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + (uint64_t)k0 + T::ZVALS * zpart;
-    if constexpr (T::kSigns) {
+    if constexpr (T::kSigns && !T::kBits) {
       const bool aligned = (sg.zoff % 128u) == 0 && (sg.ldw % 128) == 0;
 #pragma unroll
       for (int i = 0; i < T::WPT; ++i) {
         const uint64_t j = j0 + 32u * (uint64_t)i;
         uint32_t word;
-        if constexpr (T::kBits) {
-          word = wbuf[S][i];
-        } else if (aligned) {
+        if (aligned) {
           // one Philox block holds the words of 128 k
           if ((j & 127u) == 0 || i == 0) zcache = stream_block(key, j >> 7, probe, kTagRademacher);
           const int q = (int)((j >> 5) & 3u);
@@ -504,7 +506,12 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     if constexpr (T::kSigns) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const uint2 wd = *(const uint2*)(words4<S>() + w_lane + 32 * 8 * nt);
+        const uint8_t* wsrc;
+        if constexpr (T::kBits)
+          wsrc = lds_wring + (it & 3) * kWordBytes;
+        else
+          wsrc = words4<S>();
+        const uint2 wd = *(const uint2*)(wsrc + w_lane + 32 * 8 * nt);
         us[nt][0] = (wd.x ^ flip) >> lshift;
         us[nt][1] = (wd.y ^ flip) >> lshift;
       }
@@ -526,8 +533,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
       if (s == 0) {
         // the sign words two tiles ahead (cached), then the next tile's
         // activation copies, then this step's B loads
-        if constexpr (T::kBits) {
-          load_words(wbuf[S]);
+        if constexpr (T::kBits && S == 0) {
+          wq = tile_words(it + 2 + zpart);
           issue_fence();
         }
         issue_copies(next);
@@ -588,7 +595,10 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         }
         mma(wz);
       }
-      if (s == 2) issue_probe(next);
+      if (s == 2) {
+        if constexpr (T::kBits && S == 1) put_words(it + 1 + zpart, wq);
+        issue_probe(next);
+      }
     }
   };
 
@@ -599,8 +609,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // other stage. Prologue: the sign words of tiles 0 and 1 (cached), tile 0's
   // copies and probe part, the first DIST steps' B loads.
   if constexpr (T::kBits) {
-    load_words(wbuf[0]);
-    load_words(wbuf[1]);
+    wq = tile_words(zpart);
     issue_fence();
   }
   issue_copies(std::integral_constant<int, 0>{});
@@ -615,6 +624,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
         with_slot<KSTEPS>(g % KSTEPS, [&](auto step_tag) { load_b(slot_tag, step_tag, tb0[g / KSTEPS]); });
       });
   }
+  if constexpr (T::kBits) put_words(zpart, wq);
   issue_probe(std::integral_constant<int, 0>{});
   // loads issued after the copies of the tile a barrier waits for: the first
   // DIST steps' B loads (prologue), then a whole tile's B loads (every later

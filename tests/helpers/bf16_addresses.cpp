@@ -151,18 +151,23 @@ static void check_head_bias(int64_t vt, int64_t V) {
   }
 }
 
-// the sign-probe cache loads: the two words (32 k each, one per thread of a
-// column's pair) of K tile k0 of the parameter row n of a matrix at zoff (row
+// the sign-probe cache loads: the two words (32 k each; one 8-byte load by
+// one thread of the column's pair) of K tile k0 of the parameter row n of a matrix at zoff (row
 // stride ldw), inside the bit_words(P) words of one probe
 static void check_words(uint64_t zoff, int64_t n, int64_t ldw, int64_t K, uint64_t P, const char* what) {
   const uint64_t bytes = 4 * (4 * ((P + 127) / 128));
-  for (int64_t k0 : {(int64_t)0, K - TK})
+  for (int64_t k0 : {(int64_t)0, K - TK}) {
+    // one 8-byte load per thread and tile: both words, 8-byte aligned
+    const uint64_t jt = zoff + (uint64_t)n * (uint64_t)ldw + (uint64_t)k0;
+    CHECK(jt % 64 == 0 && sign_word_offset(jt) % 8 == 0, "%s: sign words of parameter %llu not 8-byte aligned", what,
+          (unsigned long long)jt);
     for (int i = 0; i < 2; ++i) {
       const uint64_t j = zoff + (uint64_t)n * (uint64_t)ldw + (uint64_t)k0 + 32u * (uint64_t)i;
       const uint64_t off = sign_word_offset(j);
       CHECK(j < P && off + 4 <= bytes && off == (j / 32) * 4, "%s: sign word of parameter %llu at %llu of %llu",
             what, (unsigned long long)j, (unsigned long long)off, (unsigned long long)bytes);
     }
+  }
 }
 
 int main(int argc, char** argv) {
