@@ -219,8 +219,9 @@ int zo_update(const zo_config* cfg, void* theta, uint64_t seed, float eps, float
  * probes can be stored as bits). A workspace of at least zo_workspace_bytes()
  * holds, at byte offset zo_probe_bits_offset(cfg, N, B, C), the sign words of
  * the call's probes i0 .. i0+N-1 over the whole of theta: probe n's word w at
- * n * 4 * ceil(P / 128) + w (uint32), bit b of word w set when
- * z_{i0+n}[32 w + b] = +1. zo_perturbed_losses writes it once per call and its
+ * n * 4 * ceil(P / 128) + w (uint32) holds the signs of parameters 32 w ..
+ * 32 w + 31, unshuffled: bit i set when z_{i0+n}[32 w + 2 i] = +1 and bit
+ * 16 + i when z_{i0+n}[32 w + 2 i + 1] = +1 (i < 16). zo_perturbed_losses writes it once per call and its
  * kernels read the words from it instead of regenerating them (the losses are
  * bit-identical either way); a smaller workspace regenerates them.
  * zo_probe_bits_offset returns 0 for shapes without the cache or invalid

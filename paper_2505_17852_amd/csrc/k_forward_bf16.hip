@@ -191,22 +191,6 @@ __device__ __forceinline__ void with_slot(int i, F&& f) {
   }
 }
 
-// The word of 32 consecutive sign flags with the even elements' flags moved
-// to bits 0..15 and the odd elements' to bits 16..31 (in order), so that the
-// two elements of one packed fp16 pair sit 16 bits apart.
-__device__ __forceinline__ uint32_t unshuffle_bits(uint32_t x) {
-  uint32_t t;
-  t = (x ^ (x >> 1)) & 0x22222222u;
-  x = x ^ t ^ (t << 1);
-  t = (x ^ (x >> 2)) & 0x0C0C0C0Cu;
-  x = x ^ t ^ (t << 2);
-  t = (x ^ (x >> 4)) & 0x00F000F0u;
-  x = x ^ t ^ (t << 4);
-  t = (x ^ (x >> 8)) & 0x0000FF00u;
-  x = x ^ t ^ (t << 8);
-  return x;
-}
-
 // A raw buffer resource over [base, base + bytes), bytes < 2^31.
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -396,8 +380,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // cached sign words: every thread reads the two words (64 k) of its column
   // zn for one tile with one 8-byte load, two tiles per round: at each even
   // tile it, thread (zn, zpart) loads tile it + 2 + zpart's words; at the
-  // following odd tile both tiles' words go, unshuffled, into the ring of
-  // four LDS buffers (tile t in buffer t % 4, rewritten two barriers after
+  // following odd tile both tiles' words (stored unshuffled in the cache) go
+  // into the ring of four LDS buffers (tile t in buffer t % 4, rewritten two barriers after
   // its tile was read)
   Rsrc rbits = rw0;
   if constexpr (T::kBits) rbits = make_rsrc(bits.words, bits.bytes);
@@ -410,9 +394,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     const uint64_t j0 = sg.zoff + (uint64_t)zn * (uint64_t)sg.ldw + kt;
     return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rbits, sign_word_offset(j0), 0, 0));
   };
-  auto put_words = [&](int ti, uint2 w) {
-    *(uint2*)(lds_wring + (ti & 3) * kWordBytes + zr * 8) = uint2{unshuffle_bits(w.x), unshuffle_bits(w.y)};
-  };
+  auto put_words = [&](int ti, uint2 w) { *(uint2*)(lds_wring + (ti & 3) * kWordBytes + zr * 8) = w; };
 
   // The next K tile's activation copies into stage S (the last loads of a
   // tile before its B loads: the count wait_and_barrier leaves in flight).
@@ -450,7 +432,7 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
           word = rademacher_word(key, probe, j >> 5);
         }
         // the word of column zr's 32 k at 32 (WPT zpart + i), unshuffled
-        *(uint32_t*)(words4<S>() + zr * 8 + (T::WPT * zpart + i) * 4) = unshuffle_bits(word);
+        *(uint32_t*)(words4<S>() + zr * 8 + (T::WPT * zpart + i) * 4) = sign_word_unshuffle(word);
       }
     } else if constexpr (T::kZTile) {
       uint8_t* zrow = stage<kind, S>() + T::ABytes + zr * T::RowBytes;

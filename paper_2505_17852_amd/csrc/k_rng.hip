@@ -205,12 +205,13 @@ __device__ __forceinline__ void decode_raw8(const Raw8<T>& r, float v[8]) {
 }
 
 // The 4 sign words of Philox block blk of probe n from the sign-probe cache
-// (layout: bit_words); zeros past the parameters, as their signs only ever
-// meet parameters that are not stored.
+// (layout: bit_words; its words are stored unshuffled, so they are shuffled
+// back into the generator's order); zeros past the parameters, as their signs
+// only ever meet parameters that are not stored.
 __device__ __forceinline__ Words cached_block(const uint32_t* bits, uint64_t P, int n, uint64_t blk) {
   if (blk >= (P + 127) / 128) return Words{{0u, 0u, 0u, 0u}};
   const uint4 v = *(const uint4*)(bits + (uint64_t)n * bit_words(P) + 4 * blk);
-  return Words{{v.x, v.y, v.z, v.w}};
+  return Words{{sign_word_shuffle(v.x), sign_word_shuffle(v.y), sign_word_shuffle(v.z), sign_word_shuffle(v.w)}};
 }
 
 // Workgroup barrier for LDS data only: waits for this thread's LDS accesses
@@ -638,14 +639,16 @@ struct TypeTag {
   using type = T;
 };
 
-// The sign-probe cache: probe n's Philox blocks (tag 0), 4 words each, at
-// n * bit_words(P) + 4 blk. One thread per block and probe.
+// The sign-probe cache: probe n's Philox blocks (tag 0), 4 words each,
+// unshuffled, at n * bit_words(P) + 4 blk. One thread per block and probe.
 __global__ __launch_bounds__(256) void bits_fill_kernel(uint32_t* bits, uint64_t P, Key key, uint32_t i0, int N) {
   const uint64_t nblk = (P + 127) / 128;
   for (int n = blockIdx.y; n < N; n += gridDim.y)
     for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nblk; b += (uint64_t)gridDim.x * blockDim.x) {
       const Words x = stream_block(key, b, i0 + (uint32_t)n, kTagRademacher);
-      *(uint4*)(bits + (uint64_t)n * bit_words(P) + 4 * b) = uint4{x.w[0], x.w[1], x.w[2], x.w[3]};
+      *(uint4*)(bits + (uint64_t)n * bit_words(P) + 4 * b) =
+          uint4{sign_word_unshuffle(x.w[0]), sign_word_unshuffle(x.w[1]), sign_word_unshuffle(x.w[2]),
+                sign_word_unshuffle(x.w[3])};
     }
 }
 

@@ -169,12 +169,43 @@ inline bool probe_cache_kind(const zo_config& c) { return c.probe == ZO_GAUSSIAN
 // Bit-packed sign-probe cache (bf16 weights with sign probes): the sign words
 // of probes i0 .. i0+N-1 over the whole parameter vector, written once per call
 // (one Philox block per 128 parameters and probe) and read by the forward
-// kernels in place of regenerating them in every K tile: probe n's word w
-// (the signs of parameters 32 w .. 32 w + 31, bit b set for z = +1) at
-// n * bit_words(P) + w. The update can read the same words
+// kernels in place of regenerating them in every K tile: probe n's word w, the
+// signs of parameters 32 w .. 32 w + 31 (a set bit for z = +1), at
+// n * bit_words(P) + w, unshuffled: parameter 32 w + 2 i at bit i and
+// 32 w + 2 i + 1 at bit 16 + i (sign_word_unshuffle of the generator's word),
+// the order in which the bf16 products turn a pair of flags into a packed
+// fp16 pair with one shift. The update can read the same words
 // (zo_update_cached) instead of regenerating them.
 inline bool bit_cache_kind(const zo_config& c) { return c.probe == ZO_RADEMACHER && c.wdtype == ZO_WBF16; }
 __host__ __device__ inline uint64_t bit_words(uint64_t P) { return (P + 127) / 128 * 4; }
+
+// A word of 32 flags with the even-indexed flags moved to bits 0..15 and the
+// odd-indexed ones to bits 16..31, each half in order (four delta swaps);
+// sign_word_shuffle is its inverse (the same swaps in reverse order).
+__host__ __device__ inline uint32_t sign_word_unshuffle(uint32_t x) {
+  uint32_t t;
+  t = (x ^ (x >> 1)) & 0x22222222u;
+  x = x ^ t ^ (t << 1);
+  t = (x ^ (x >> 2)) & 0x0C0C0C0Cu;
+  x = x ^ t ^ (t << 2);
+  t = (x ^ (x >> 4)) & 0x00F000F0u;
+  x = x ^ t ^ (t << 4);
+  t = (x ^ (x >> 8)) & 0x0000FF00u;
+  x = x ^ t ^ (t << 8);
+  return x;
+}
+__host__ __device__ inline uint32_t sign_word_shuffle(uint32_t x) {
+  uint32_t t;
+  t = (x ^ (x >> 8)) & 0x0000FF00u;
+  x = x ^ t ^ (t << 8);
+  t = (x ^ (x >> 4)) & 0x00F000F0u;
+  x = x ^ t ^ (t << 4);
+  t = (x ^ (x >> 2)) & 0x0C0C0C0Cu;
+  x = x ^ t ^ (t << 2);
+  t = (x ^ (x >> 1)) & 0x22222222u;
+  x = x ^ t ^ (t << 1);
+  return x;
+}
 
 // Kernel variants for normal probes read from the probe cache (fp16(eps z)
 // as a second operand stream; or, bf16 weights with fused products, the

@@ -170,6 +170,21 @@ static void check_words(uint64_t zoff, int64_t n, int64_t ldw, int64_t K, uint64
   }
 }
 
+// the sign-probe cache's word order: sign_word_unshuffle puts flag 2 i at
+// bit i and flag 2 i + 1 at bit 16 + i, and sign_word_shuffle undoes it
+static void check_word_order() {
+  uint64_t s = 0x9E3779B97F4A7C15ull;
+  for (int r = 0; r < 4096; ++r) {
+    s = s * 6364136223846793005ull + 1442695040888963407ull;
+    const uint32_t x = r < 32 ? (1u << r) : (uint32_t)(s >> 32);
+    uint32_t want = 0;
+    for (int b = 0; b < 32; ++b)
+      if (x >> b & 1u) want |= 1u << ((b >> 1) + 16 * (b & 1));
+    CHECK(sign_word_unshuffle(x) == want, "unshuffle of %08x", x);
+    CHECK(sign_word_shuffle(sign_word_unshuffle(x)) == x, "shuffle does not undo unshuffle of %08x", x);
+  }
+}
+
 int main(int argc, char** argv) {
   if (argc != 8) {
     std::printf("usage: bf16_addresses L V E H N B fd\n");
@@ -182,6 +197,7 @@ int main(int argc, char** argv) {
   const int64_t gran = fd ? 256 : 128;
   const int64_t Bp = (B + gran - 1) / gran * gran;
   const int64_t M = fd ? (N + 1) * Bp : 2 * N * Bp;
+  check_word_order();
   const int64_t nvt = (V + TN - 1) / TN;
   const int64_t out_rows = nvt * TN;
   CHECK(M % TM == 0, "rows %lld not a whole number of tiles", (long long)M);

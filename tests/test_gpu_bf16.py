@@ -270,7 +270,8 @@ SIGN_CACHE_CASES = [
 @pytest.mark.parametrize("name,cfg,N,B,C", SIGN_CACHE_CASES, ids=[c[0] for c in SIGN_CACHE_CASES])
 def test_sign_probe_cache(zo, oracle, name, cfg, N, B, C):
     """The bit-packed sign-probe cache (a workspace of zo_workspace_bytes):
-    its words are the oracle's probe signs; the losses read from it are
+    its words are the oracle's probe signs (in the stored, unshuffled bit
+    order); the losses read from it are
     bit-identical to the regenerating path (the smallest workspace), for
     central and forward differences and with the two-stream products; and
     the update reading the same words (zo_update_cached) gives theta bit for
@@ -299,7 +300,8 @@ def test_sign_probe_cache(zo, oracle, name, cfg, N, B, C):
     for n in range(N):
         for w0 in (0, wpp // 2 - 3, (P - 1) // 32 - 3):
             z = oracle.probe(wl.RADEMACHER, 303, 7 + n, 32 * w0, 96)
-            want = [int(sum(1 << b for b in range(32) if z[32 * q + b] > 0)) for q in range(3)]
+            # stored unshuffled: parameter 32 w + 2 i at bit i, 32 w + 2 i + 1 at bit 16 + i
+            want = [int(sum(1 << (b // 2 + 16 * (b % 2)) for b in range(32) if z[32 * q + b] > 0)) for q in range(3)]
             got = [int(x) for x in words[n * wpp + w0:n * wpp + w0 + 3]]
             assert got == want, (n, w0)
     t1, t2 = theta.clone(), theta.clone()
