@@ -18,7 +18,7 @@
 // acc += A . W; acc += A . (s eps z) is used instead (kSplit).
 //
 // Tiles: a workgroup of 8 waves computes TM rows x TN columns, TM x TN =
-// 65536 (TN = kVocabTileWide: 128 x 512, or 256 x 256); its waves split the
+// 65536 (TN = kVocabTileWide, 256: 256 x 256); its waves split the
 // columns into TN / 64 wave columns and the rows into 8 / (TN / 64) wave
 // rows, each wave computing 128 rows x 64 columns (4 x 2 tiles of 32x32 MFMA
 // output). Two waves share each SIMD, so one wave's loads, probe expansion
@@ -36,8 +36,10 @@
 // sized to its matrix (or to the workgroup's activation rows), so an offset
 // outside it reads zeros rather than faulting. The probe term: sign probes as
 // two words of sign flags per column and K tile (regenerated, one Philox word
-// per 32 k, or read from the sign-probe cache) in a small LDS array of their
-// own, which every lane expands into +-fp16(eps) fragments in registers;
+// per 32 k, or read from the sign-probe cache, one 8-byte load per thread
+// for both words of a tile, into a ring of tile buffers) in a small LDS
+// array of their own, which every lane expands into +-fp16(eps) fragments in
+// registers;
 // normal probes regenerated into an LDS tile per K tile, or read from the
 // probe cache: with the fused form as the pass's perturbed weights
 // fp16(W + s eps z), written once per call and loaded as the only B operand,
@@ -855,7 +857,10 @@ __global__ __launch_bounds__(NT, 1) void head_bf16_kernel(HeadArgsB g) {
   // the tile's bias values into LDS (waves 0-3: eps z of the bias, one column
   // per lane; waves 4-7: the bf16 bias as 4-byte words from the aligned
   // boundary; columns past V read zeros). Issued before the loop's first
-  // loads: its first barrier waits for them.
+  // loads: its first barrier waits for them. The word resource spans the
+  // 4-byte words that hold the V bias values: at most 2 bytes before the
+  // first and 2 after the last, inside those aligned words, so inside the
+  // pages that hold theta.
   const uintptr_t bias_at = (uintptr_t)(g.theta + g.off_b);
   const uint32_t bias_lead = (uint32_t)(bias_at & 3u);  // 0 or 2 bytes before the first element
   {
