@@ -87,10 +87,10 @@ struct Tiles {
   static constexpr int ACopies = ABytes / 1024 / NWAVES;  // activation copies per wave and tile
   // B fragments for k step s + DIST are loaded at step s, into SLOTS rotating
   // register sets, as far ahead as the registers of two waves per SIMD allow
-  // without spilling (the cached normal probe doubles the loads; regenerated
-  // probes hold the generator's state): cached sign probes 7 k steps (c4 gate
-  // 2.25 -> 2.18 ms against 3), the others 3 (c3 gate 0.90 -> 0.74 ms
-  // against 1).
+  // without spilling (fp16(eps z) as a second stream doubles the loads;
+  // regenerated probes hold the generator's state): cached sign probes and
+  // the perturbed-weight cache 7 k steps (c4 gate 2.25 -> 2.18 ms against 3),
+  // the others 3 (c3 gate with fp16(eps z) streamed 0.90 -> 0.74 ms against 1).
   static constexpr bool kPerturbed = kind == kGaussPerturbed;  // B is the cached fp16(W + s eps z) itself
   static constexpr int DIST = kBits || kPerturbed ? 7 : 3;
   static constexpr int SLOTS = DIST < 4 ? 4 : 8;  // a divisor of the two K tiles the loop body spans
@@ -110,8 +110,9 @@ static_assert(2 * kRowGranuleBF16 % TM == 0, "a probe's rows must be a whole num
 static_assert(TM % 128 == 0 && TM * kVocabTileWide == 65536, "workgroup tile");
 
 // LDS stages (static, so that every offset is a constant): activation tile
-// and probe tile (sign and regenerated normal probes), or the activation tile
-// alone (cached normal probes).
+// and probe tile (regenerated normal probes), or the activation tile alone
+// (sign probes, whose words have arrays of their own, and cached normal
+// probes).
 __shared__ __align__(16) uint8_t lds_s0[Tiles<ZO_GAUSSIAN>::StageBytes];
 __shared__ __align__(16) uint8_t lds_s1[Tiles<ZO_GAUSSIAN>::StageBytes];
 __shared__ __align__(16) uint8_t lds_c0[Tiles<kGaussCached>::StageBytes];
@@ -383,8 +384,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // zn for one tile with one 8-byte load, two tiles per round: at each even
   // tile it, thread (zn, zpart) loads tile it + 2 + zpart's words; at the
   // following odd tile both tiles' words (stored unshuffled in the cache) go
-  // into the ring of four LDS buffers (tile t in buffer t % 4, rewritten two barriers after
-  // its tile was read)
+  // into the ring of four LDS buffers (tile t in buffer t % 4, rewritten two
+  // barriers after its tile was read)
   Rsrc rbits = rw0;
   if constexpr (T::kBits) rbits = make_rsrc(bits.words, bits.bytes);
   uint2 wq = {0u, 0u};
@@ -515,8 +516,8 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
     for (int s = 0; s < KSTEPS; ++s) {
       const Frag& c = f[s & 1];
       if (s == 0) {
-        // the sign words two tiles ahead (cached), then the next tile's
-        // activation copies, then this step's B loads
+        // the sign words of the next round's two tiles (cached, even tiles),
+        // then the next tile's activation copies, then this step's B loads
         if constexpr (T::kBits && S == 0) {
           wq = tile_words(it + 2 + zpart);
           issue_fence();
@@ -590,8 +591,9 @@ __device__ __forceinline__ void mainloop_bf16(f16v (&acc)[Tiles<kind>::MT][2], c
   // copies of tile it (the B loads issued after them may stay in flight) and
   // its LDS writes; barrier (tile it complete for every wave, and the stage
   // computed at it - 1 free); compute it while issuing tile it + 1 into the
-  // other stage. Prologue: the sign words of tiles 0 and 1 (cached), tile 0's
-  // copies and probe part, the first DIST steps' B loads.
+  // other stage. Prologue: the sign words of tiles 0 and 1 (cached, put into
+  // the ring after the B loads are issued), tile 0's copies and probe part,
+  // the first DIST steps' B loads.
   if constexpr (T::kBits) {
     wq = tile_words(zpart);
     issue_fence();
